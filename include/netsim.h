@@ -1,0 +1,261 @@
+/*
+ * netsim -- flow-level network simulator with max-min fair bandwidth
+ * sharing, solved on an AMD Instinct MI355X (gfx950).
+ *
+ * What is computed (the communication-time model of the paper's simulator:
+ * Section 4.1, the "netsim" description, and Section 4.2, "Network
+ * simulator with time rollback"):
+ *   - collectives are decomposed into point-to-point flows over a cluster
+ *     topology (ring all-reduce / reduce-scatter / all-gather as NCCL's ring
+ *     would run them, all-to-all, pipeline send/recv);
+ *   - each flow follows one route chosen by the topology's multipath
+ *     (ECMP) rule;
+ *   - at every instant the rates of the active flows are their max-min fair
+ *     (per-flow fair) allocation over the link capacities, and stay constant
+ *     between consecutive events;
+ *   - an event loop advances simulated time to the next flow arrival or
+ *     completion and re-solves the rates; the output is every flow's
+ *     completion time.
+ *
+ * Conventions for every entry point:
+ *   - Units: bytes, seconds, bytes per second.
+ *   - Pointers are host pointers unless the name says "device".  The caller
+ *     owns every array it passes; the library copies what it keeps before
+ *     the call returns.  Outputs go to caller-provided buffers.
+ *   - Every call returns a netsim_status and never aborts.  On failure the
+ *     handle is unchanged and netsim_last_error() describes the problem.
+ *   - A handle is not thread-safe; distinct handles may be used from
+ *     distinct threads.
+ *   - Flow ids are assigned consecutively from 0 in the order flows are
+ *     added (across all scenarios of the handle).
+ *   - Link ids passed in or out are local to their scenario: 0 .. L_s-1.
+ */
+#ifndef NETSIM_H
+#define NETSIM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct netsim netsim_t;
+typedef int32_t netsim_status;
+
+enum {
+  NETSIM_OK = 0,
+  NETSIM_E_INVALID = -1, /* bad argument (NULL, out of range, non-finite, ...) */
+  NETSIM_E_NOMEM = -2,   /* host or device allocation failed                  */
+  NETSIM_E_DEVICE = -3,  /* HIP error, or the device solver reported a fault  */
+  NETSIM_E_STATE = -4,   /* call not allowed in the handle's current state    */
+  NETSIM_E_LIMIT = -5    /* a size limit or the per-solve round watchdog      */
+};
+
+/* Built-in fabrics (netsim_topology.kind). */
+enum { NETSIM_TOPO_LEAF_SPINE = 1, NETSIM_TOPO_RAIL = 2, NETSIM_TOPO_FAT_TREE = 3 };
+/* Ring collectives (netsim_add_ring kind). */
+enum { NETSIM_RING_ALLREDUCE = 0, NETSIM_RING_REDUCE_SCATTER = 1, NETSIM_RING_ALL_GATHER = 2 };
+/* Ring decomposition (netsim_add_ring mode). */
+enum { NETSIM_MODE_CHAINED = 0, NETSIM_MODE_FLAT = 1, NETSIM_MODE_AGGREGATED = 2 };
+/* Execution layout (netsim_options.exec). */
+enum {
+  NETSIM_EXEC_AUTO = 0,  /* block per scenario when batched or small, else grid */
+  NETSIM_EXEC_GRID = 1,  /* whole GPU on one scenario at a time (grid barriers)  */
+  NETSIM_EXEC_BLOCK = 2  /* one workgroup per scenario (workgroup barriers)      */
+};
+
+typedef struct {
+  int32_t device;            /* HIP device ordinal                               */
+  int32_t exec;              /* NETSIM_EXEC_*                                    */
+  int64_t max_events;        /* stop each scenario after this many events; 0 = no limit */
+  double until;              /* do not process events later than this time (s); +inf = none */
+  int32_t max_rounds;        /* per-solve round watchdog; 0 = number of flows + 1 */
+  int32_t block_threads;     /* threads per workgroup in block mode; 0 = 1024    */
+} netsim_options;
+
+/*
+ * Built-in fabric.  Directed links; a cable is two links at full rate.
+ * Inside a server every ordered GPU pair has its own link (nvlink_Bps).
+ *   LEAF_SPINE: servers_per_leaf servers per leaf; every GPU has a NIC to its
+ *               leaf; every leaf has one cable to each of `spines` spines.
+ *   RAIL:       rail-optimised: local GPU g of the servers_per_leaf servers
+ *               of a group attaches to leaf (g, group); leaves as above.
+ *   FAT_TREE:   pods x (edges_per_pod edge + aggs_per_pod aggregation
+ *               switches); servers_per_leaf servers per edge switch
+ *               (servers = pods*edges_per_pod*servers_per_leaf); each edge has
+ *               one cable to every aggregation switch of its pod; aggregation
+ *               switch a has agg_uplinks cables to cores a*agg_uplinks + u.
+ * Link numbering: intra-server links first (server s, pair i->j:
+ *   s*G*(G-1) + i*(G-1) + (j<i ? j : j-1)), then cable c gives links
+ *   NV+2c (upwards) and NV+2c+1 (downwards).  Cables: the NIC of GPU h is
+ *   cable h; LEAF_SPINE/RAIL leaf-spine cables N + leaf*spines + spine
+ *   (RAIL leaf = g*groups + group); FAT_TREE edge-agg cables
+ *   N + (pod*E + e)*A + a, then agg-core cables N + P*E*A + (pod*A + a)*U + u.
+ * Routes: same server -> its one link; same leaf/edge -> NIC up, NIC down;
+ *   otherwise up through the tiers and down again, picking the spine (or
+ *   aggregation switch a = h mod A and core uplink u = (h / A) mod U) from
+ *   h = mix(mix(ecmp_seed) ^ (src << 32 | dst)), mix = SplitMix64's output
+ *   function.
+ * degraded_cables (num_degraded entries, may be NULL when 0): cable ids whose
+ * two links run at degraded_Bps.  Copied by netsim_create_topology.
+ */
+typedef struct {
+  int32_t kind;
+  int32_t servers;
+  int32_t gpus_per_server;
+  int32_t servers_per_leaf;
+  int32_t spines;
+  int32_t pods;
+  int32_t edges_per_pod;
+  int32_t aggs_per_pod;
+  int32_t agg_uplinks;
+  int32_t reserved;
+  double nvlink_Bps;
+  double nic_Bps;
+  double fabric_Bps;
+  uint64_t ecmp_seed;
+  int64_t num_degraded;
+  const int64_t* degraded_cables;
+  double degraded_Bps;
+} netsim_topology;
+
+typedef struct {
+  int64_t events;            /* event-loop iterations (arrivals/completions)    */
+  int64_t solves;            /* max-min rate solves                              */
+  int64_t rounds;            /* freezing rounds over all solves                  */
+  int64_t flows_swept;       /* sum over rounds of unfrozen flows visited        */
+  int64_t incidences_swept;  /* sum over rounds of their flow-link incidences    */
+  int64_t active_swept;      /* sum over events of active flows visited          */
+  int64_t pending_swept;     /* sum over events of pending flows visited         */
+  int64_t completed_flows;   /* flows with a finish time                         */
+  int32_t complete;          /* 1 if every scenario ran to its end               */
+  int32_t reserved;
+  double sim_time;           /* largest simulated time reached over scenarios    */
+  double device_seconds;     /* device time of the last netsim_run (HIP events)  */
+  double upload_seconds;     /* host->device preparation of the last run          */
+} netsim_stats;
+
+/* Fills *opt with the defaults (device 0, auto layout, no limits). */
+void netsim_default_options(netsim_options* opt);
+
+/*
+ * Explicit topology: num_scenarios independent scenarios; scenario s owns
+ * links link_off[s] .. link_off[s+1]-1 of capacity_Bps (link_off has S+1
+ * entries, link_off[0] = 0, non-decreasing).  Capacities must be finite and
+ * > 0.  opt may be NULL (defaults).  Flows must then carry explicit paths.
+ * No device work happens until netsim_run.
+ */
+netsim_status netsim_create(netsim_t** out, int32_t num_scenarios, const int64_t* link_off,
+                            const double* capacity_Bps, const netsim_options* opt);
+
+/* Built-in fabrics, one per scenario (topos[num_scenarios]). */
+netsim_status netsim_create_topology(netsim_t** out, int32_t num_scenarios,
+                                     const netsim_topology* topos, const netsim_options* opt);
+
+/* Number of links of scenario scen, and their capacities (cap_out[L_s], may be NULL). */
+netsim_status netsim_get_links(const netsim_t* h, int32_t scen, int64_t* num_links,
+                               double* cap_out);
+
+/*
+ * Appends n flows to scenario scen.  Flow i: endpoints src[i] -> dst[i]
+ * (GPU ranks; may be NULL when paths are given), nbytes[i] >= 0, start[i] >= 0.
+ * Path: if path_off is NULL the built-in router chooses it from (src, dst);
+ * otherwise flow i crosses links path_link[path_off[i] .. path_off[i+1]-1]
+ * (path_off[0] = 0, n+1 entries, local link ids, no link twice).
+ * Dependencies (dep_off may be NULL = none): flow i waits for the flows
+ * dep_ids[dep_off[i] .. dep_off[i+1]-1], ids of earlier flows of the same
+ * scenario (which keeps the graph acyclic).  A flow with no dependencies
+ * is released at start[i]; one with dependencies at start[i] + the latest
+ * finish time among them.  A zero-byte flow takes no route and finishes at
+ * its release time (a barrier).  bytes > 0 with src == dst or with an
+ * empty path is invalid.  *first_id (may be NULL) receives the first id.
+ */
+netsim_status netsim_add_flows(netsim_t* h, int32_t scen, int64_t n, const int32_t* src,
+                               const int32_t* dst, const double* nbytes, const double* start,
+                               const int64_t* path_off, const int32_t* path_link,
+                               const int64_t* dep_off, const int64_t* dep_ids,
+                               int64_t* first_id);
+
+/*
+ * Ring collective over ranks[0..p) (distinct, p >= 2) of `nbytes` in total
+ * on a built-in fabric (Section 4.1: all-reduce as NCCL's ring).  Steps:
+ * 2(p-1) for all-reduce, p-1 for reduce-scatter / all-gather; in every step
+ * position i sends nbytes/p (fp64 division) from ranks[i] to ranks[(i+1)%p].
+ * CHAINED: step k out of position i waits for step k-1 into position i;
+ * FLAT: all steps released together; AGGREGATED: one flow per ring edge of
+ * steps*(nbytes/p).  Flows are numbered step-major (first + k*p + i).  The
+ * first step (every flow, when not chained) waits for the n_after flows in
+ * after[] and then `lag` seconds.  *first_id and *count may be NULL.
+ */
+netsim_status netsim_add_ring(netsim_t* h, int32_t scen, int32_t kind, int32_t mode, int32_t p,
+                              const int32_t* ranks, double nbytes, double lag, int64_t n_after,
+                              const int64_t* after, int64_t* first_id, int64_t* count);
+
+/*
+ * All-to-all among ranks[0..p) (distinct): flow (i, j), j != i, carries
+ * nbytes[i*p + j] (row-major p x p; the diagonal is ignored), numbered
+ * row-major skipping the diagonal.  Every flow waits for after[] then lag.
+ */
+netsim_status netsim_add_all_to_all(netsim_t* h, int32_t scen, int32_t p, const int32_t* ranks,
+                                    const double* nbytes, double lag, int64_t n_after,
+                                    const int64_t* after, int64_t* first_id, int64_t* count);
+
+/* Totals over all scenarios: flows, path incidences, dependency entries. */
+netsim_status netsim_counts(const netsim_t* h, int64_t* num_flows, int64_t* num_incidences,
+                            int64_t* num_deps);
+
+/*
+ * Copies the flows as stored (id order): scenario, endpoints, bytes, start,
+ * path CSR (local link ids) and dependency CSR.  Any pointer may be NULL.
+ * Sizes: num_flows (+1 for the offsets), num_incidences, num_deps.
+ */
+netsim_status netsim_export_flows(const netsim_t* h, int32_t* scen, int32_t* src, int32_t* dst,
+                                  double* nbytes, double* start, int64_t* path_off,
+                                  int32_t* path_link, int64_t* dep_off, int64_t* dep_ids);
+
+/* Replaces the stopping points of later runs (see netsim_options). */
+netsim_status netsim_set_limits(netsim_t* h, int64_t max_events, double until);
+
+/*
+ * Simulates every scenario from t = 0 on the device, in one kernel launch
+ * (the event loop and the rate solves stay on the GPU).  hip_stream may be
+ * NULL (the default stream) or a hipStream_t, e.g. torch.cuda's current
+ * stream.  Blocks until the run is done.  May be called again: every call
+ * starts over from t = 0 with the same flows.  No flows can be added after
+ * the first run (NETSIM_E_STATE).
+ */
+netsim_status netsim_run(netsim_t* h, void* hip_stream);
+
+/*
+ * finish[num_flows] (host) receives each flow's completion time (NaN for a
+ * flow not finished when the run stopped early); makespan[num_scenarios]
+ * (may be NULL) each scenario's largest finish time.  Needs a prior run.
+ */
+netsim_status netsim_get_finish(const netsim_t* h, double* finish, double* makespan);
+
+/* Same as netsim_get_finish, into device memory d_finish[num_flows]. */
+netsim_status netsim_get_finish_device(const netsim_t* h, double* d_finish);
+
+netsim_status netsim_get_stats(const netsim_t* h, netsim_stats* stats);
+
+/*
+ * One rate solve (Section 4.2: the max-min allocation of the flows active
+ * at one instant) of the flows active_ids[0..n_active) of scenario scen,
+ * ignoring their start times and dependencies.  rates_out[n_active] (host)
+ * receives their rates.  Ids must be distinct flows of that scenario with
+ * a non-empty path.
+ */
+netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active,
+                                const int64_t* active_ids, double* rates_out);
+
+/* Message of the last failure on h (or of the calling thread when h is NULL). */
+const char* netsim_last_error(const netsim_t* h);
+
+/* Frees the handle and its device memory; NULL is ignored. */
+void netsim_destroy(netsim_t* h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NETSIM_H */

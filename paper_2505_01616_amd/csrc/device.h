@@ -1,0 +1,87 @@
+// Internal interface between the host side of libnetsim and its HIP kernels.
+// Not part of the public C ABI (include/netsim.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace netsim_dev {
+
+// Per-scenario control block in device memory.  The host fills the ranges
+// and the initial counters; the kernels keep their list counters here and
+// write the results back at the end of the run.
+struct ScenCtl {
+  int32_t f0, f1;          // device flow range [f0, f1)
+  int32_t l0, l1;          // device link range [l0, l1)
+  int32_t n_pend0;         // flows initially pending (listed in pend0 + f0)
+  int32_t n_solve;         // solve-once: active flows listed in act0 + f0
+  // results
+  double t;                // simulated time reached
+  int64_t events, solves, rounds, flows_swept, incidences_swept;
+  int64_t active_swept, pending_swept;
+  int32_t status;          // 0 ran to the end, 1 stopped at a limit, < 0 fault
+  int32_t fault_info;
+  // list counters (kernel scratch; zero at launch)
+  int32_t cnt_act[2];
+  int32_t cnt_pend[2];
+  int32_t cnt_comp[3];
+  int32_t cnt_unf[2];
+  int32_t changed[2];
+  int32_t pad;
+};
+
+enum : int32_t {
+  ST_DONE = 0,
+  ST_STOPPED = 1,
+  ST_BAD_SHARE = -3,       // non-positive or non-finite fair share
+  ST_ROUNDS = -5,          // round watchdog
+  ST_BARRIER = -6,         // grid barrier timed out
+  ST_OVERFLOW = -7         // a work list exceeded its capacity
+};
+
+struct Params {
+  int32_t num_scen;
+  int32_t mode;            // 0 event loop, 1 one rate solve per scenario
+  int64_t max_events;      // 0 = no limit
+  double until;
+  int32_t max_rounds;
+  int32_t pad;
+  double scale;            // fixed-point units per B/s (a power of two)
+  double inv_scale;
+  // static flow / link data (device order)
+  const int32_t* poff;     // [F+1] path offsets
+  const int32_t* plink;    // [nnz] device link ids
+  const double* nbytes;    // [F]
+  const double* start;     // [F]
+  const int32_t* soff;     // [F+1] successor offsets
+  const int32_t* succ;     // [nsucc]
+  const int64_t* R0;       // [L] capacity in fixed point
+  // dynamic flow state
+  double* rem;             // [F] bytes left (active flows)
+  double* rate;            // [F] current rate
+  double* finish;          // [F] completion time (NaN until finished)
+  double* mf;              // [F] smallest fair share on the path (current round)
+  double* rel;             // [F] release time (pending flows)
+  int32_t* cnt;            // [F] predecessors not yet finished
+  // dynamic link state
+  int64_t* Rres;           // [L] residual capacity (fixed point) during a solve
+  int32_t* nres;           // [L] unfrozen flows during a solve
+  int32_t* nact;           // [L] active flows
+  uint8_t* blocked0;       // [L] round flags (two, alternating)
+  uint8_t* blocked1;
+  // work lists, each [F], used per scenario on [f0, f1)
+  int32_t* act0; int32_t* act1;
+  int32_t* pend0; int32_t* pend1;
+  int32_t* comp0; int32_t* comp1; int32_t* comp2;
+  int32_t* unf0; int32_t* unf1;
+  ScenCtl* ctl;            // [num_scen]
+  uint32_t* bar;           // grid barrier: [0] arrivals, [1] generation, [2] abort
+  uint64_t* slots;         // grid min-reduction slots [4]
+};
+
+hipError_t launch_block(const Params& p, int blocks, int threads, hipStream_t s);
+hipError_t launch_grid(const Params& p, int blocks, int threads, hipStream_t s);
+// Largest co-resident grid for launch_grid at `threads` per block.
+hipError_t grid_capacity(int device, int threads, int* blocks);
+
+}  // namespace netsim_dev

@@ -1,0 +1,820 @@
+// libnetsim: the C ABI of include/netsim.h (host side).
+//
+// Host work: argument validation, built-in fabrics and ECMP routes,
+// decomposition of ring and all-to-all collectives into flows (Section 4.1:
+// collectives as communication patterns, all-reduce as NCCL's ring), the
+// device layout (flows grouped by scenario, links compacted to the used
+// ones, successor lists, fixed-point capacities), upload, one kernel launch
+// per run, and results.  Every step of the simulation itself runs in the
+// HIP kernels (kernels.hip).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <string>
+#include <vector>
+
+#include "device.h"
+#include "fabric.h"
+#include "netsim.h"
+
+using netsim_dev::Params;
+using netsim_dev::ScenCtl;
+
+namespace {
+
+thread_local std::string g_thread_err;
+
+struct Scen {
+  std::vector<double> cap;
+  bool has_fabric = false;
+  netsim_host::Fabric fab;
+  std::vector<int64_t> flows;  // ids of this scenario's flows, ascending
+};
+
+}  // namespace
+
+struct netsim {
+  netsim_options opt{};
+  std::vector<Scen> scen;
+  // flows in id order
+  std::vector<int32_t> f_scen, f_src, f_dst;
+  std::vector<double> f_bytes, f_start;
+  std::vector<int64_t> p_off{0};
+  std::vector<int32_t> p_link;
+  std::vector<int64_t> d_off{0};
+  std::vector<int64_t> d_ids;
+  std::string err;
+  // device layout (built at the first run)
+  bool prepared = false;
+  bool has_result = false;
+  int64_t F = 0, L = 0, nnz = 0, nsucc = 0;
+  std::vector<int32_t> dev_of_flow;   // id -> device flow index
+  std::vector<int32_t> link_base;     // scenario -> first device link
+  std::vector<std::vector<int32_t>> dev_link;  // scenario, local link -> device link (-1 unused)
+  std::vector<int32_t> h_cnt0;
+  std::vector<double> h_rel0;
+  std::vector<int32_t> h_pend0;
+  std::vector<ScenCtl> h_ctl0;
+  double scale = 1.0;
+  void* d_block = nullptr;            // one allocation holding every device array
+  Params prm{};
+  // results
+  std::vector<double> finish;         // id order
+  std::vector<double> makespan;
+  netsim_stats stats{};
+};
+
+namespace {
+
+netsim_status fail(const netsim_t* h, netsim_status code, const std::string& msg) {
+  if (h) const_cast<netsim_t*>(h)->err = msg;
+  else g_thread_err = msg;
+  return code;
+}
+
+bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0.0; }
+
+netsim_status hip_fail(const netsim_t* h, hipError_t e, const char* what) {
+  return fail(h, NETSIM_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Validates and appends n flows (all or nothing).  paths: explicit CSR or
+// NULL (route with the scenario's fabric).  deps: CSR of earlier ids or NULL.
+netsim_status add_flows_impl(netsim_t* h, int32_t s, int64_t n, const int32_t* src,
+                             const int32_t* dst, const double* nbytes, const double* start,
+                             const int64_t* path_off, const int32_t* path_link,
+                             const int64_t* dep_off, const int64_t* dep_ids, int64_t* first_id) {
+  if (h->prepared) return fail(h, NETSIM_E_STATE, "add_flows: flows cannot be added after a run");
+  if (s < 0 || s >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "add_flows: bad scenario");
+  if (n < 0) return fail(h, NETSIM_E_INVALID, "add_flows: n < 0");
+  if (n > 0 && (!nbytes || !start)) return fail(h, NETSIM_E_INVALID, "add_flows: nbytes and start are required");
+  Scen& sc = h->scen[s];
+  const int64_t first = (int64_t)h->f_bytes.size();
+  if (first + n > std::numeric_limits<int32_t>::max())
+    return fail(h, NETSIM_E_LIMIT, "add_flows: more than 2^31-1 flows");
+  const bool routed = path_off == nullptr;
+  if (routed) {
+    if (!sc.has_fabric) return fail(h, NETSIM_E_INVALID, "add_flows: no paths given and the scenario has no built-in fabric");
+    if (n > 0 && (!src || !dst)) return fail(h, NETSIM_E_INVALID, "add_flows: src and dst are required for routing");
+  } else {
+    if (!path_link && n > 0 && path_off[n] > 0) return fail(h, NETSIM_E_INVALID, "add_flows: path_link is NULL");
+    if (n > 0 && path_off[0] != 0) return fail(h, NETSIM_E_INVALID, "add_flows: path_off[0] must be 0");
+  }
+  if (dep_off && n > 0 && dep_off[0] != 0) return fail(h, NETSIM_E_INVALID, "add_flows: dep_off[0] must be 0");
+  if (dep_off && n > 0 && dep_off[n] > 0 && !dep_ids) return fail(h, NETSIM_E_INVALID, "add_flows: dep_ids is NULL");
+  const int64_t L = (int64_t)sc.cap.size();
+  const int64_t N = sc.has_fabric ? sc.fab.endpoints() : 0;
+  std::vector<int32_t> links;
+  std::vector<int64_t> lens((size_t)n, 0);
+  int32_t hop[netsim_host::Fabric::kMaxHops];
+  for (int64_t i = 0; i < n; ++i) {
+    const double b = nbytes[i];
+    if (!finite_nonneg(b)) return fail(h, NETSIM_E_INVALID, "add_flows: bytes must be finite and >= 0 (flow " + std::to_string(i) + ")");
+    if (!finite_nonneg(start[i])) return fail(h, NETSIM_E_INVALID, "add_flows: start must be finite and >= 0 (flow " + std::to_string(i) + ")");
+    if (dep_off) {
+      if (dep_off[i + 1] < dep_off[i]) return fail(h, NETSIM_E_INVALID, "add_flows: dep_off must not decrease");
+      for (int64_t k = dep_off[i]; k < dep_off[i + 1]; ++k) {
+        const int64_t d = dep_ids[k];
+        if (d < 0 || d >= first + i) return fail(h, NETSIM_E_INVALID, "add_flows: a dependency must name an earlier flow (flow " + std::to_string(i) + ")");
+        if (d >= first) {
+          // same batch: same scenario by construction
+        } else if (h->f_scen[(size_t)d] != s) {
+          return fail(h, NETSIM_E_INVALID, "add_flows: a dependency must be in the same scenario");
+        }
+      }
+    }
+    if (routed) {
+      if (b == 0.0) continue;  // zero-byte flows take no route
+      const int64_t a = src[i], c = dst[i];
+      if (a < 0 || a >= N || c < 0 || c >= N) return fail(h, NETSIM_E_INVALID, "add_flows: endpoint out of range (flow " + std::to_string(i) + ")");
+      if (a == c) return fail(h, NETSIM_E_INVALID, "add_flows: src == dst with bytes > 0 (flow " + std::to_string(i) + ")");
+      const int k = sc.fab.route(a, c, hop);
+      lens[(size_t)i] = k;
+      links.insert(links.end(), hop, hop + k);
+    } else {
+      if (path_off[i + 1] < path_off[i]) return fail(h, NETSIM_E_INVALID, "add_flows: path_off must not decrease");
+      const int64_t e0 = path_off[i], e1 = path_off[i + 1];
+      if (b == 0.0) continue;
+      if (e1 == e0) return fail(h, NETSIM_E_INVALID, "add_flows: empty path with bytes > 0 (flow " + std::to_string(i) + ")");
+      if (src && dst && src[i] >= 0 && src[i] == dst[i]) return fail(h, NETSIM_E_INVALID, "add_flows: src == dst with bytes > 0");
+      for (int64_t e = e0; e < e1; ++e) {
+        const int32_t l = path_link[e];
+        if (l < 0 || l >= L) return fail(h, NETSIM_E_INVALID, "add_flows: link id out of range (flow " + std::to_string(i) + ")");
+        for (int64_t e2 = e0; e2 < e; ++e2)
+          if (path_link[e2] == l) return fail(h, NETSIM_E_INVALID, "add_flows: link repeated in a path (flow " + std::to_string(i) + ")");
+      }
+      lens[(size_t)i] = e1 - e0;
+      links.insert(links.end(), path_link + e0, path_link + e1);
+    }
+  }
+  if ((int64_t)h->p_link.size() + (int64_t)links.size() > std::numeric_limits<int32_t>::max())
+    return fail(h, NETSIM_E_LIMIT, "add_flows: more than 2^31-1 path incidences");
+  // commit
+  for (int64_t i = 0; i < n; ++i) {
+    h->f_scen.push_back(s);
+    h->f_src.push_back(src ? src[i] : -1);
+    h->f_dst.push_back(dst ? dst[i] : -1);
+    h->f_bytes.push_back(nbytes[i]);
+    h->f_start.push_back(start[i]);
+    h->p_off.push_back(h->p_off.back() + lens[(size_t)i]);
+    if (dep_off) {
+      for (int64_t k = dep_off[i]; k < dep_off[i + 1]; ++k) h->d_ids.push_back(dep_ids[k]);
+      h->d_off.push_back(h->d_off.back() + (dep_off[i + 1] - dep_off[i]));
+    } else {
+      h->d_off.push_back(h->d_off.back());
+    }
+    sc.flows.push_back(first + i);
+  }
+  h->p_link.insert(h->p_link.end(), links.begin(), links.end());
+  if (first_id) *first_id = first;
+  return NETSIM_OK;
+}
+
+netsim_status check_after(netsim_t* h, int32_t s, int64_t n_after, const int64_t* after) {
+  if (n_after < 0 || (n_after > 0 && !after)) return fail(h, NETSIM_E_INVALID, "collective: bad 'after' list");
+  const int64_t F = (int64_t)h->f_bytes.size();
+  for (int64_t k = 0; k < n_after; ++k)
+    if (after[k] < 0 || after[k] >= F || h->f_scen[(size_t)after[k]] != s)
+      return fail(h, NETSIM_E_INVALID, "collective: 'after' must name existing flows of the same scenario");
+  return NETSIM_OK;
+}
+
+netsim_status check_ranks(netsim_t* h, int32_t s, int32_t p, const int32_t* ranks) {
+  if (s < 0 || s >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "collective: bad scenario");
+  if (!h->scen[s].has_fabric) return fail(h, NETSIM_E_INVALID, "collective: the scenario has no built-in fabric");
+  if (p > 0 && !ranks) return fail(h, NETSIM_E_INVALID, "collective: ranks is NULL");
+  const int64_t N = h->scen[s].fab.endpoints();
+  std::vector<int32_t> r(ranks, ranks + p);
+  for (int32_t x : r)
+    if (x < 0 || x >= N) return fail(h, NETSIM_E_INVALID, "collective: rank out of range");
+  std::sort(r.begin(), r.end());
+  if (std::adjacent_find(r.begin(), r.end()) != r.end()) return fail(h, NETSIM_E_INVALID, "collective: ranks must be distinct");
+  return NETSIM_OK;
+}
+
+// ---------------------------------------------------------- device layout
+netsim_status prepare(netsim_t* h) {
+  const int32_t S = (int32_t)h->scen.size();
+  const int64_t F = (int64_t)h->f_bytes.size();
+  h->F = F;
+  // device flow order: grouped by scenario, id order inside
+  h->dev_of_flow.assign((size_t)F, -1);
+  std::vector<int32_t> flow_of_dev((size_t)F);
+  std::vector<ScenCtl> ctl((size_t)S);
+  int64_t fd = 0;
+  for (int32_t s = 0; s < S; ++s) {
+    ScenCtl c{};
+    c.f0 = (int32_t)fd;
+    for (int64_t id : h->scen[s].flows) {
+      h->dev_of_flow[(size_t)id] = (int32_t)fd;
+      flow_of_dev[(size_t)fd] = (int32_t)id;
+      ++fd;
+    }
+    c.f1 = (int32_t)fd;
+    ctl[(size_t)s] = c;
+  }
+  // used links per scenario, compacted
+  h->dev_link.assign((size_t)S, {});
+  h->link_base.assign((size_t)S + 1, 0);
+  int64_t ld = 0;
+  double maxcap = 0.0;
+  for (int32_t s = 0; s < S; ++s) {
+    const Scen& sc = h->scen[s];
+    std::vector<int32_t>& m = h->dev_link[(size_t)s];
+    m.assign(sc.cap.size(), -1);
+    for (int64_t id : sc.flows)
+      for (int64_t e = h->p_off[(size_t)id]; e < h->p_off[(size_t)id + 1]; ++e) m[(size_t)h->p_link[(size_t)e]] = 0;
+    h->link_base[(size_t)s] = (int32_t)ld;
+    ctl[(size_t)s].l0 = (int32_t)ld;
+    for (size_t l = 0; l < m.size(); ++l)
+      if (m[l] == 0) {
+        m[l] = (int32_t)ld++;
+        maxcap = std::max(maxcap, sc.cap[l]);
+      }
+    ctl[(size_t)s].l1 = (int32_t)ld;
+    if (ld > std::numeric_limits<int32_t>::max()) return fail(h, NETSIM_E_LIMIT, "run: more than 2^31-1 used links");
+  }
+  h->link_base[(size_t)S] = (int32_t)ld;
+  h->L = ld;
+  h->nnz = (int64_t)h->p_link.size();
+  // fixed-point scale: largest capacity below 2^61 units
+  int ex = 0;
+  if (maxcap > 0.0) std::frexp(maxcap, &ex);
+  h->scale = std::ldexp(1.0, 61 - ex);
+  std::vector<int64_t> R0((size_t)std::max<int64_t>(ld, 1));
+  for (int32_t s = 0; s < S; ++s) {
+    const Scen& sc = h->scen[s];
+    for (size_t l = 0; l < sc.cap.size(); ++l) {
+      const int32_t d = h->dev_link[(size_t)s][l];
+      if (d >= 0) R0[(size_t)d] = (int64_t)std::llrint(sc.cap[l] * h->scale);
+    }
+  }
+  // paths, bytes, start in device order
+  std::vector<int32_t> poff((size_t)F + 1);
+  std::vector<int32_t> plink((size_t)std::max<int64_t>(h->nnz, 1));
+  std::vector<double> nbytes((size_t)std::max<int64_t>(F, 1)), start((size_t)std::max<int64_t>(F, 1));
+  std::vector<int32_t> ndeps((size_t)std::max<int64_t>(F, 1), 0);
+  int64_t e = 0;
+  for (int64_t d = 0; d < F; ++d) {
+    const int64_t id = flow_of_dev[(size_t)d];
+    const int32_t s = h->f_scen[(size_t)id];
+    poff[(size_t)d] = (int32_t)e;
+    for (int64_t k = h->p_off[(size_t)id]; k < h->p_off[(size_t)id + 1]; ++k)
+      plink[(size_t)e++] = h->dev_link[(size_t)s][(size_t)h->p_link[(size_t)k]];
+    nbytes[(size_t)d] = h->f_bytes[(size_t)id];
+    start[(size_t)d] = h->f_start[(size_t)id];
+    ndeps[(size_t)d] = (int32_t)(h->d_off[(size_t)id + 1] - h->d_off[(size_t)id]);
+  }
+  poff[(size_t)F] = (int32_t)e;
+  // successor lists (device ids)
+  std::vector<int32_t> soff((size_t)F + 1, 0);
+  for (int64_t id = 0; id < F; ++id)
+    for (int64_t k = h->d_off[(size_t)id]; k < h->d_off[(size_t)id + 1]; ++k)
+      soff[(size_t)h->dev_of_flow[(size_t)h->d_ids[(size_t)k]] + 1] += 1;
+  for (int64_t d = 0; d < F; ++d) soff[(size_t)d + 1] += soff[(size_t)d];
+  h->nsucc = soff[(size_t)F];
+  std::vector<int32_t> succ((size_t)std::max<int64_t>(h->nsucc, 1));
+  {
+    std::vector<int32_t> fill(soff.begin(), soff.end() - 1);
+    for (int64_t id = 0; id < F; ++id)
+      for (int64_t k = h->d_off[(size_t)id]; k < h->d_off[(size_t)id + 1]; ++k) {
+        const int32_t pred = h->dev_of_flow[(size_t)h->d_ids[(size_t)k]];
+        succ[(size_t)fill[(size_t)pred]++] = h->dev_of_flow[(size_t)id];
+      }
+  }
+  // initial dynamic state
+  h->h_cnt0 = ndeps;
+  h->h_rel0.assign((size_t)std::max<int64_t>(F, 1), 0.0);
+  h->h_pend0.assign((size_t)std::max<int64_t>(F, 1), 0);
+  for (int32_t s = 0; s < S; ++s) {
+    ScenCtl& c = ctl[(size_t)s];
+    int32_t np = 0;
+    for (int32_t d = c.f0; d < c.f1; ++d)
+      if (ndeps[(size_t)d] == 0) {
+        h->h_pend0[(size_t)(c.f0 + np)] = d;
+        h->h_rel0[(size_t)d] = start[(size_t)d];
+        ++np;
+      }
+    c.n_pend0 = np;
+  }
+  h->h_ctl0 = ctl;
+  // one device allocation, carved into aligned arrays
+  const size_t Fz = (size_t)std::max<int64_t>(F, 1), Lz = (size_t)std::max<int64_t>(ld, 1);
+  struct Part { void** dst; size_t bytes; };
+  Params& P = h->prm;
+  P = Params{};
+  std::vector<Part> parts = {
+      {(void**)&P.poff, sizeof(int32_t) * (Fz + 1)},
+      {(void**)&P.plink, sizeof(int32_t) * plink.size()},
+      {(void**)&P.nbytes, sizeof(double) * Fz},
+      {(void**)&P.start, sizeof(double) * Fz},
+      {(void**)&P.soff, sizeof(int32_t) * (Fz + 1)},
+      {(void**)&P.succ, sizeof(int32_t) * succ.size()},
+      {(void**)&P.R0, sizeof(int64_t) * Lz},
+      {(void**)&P.rem, sizeof(double) * Fz},
+      {(void**)&P.rate, sizeof(double) * Fz},
+      {(void**)&P.finish, sizeof(double) * Fz},
+      {(void**)&P.mf, sizeof(double) * Fz},
+      {(void**)&P.rel, sizeof(double) * Fz},
+      {(void**)&P.cnt, sizeof(int32_t) * Fz},
+      {(void**)&P.Rres, sizeof(int64_t) * Lz},
+      {(void**)&P.nres, sizeof(int32_t) * Lz},
+      {(void**)&P.nact, sizeof(int32_t) * Lz},
+      {(void**)&P.blocked0, Lz},
+      {(void**)&P.blocked1, Lz},
+      {(void**)&P.act0, sizeof(int32_t) * Fz},
+      {(void**)&P.act1, sizeof(int32_t) * Fz},
+      {(void**)&P.pend0, sizeof(int32_t) * Fz},
+      {(void**)&P.pend1, sizeof(int32_t) * Fz},
+      {(void**)&P.comp0, sizeof(int32_t) * Fz},
+      {(void**)&P.comp1, sizeof(int32_t) * Fz},
+      {(void**)&P.comp2, sizeof(int32_t) * Fz},
+      {(void**)&P.unf0, sizeof(int32_t) * Fz},
+      {(void**)&P.unf1, sizeof(int32_t) * Fz},
+      {(void**)&P.ctl, sizeof(ScenCtl) * (size_t)std::max<int32_t>(S, 1)},
+      {(void**)&P.bar, sizeof(uint32_t) * 64},
+      {(void**)&P.slots, sizeof(uint64_t) * 8},
+  };
+  size_t total = 0;
+  for (auto& p : parts) total += (p.bytes + 255) & ~size_t(255);
+  hipError_t he = hipSetDevice(h->opt.device);
+  if (he != hipSuccess) return hip_fail(h, he, "hipSetDevice");
+  he = hipMalloc(&h->d_block, total);
+  if (he != hipSuccess) {
+    h->d_block = nullptr;
+    return fail(h, NETSIM_E_NOMEM, "hipMalloc of " + std::to_string(total) + " bytes failed");
+  }
+  char* base = (char*)h->d_block;
+  for (auto& p : parts) {
+    *p.dst = base;
+    base += (p.bytes + 255) & ~size_t(255);
+  }
+  struct Up { const void* src; const void* dst; size_t bytes; };
+  const Up ups[] = {
+      {poff.data(), P.poff, sizeof(int32_t) * (size_t)(F + 1)},
+      {plink.data(), P.plink, sizeof(int32_t) * plink.size()},
+      {nbytes.data(), P.nbytes, sizeof(double) * nbytes.size()},
+      {start.data(), P.start, sizeof(double) * start.size()},
+      {soff.data(), P.soff, sizeof(int32_t) * (size_t)(F + 1)},
+      {succ.data(), P.succ, sizeof(int32_t) * succ.size()},
+      {R0.data(), P.R0, sizeof(int64_t) * R0.size()},
+  };
+  for (const Up& u : ups) {
+    he = hipMemcpy((void*)u.dst, u.src, u.bytes, hipMemcpyHostToDevice);
+    if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (upload)");
+  }
+  P.num_scen = S;
+  P.scale = h->scale;
+  P.inv_scale = 1.0 / h->scale;
+  h->prepared = true;
+  return NETSIM_OK;
+}
+
+// Resets the dynamic state for a run from t = 0 (on `stream`).
+netsim_status reset_state(netsim_t* h, hipStream_t st) {
+  Params& P = h->prm;
+  const size_t Fz = (size_t)std::max<int64_t>(h->F, 1), Lz = (size_t)std::max<int64_t>(h->L, 1);
+  hipError_t he;
+  std::vector<double> nan((size_t)Fz, std::numeric_limits<double>::quiet_NaN());
+  const uint64_t inf_bits = 0x7FF0000000000000ull;
+  uint64_t slots[8];
+  for (auto& x : slots) x = inf_bits;
+  struct Up { const void* src; void* dst; size_t bytes; };
+  const Up ups[] = {
+      {h->h_cnt0.data(), P.cnt, sizeof(int32_t) * Fz},
+      {h->h_rel0.data(), P.rel, sizeof(double) * Fz},
+      {h->h_pend0.data(), P.pend0, sizeof(int32_t) * Fz},
+      {nan.data(), P.finish, sizeof(double) * Fz},
+      {h->h_ctl0.data(), P.ctl, sizeof(ScenCtl) * h->h_ctl0.size()},
+      {slots, P.slots, sizeof(slots)},
+  };
+  for (const Up& u : ups) {
+    if (u.bytes == 0) continue;
+    he = hipMemcpyAsync(u.dst, u.src, u.bytes, hipMemcpyHostToDevice, st);
+    if (he != hipSuccess) return hip_fail(h, he, "hipMemcpyAsync (reset)");
+  }
+  he = hipMemsetAsync(P.nact, 0, sizeof(int32_t) * Lz, st);
+  if (he == hipSuccess) he = hipMemsetAsync(P.rate, 0, sizeof(double) * Fz, st);
+  if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 64, st);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemsetAsync (reset)");
+  he = hipStreamSynchronize(st);
+  if (he != hipSuccess) return hip_fail(h, he, "hipStreamSynchronize (reset)");
+  return NETSIM_OK;
+}
+
+netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms) {
+  Params P = h->prm;
+  P.mode = solve_only ? 1 : 0;
+  P.max_events = solve_only ? 0 : h->opt.max_events;
+  P.until = std::isnan(h->opt.until) ? std::numeric_limits<double>::infinity() : h->opt.until;
+  P.max_rounds = h->opt.max_rounds > 0 ? h->opt.max_rounds
+                                       : (int32_t)std::min<int64_t>(h->F + 1, std::numeric_limits<int32_t>::max());
+  const int32_t S = (int32_t)h->scen.size();
+  int exec = h->opt.exec;
+  if (exec == NETSIM_EXEC_AUTO) exec = (S > 1 || h->F < 100000) ? NETSIM_EXEC_BLOCK : NETSIM_EXEC_GRID;
+  hipEvent_t e0, e1;
+  hipError_t he = hipEventCreate(&e0);
+  if (he == hipSuccess) he = hipEventCreate(&e1);
+  if (he != hipSuccess) return hip_fail(h, he, "hipEventCreate");
+  he = hipEventRecord(e0, st);
+  if (he == hipSuccess) {
+    if (exec == NETSIM_EXEC_GRID) {
+      const int threads = 1024;
+      int cap = 0;
+      he = netsim_dev::grid_capacity(h->opt.device, threads, &cap);
+      hipDeviceProp_t prop;
+      if (he == hipSuccess) he = hipGetDeviceProperties(&prop, h->opt.device);
+      if (he == hipSuccess) {
+        int blocks = std::min(cap, prop.multiProcessorCount);
+        if (blocks < 1) blocks = 1;
+        he = netsim_dev::launch_grid(P, blocks, threads, st);
+      }
+    } else {
+      int threads = h->opt.block_threads > 0 ? h->opt.block_threads : 1024;
+      threads = std::max(64, std::min(1024, threads / 64 * 64));
+      const int blocks = std::max(1, std::min<int32_t>(S, 1 << 20));
+      he = netsim_dev::launch_block(P, blocks, threads, st);
+    }
+  }
+  if (he == hipSuccess) he = hipEventRecord(e1, st);
+  if (he == hipSuccess) he = hipEventSynchronize(e1);
+  if (he == hipSuccess) he = hipEventElapsedTime(ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (he != hipSuccess) return hip_fail(h, he, "kernel launch");
+  return NETSIM_OK;
+}
+
+netsim_status collect(netsim_t* h, std::vector<ScenCtl>* ctl_out) {
+  const int32_t S = (int32_t)h->scen.size();
+  std::vector<ScenCtl> ctl((size_t)S);
+  hipError_t he = hipMemcpy(ctl.data(), h->prm.ctl, sizeof(ScenCtl) * (size_t)S, hipMemcpyDeviceToHost);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (control blocks)");
+  *ctl_out = ctl;
+  for (int32_t s = 0; s < S; ++s) {
+    const int32_t st = ctl[(size_t)s].status;
+    if (st < 0) {
+      std::string why = st == netsim_dev::ST_ROUNDS ? "round watchdog fired"
+                        : st == netsim_dev::ST_BARRIER ? "grid barrier timed out"
+                        : st == netsim_dev::ST_OVERFLOW ? "work list overflow"
+                                                        : "non-positive fair share";
+      return fail(h, st == netsim_dev::ST_ROUNDS ? NETSIM_E_LIMIT : NETSIM_E_DEVICE,
+                  "device solver fault in scenario " + std::to_string(s) + ": " + why);
+    }
+  }
+  return NETSIM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void netsim_default_options(netsim_options* opt) {
+  if (!opt) return;
+  std::memset(opt, 0, sizeof *opt);
+  opt->until = std::numeric_limits<double>::infinity();
+}
+
+netsim_status netsim_create(netsim_t** out, int32_t num_scenarios, const int64_t* link_off,
+                            const double* capacity_Bps, const netsim_options* opt) {
+  if (!out) return fail(nullptr, NETSIM_E_INVALID, "create: out is NULL");
+  *out = nullptr;
+  if (num_scenarios < 1 || !link_off) return fail(nullptr, NETSIM_E_INVALID, "create: need >= 1 scenario and link_off");
+  if (link_off[0] != 0) return fail(nullptr, NETSIM_E_INVALID, "create: link_off[0] must be 0");
+  for (int32_t s = 0; s < num_scenarios; ++s)
+    if (link_off[s + 1] < link_off[s]) return fail(nullptr, NETSIM_E_INVALID, "create: link_off must not decrease");
+  const int64_t L = link_off[num_scenarios];
+  if (L > 0 && !capacity_Bps) return fail(nullptr, NETSIM_E_INVALID, "create: capacity_Bps is NULL");
+  for (int64_t l = 0; l < L; ++l)
+    if (!(std::isfinite(capacity_Bps[l]) && capacity_Bps[l] > 0.0))
+      return fail(nullptr, NETSIM_E_INVALID, "create: capacities must be finite and > 0 (link " + std::to_string(l) + ")");
+  netsim_t* h = new (std::nothrow) netsim_t();
+  if (!h) return fail(nullptr, NETSIM_E_NOMEM, "create: out of memory");
+  if (opt) h->opt = *opt;
+  else netsim_default_options(&h->opt);
+  h->scen.resize((size_t)num_scenarios);
+  for (int32_t s = 0; s < num_scenarios; ++s)
+    h->scen[(size_t)s].cap.assign(capacity_Bps + link_off[s], capacity_Bps + link_off[s + 1]);
+  *out = h;
+  return NETSIM_OK;
+}
+
+netsim_status netsim_create_topology(netsim_t** out, int32_t num_scenarios,
+                                     const netsim_topology* topos, const netsim_options* opt) {
+  if (!out) return fail(nullptr, NETSIM_E_INVALID, "create_topology: out is NULL");
+  *out = nullptr;
+  if (num_scenarios < 1 || !topos) return fail(nullptr, NETSIM_E_INVALID, "create_topology: need >= 1 topology");
+  netsim_t* h = new (std::nothrow) netsim_t();
+  if (!h) return fail(nullptr, NETSIM_E_NOMEM, "create_topology: out of memory");
+  if (opt) h->opt = *opt;
+  else netsim_default_options(&h->opt);
+  h->scen.resize((size_t)num_scenarios);
+  for (int32_t s = 0; s < num_scenarios; ++s) {
+    Scen& sc = h->scen[(size_t)s];
+    std::string err;
+    if (!sc.fab.init(topos[s], &err)) {
+      delete h;
+      return fail(nullptr, NETSIM_E_INVALID, "scenario " + std::to_string(s) + ": " + err);
+    }
+    sc.has_fabric = true;
+    sc.fab.capacities(&sc.cap);
+  }
+  *out = h;
+  return NETSIM_OK;
+}
+
+netsim_status netsim_get_links(const netsim_t* h, int32_t scen, int64_t* num_links, double* cap_out) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "get_links: handle is NULL");
+  if (scen < 0 || scen >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "get_links: bad scenario");
+  const auto& c = h->scen[(size_t)scen].cap;
+  if (num_links) *num_links = (int64_t)c.size();
+  if (cap_out) std::copy(c.begin(), c.end(), cap_out);
+  return NETSIM_OK;
+}
+
+netsim_status netsim_add_flows(netsim_t* h, int32_t scen, int64_t n, const int32_t* src,
+                               const int32_t* dst, const double* nbytes, const double* start,
+                               const int64_t* path_off, const int32_t* path_link,
+                               const int64_t* dep_off, const int64_t* dep_ids, int64_t* first_id) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "add_flows: handle is NULL");
+  return add_flows_impl(h, scen, n, src, dst, nbytes, start, path_off, path_link, dep_off, dep_ids, first_id);
+}
+
+netsim_status netsim_add_ring(netsim_t* h, int32_t scen, int32_t kind, int32_t mode, int32_t p,
+                              const int32_t* ranks, double nbytes, double lag, int64_t n_after,
+                              const int64_t* after, int64_t* first_id, int64_t* count) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "add_ring: handle is NULL");
+  if (h->prepared) return fail(h, NETSIM_E_STATE, "add_ring: flows cannot be added after a run");
+  if (kind < NETSIM_RING_ALLREDUCE || kind > NETSIM_RING_ALL_GATHER) return fail(h, NETSIM_E_INVALID, "add_ring: bad kind");
+  if (mode < NETSIM_MODE_CHAINED || mode > NETSIM_MODE_AGGREGATED) return fail(h, NETSIM_E_INVALID, "add_ring: bad mode");
+  if (p < 2) return fail(h, NETSIM_E_INVALID, "add_ring: need p >= 2");
+  if (!finite_nonneg(nbytes) || !finite_nonneg(lag)) return fail(h, NETSIM_E_INVALID, "add_ring: bytes and lag must be finite and >= 0");
+  netsim_status st = check_ranks(h, scen, p, ranks);
+  if (st) return st;
+  st = check_after(h, scen, n_after, after);
+  if (st) return st;
+  const int64_t steps = kind == NETSIM_RING_ALLREDUCE ? 2 * (int64_t)(p - 1) : (int64_t)(p - 1);
+  const double chunk = nbytes / (double)p;
+  const int64_t first = (int64_t)h->f_bytes.size();
+  const int64_t n = mode == NETSIM_MODE_AGGREGATED ? p : steps * p;
+  std::vector<int32_t> src((size_t)n), dst((size_t)n);
+  std::vector<double> b((size_t)n), t0((size_t)n);
+  std::vector<int64_t> doff((size_t)n + 1, 0), dids;
+  for (int64_t k = 0; k < n / p; ++k)
+    for (int32_t i = 0; i < p; ++i) {
+      const int64_t f = k * p + i;
+      src[(size_t)f] = ranks[i];
+      dst[(size_t)f] = ranks[(i + 1) % p];
+      b[(size_t)f] = mode == NETSIM_MODE_AGGREGATED ? (double)steps * chunk : chunk;
+      const bool entry = mode != NETSIM_MODE_CHAINED || k == 0;
+      t0[(size_t)f] = entry ? lag : 0.0;
+      if (entry) {
+        dids.insert(dids.end(), after, after + n_after);
+      } else {
+        dids.push_back(first + (k - 1) * p + (i + p - 1) % p);  // the step-(k-1) flow into rank i
+      }
+      doff[(size_t)f + 1] = (int64_t)dids.size();
+    }
+  st = add_flows_impl(h, scen, n, src.data(), dst.data(), b.data(), t0.data(), nullptr, nullptr,
+                      doff.data(), dids.data(), nullptr);
+  if (st) return st;
+  if (first_id) *first_id = first;
+  if (count) *count = n;
+  return NETSIM_OK;
+}
+
+netsim_status netsim_add_all_to_all(netsim_t* h, int32_t scen, int32_t p, const int32_t* ranks,
+                                    const double* nbytes, double lag, int64_t n_after,
+                                    const int64_t* after, int64_t* first_id, int64_t* count) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "add_all_to_all: handle is NULL");
+  if (h->prepared) return fail(h, NETSIM_E_STATE, "add_all_to_all: flows cannot be added after a run");
+  if (p < 1) return fail(h, NETSIM_E_INVALID, "add_all_to_all: need p >= 1");
+  if (!nbytes) return fail(h, NETSIM_E_INVALID, "add_all_to_all: nbytes is NULL");
+  if (!finite_nonneg(lag)) return fail(h, NETSIM_E_INVALID, "add_all_to_all: lag must be finite and >= 0");
+  netsim_status st = check_ranks(h, scen, p, ranks);
+  if (st) return st;
+  st = check_after(h, scen, n_after, after);
+  if (st) return st;
+  const int64_t first = (int64_t)h->f_bytes.size();
+  const int64_t n = (int64_t)p * (p - 1);
+  std::vector<int32_t> src, dst;
+  std::vector<double> b, t0;
+  std::vector<int64_t> doff(1, 0), dids;
+  src.reserve((size_t)n);
+  for (int32_t i = 0; i < p; ++i)
+    for (int32_t j = 0; j < p; ++j) {
+      if (i == j) continue;
+      src.push_back(ranks[i]);
+      dst.push_back(ranks[j]);
+      b.push_back(nbytes[(size_t)i * p + j]);
+      t0.push_back(lag);
+      dids.insert(dids.end(), after, after + n_after);
+      doff.push_back((int64_t)dids.size());
+    }
+  st = add_flows_impl(h, scen, n, src.data(), dst.data(), b.data(), t0.data(), nullptr, nullptr,
+                      doff.data(), dids.data(), nullptr);
+  if (st) return st;
+  if (first_id) *first_id = first;
+  if (count) *count = n;
+  return NETSIM_OK;
+}
+
+netsim_status netsim_counts(const netsim_t* h, int64_t* num_flows, int64_t* num_incidences,
+                            int64_t* num_deps) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "counts: handle is NULL");
+  if (num_flows) *num_flows = (int64_t)h->f_bytes.size();
+  if (num_incidences) *num_incidences = (int64_t)h->p_link.size();
+  if (num_deps) *num_deps = (int64_t)h->d_ids.size();
+  return NETSIM_OK;
+}
+
+netsim_status netsim_export_flows(const netsim_t* h, int32_t* scen, int32_t* src, int32_t* dst,
+                                  double* nbytes, double* start, int64_t* path_off,
+                                  int32_t* path_link, int64_t* dep_off, int64_t* dep_ids) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "export_flows: handle is NULL");
+  if (scen) std::copy(h->f_scen.begin(), h->f_scen.end(), scen);
+  if (src) std::copy(h->f_src.begin(), h->f_src.end(), src);
+  if (dst) std::copy(h->f_dst.begin(), h->f_dst.end(), dst);
+  if (nbytes) std::copy(h->f_bytes.begin(), h->f_bytes.end(), nbytes);
+  if (start) std::copy(h->f_start.begin(), h->f_start.end(), start);
+  if (path_off) std::copy(h->p_off.begin(), h->p_off.end(), path_off);
+  if (path_link) std::copy(h->p_link.begin(), h->p_link.end(), path_link);
+  if (dep_off) std::copy(h->d_off.begin(), h->d_off.end(), dep_off);
+  if (dep_ids) std::copy(h->d_ids.begin(), h->d_ids.end(), dep_ids);
+  return NETSIM_OK;
+}
+
+netsim_status netsim_set_limits(netsim_t* h, int64_t max_events, double until) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "set_limits: handle is NULL");
+  if (max_events < 0 || std::isnan(until)) return fail(h, NETSIM_E_INVALID, "set_limits: bad limit");
+  h->opt.max_events = max_events;
+  h->opt.until = until;
+  return NETSIM_OK;
+}
+
+netsim_status netsim_run(netsim_t* h, void* hip_stream) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "run: handle is NULL");
+  hipStream_t st = (hipStream_t)hip_stream;
+  const auto t0 = std::chrono::steady_clock::now();
+  netsim_status rc;
+  if (!h->prepared) {
+    rc = prepare(h);
+    if (rc) return rc;
+  }
+  hipError_t he = hipSetDevice(h->opt.device);
+  if (he != hipSuccess) return hip_fail(h, he, "hipSetDevice");
+  rc = reset_state(h, st);
+  if (rc) return rc;
+  const auto t1 = std::chrono::steady_clock::now();
+  float ms = 0.0f;
+  if (h->F > 0) {
+    rc = launch(h, st, false, &ms);
+    if (rc) return rc;
+  }
+  std::vector<ScenCtl> ctl;
+  rc = h->F > 0 ? collect(h, &ctl) : NETSIM_OK;
+  if (h->F == 0) ctl = h->h_ctl0;
+  // results, even on a device fault (partial), for inspection
+  const int64_t F = h->F;
+  std::vector<double> fin_dev((size_t)std::max<int64_t>(F, 1));
+  if (F > 0) {
+    he = hipMemcpy(fin_dev.data(), h->prm.finish, sizeof(double) * (size_t)F, hipMemcpyDeviceToHost);
+    if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (finish)");
+  }
+  h->finish.assign((size_t)F, 0.0);
+  for (int64_t id = 0; id < F; ++id) h->finish[(size_t)id] = fin_dev[(size_t)h->dev_of_flow[(size_t)id]];
+  const int32_t S = (int32_t)h->scen.size();
+  h->makespan.assign((size_t)S, 0.0);
+  netsim_stats s{};
+  s.complete = 1;
+  for (int32_t k = 0; k < S; ++k) {
+    const ScenCtl& c = ctl[(size_t)k];
+    double m = 0.0;
+    for (int32_t d = c.f0; d < c.f1; ++d)
+      if (!std::isnan(fin_dev[(size_t)d])) {
+        m = std::max(m, fin_dev[(size_t)d]);
+        s.completed_flows += 1;
+      }
+    h->makespan[(size_t)k] = m;
+    s.events += c.events;
+    s.solves += c.solves;
+    s.rounds += c.rounds;
+    s.flows_swept += c.flows_swept;
+    s.incidences_swept += c.incidences_swept;
+    s.active_swept += c.active_swept;
+    s.pending_swept += c.pending_swept;
+    s.sim_time = std::max(s.sim_time, c.t);
+    if (c.status != 0) s.complete = 0;
+  }
+  s.device_seconds = ms * 1e-3;
+  s.upload_seconds = std::chrono::duration<double>(t1 - t0).count();
+  h->stats = s;
+  h->has_result = true;
+  return rc;
+}
+
+netsim_status netsim_get_finish(const netsim_t* h, double* finish, double* makespan) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "get_finish: handle is NULL");
+  if (!h->has_result) return fail(h, NETSIM_E_STATE, "get_finish: no run yet");
+  if (!finish && h->F > 0) return fail(h, NETSIM_E_INVALID, "get_finish: finish is NULL");
+  std::copy(h->finish.begin(), h->finish.end(), finish);
+  if (makespan) std::copy(h->makespan.begin(), h->makespan.end(), makespan);
+  return NETSIM_OK;
+}
+
+netsim_status netsim_get_finish_device(const netsim_t* h, double* d_finish) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "get_finish_device: handle is NULL");
+  if (!h->has_result) return fail(h, NETSIM_E_STATE, "get_finish_device: no run yet");
+  if (h->F == 0) return NETSIM_OK;
+  if (!d_finish) return fail(h, NETSIM_E_INVALID, "get_finish_device: pointer is NULL");
+  hipError_t he = hipMemcpy(d_finish, h->finish.data(), sizeof(double) * (size_t)h->F, hipMemcpyHostToDevice);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (finish to device)");
+  return NETSIM_OK;
+}
+
+netsim_status netsim_get_stats(const netsim_t* h, netsim_stats* stats) {
+  if (!h || !stats) return fail(h, NETSIM_E_INVALID, "get_stats: NULL argument");
+  *stats = h->stats;
+  return NETSIM_OK;
+}
+
+netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, const int64_t* active_ids,
+                                double* rates_out) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "solve_once: handle is NULL");
+  if (scen < 0 || scen >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "solve_once: bad scenario");
+  if (n_active < 0 || (n_active > 0 && (!active_ids || !rates_out)))
+    return fail(h, NETSIM_E_INVALID, "solve_once: bad arguments");
+  const int64_t F = (int64_t)h->f_bytes.size();
+  std::vector<char> seen((size_t)F, 0);
+  for (int64_t k = 0; k < n_active; ++k) {
+    const int64_t id = active_ids[k];
+    if (id < 0 || id >= F || h->f_scen[(size_t)id] != scen) return fail(h, NETSIM_E_INVALID, "solve_once: id not in the scenario");
+    if (seen[(size_t)id]) return fail(h, NETSIM_E_INVALID, "solve_once: repeated id");
+    if (h->p_off[(size_t)id + 1] == h->p_off[(size_t)id]) return fail(h, NETSIM_E_INVALID, "solve_once: flow without a path");
+    seen[(size_t)id] = 1;
+  }
+  netsim_status rc;
+  if (!h->prepared) {
+    rc = prepare(h);
+    if (rc) return rc;
+  }
+  hipError_t he = hipSetDevice(h->opt.device);
+  if (he != hipSuccess) return hip_fail(h, he, "hipSetDevice");
+  rc = reset_state(h, nullptr);
+  if (rc) return rc;
+  const Params& P = h->prm;
+  std::vector<ScenCtl> ctl = h->h_ctl0;
+  for (auto& c : ctl) c.n_solve = 0;
+  ctl[(size_t)scen].n_solve = (int32_t)n_active;
+  std::vector<int32_t> list((size_t)std::max<int64_t>(n_active, 1));
+  std::vector<int32_t> nact((size_t)std::max<int64_t>(h->L, 1), 0);
+  for (int64_t k = 0; k < n_active; ++k) {
+    const int64_t id = active_ids[k];
+    const int32_t d = h->dev_of_flow[(size_t)id];
+    list[(size_t)k] = d;
+    for (int64_t e = h->p_off[(size_t)id]; e < h->p_off[(size_t)id + 1]; ++e)
+      nact[(size_t)h->dev_link[(size_t)scen][(size_t)h->p_link[(size_t)e]]] += 1;
+  }
+  he = hipMemcpy(P.ctl, ctl.data(), sizeof(ScenCtl) * ctl.size(), hipMemcpyHostToDevice);
+  if (he == hipSuccess && n_active > 0)
+    he = hipMemcpy(P.act0 + ctl[(size_t)scen].f0, list.data(), sizeof(int32_t) * (size_t)n_active, hipMemcpyHostToDevice);
+  if (he == hipSuccess) he = hipMemcpy(P.nact, nact.data(), sizeof(int32_t) * nact.size(), hipMemcpyHostToDevice);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (solve_once setup)");
+  float ms = 0.0f;
+  rc = launch(h, nullptr, true, &ms);
+  if (rc) return rc;
+  std::vector<ScenCtl> out;
+  rc = collect(h, &out);
+  if (rc) return rc;
+  std::vector<double> rate((size_t)std::max<int64_t>(h->F, 1));
+  he = hipMemcpy(rate.data(), P.rate, sizeof(double) * (size_t)std::max<int64_t>(h->F, 1), hipMemcpyDeviceToHost);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (rates)");
+  for (int64_t k = 0; k < n_active; ++k) rates_out[k] = rate[(size_t)list[(size_t)k]];
+  h->stats = netsim_stats{};
+  h->stats.solves = out[(size_t)scen].solves;
+  h->stats.rounds = out[(size_t)scen].rounds;
+  h->stats.flows_swept = out[(size_t)scen].flows_swept;
+  h->stats.incidences_swept = out[(size_t)scen].incidences_swept;
+  h->stats.device_seconds = ms * 1e-3;
+  h->stats.complete = 1;
+  return NETSIM_OK;
+}
+
+const char* netsim_last_error(const netsim_t* h) {
+  return h ? h->err.c_str() : g_thread_err.c_str();
+}
+
+void netsim_destroy(netsim_t* h) {
+  if (!h) return;
+  if (h->d_block) {
+    (void)hipSetDevice(h->opt.device);
+    (void)hipFree(h->d_block);
+  }
+  delete h;
+}
+
+}  // extern "C"
