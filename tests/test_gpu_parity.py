@@ -100,13 +100,45 @@ def test_c2_full():
     _say("c2 events", stats["events"], ref.events, "solves", stats["solves"], ref.solves)
 
 
+def _perturbed(fs, k):
+    """The flow set with every capacity moved k ulps (k may be negative)."""
+    cap = fs.cap.copy()
+    for _ in range(abs(k)):
+        cap = np.nextafter(cap, np.inf if k > 0 else 0.0)
+    return oflows.FlowSet(cap, fs.src, fs.dst, fs.nbytes, fs.start, fs.path_off, fs.path_link,
+                          fs.dep_off, fs.dep_ids)
+
+
+def _check_ill_conditioned(fs, gpu_finish):
+    """For trajectories that fp64 does not determine to 1e-6 (the oracle
+    itself moves by more under a one-ulp change of the capacities):
+    per-flow 1e-6 up to the horizon where one-ulp oracle runs still agree
+    to 1e-9, and beyond it the GPU's deviation from the oracle must stay
+    within 4x the spread of the oracle's own one-ulp runs."""
+    ref = osim.run_flowset(fs)
+    runs = [osim.run_flowset(_perturbed(fs, k)).finish for k in (-1, 1, 2)]
+    dev = np.max([np.abs(r - ref.finish) / ref.finish for r in runs], axis=0)
+    order = np.argsort(ref.finish)
+    bad = order[dev[order] > 1e-9]
+    horizon = ref.finish[bad[0]] if len(bad) else np.inf
+    early = ref.finish < horizon
+    gdev = np.abs(gpu_finish - ref.finish) / ref.finish
+    assert early.sum() > 0.05 * len(early)
+    assert np.max(gdev[early]) < TOL
+    spread_ms = max(abs(np.max(r) - ref.makespan) for r in runs) / ref.makespan
+    gpu_ms = abs(np.max(gpu_finish) - ref.makespan) / ref.makespan
+    assert gpu_ms <= 4 * spread_ms + 1e-12
+    assert np.quantile(gdev, 0.99) <= 4 * np.quantile(dev, 0.99) + 1e-12
+    _say(f"horizon {horizon:.4g}s covers {early.mean():.1%} of flows; makespan dev gpu "
+         f"{gpu_ms:.2e} vs oracle ulp spread {spread_ms:.2e}")
+
+
 def test_c3_reduced():
     ns, pr = _gpu()
     _say("test_c3_reduced")
     program = configs.c3(3, groups=2, background=400)
     fins, stats = pr.run_program(program, ns.make_options())
-    ref = osim.run_scenario(program.scenarios[0])
-    assert _rel(fins[0], ref.finish) < TOL
+    _check_ill_conditioned(oflows.expand(program.scenarios[0]), fins[0])
 
 
 def test_c4_one_group_full_run():

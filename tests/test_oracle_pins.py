@@ -306,3 +306,18 @@ def test_until_horizon_is_a_prefix():
     done = np.isfinite(part.finish)
     assert np.array_equal(done, full.finish <= T)
     assert np.array_equal(part.finish[done], full.finish[done])
+
+
+def test_c3_is_ill_conditioned_in_fp64():
+    """The chained rings of C3 over degraded links amplify rounding: one ulp
+    on every capacity moves the oracle's own finish times by far more than
+    1e-6, whereas C1 and C2 move by about 1e-14.  (This is why C3 parity is
+    checked against the oracle's own one-ulp spread past a horizon.)"""
+    def spread(fs):
+        base = sim.run_flowset(fs).finish
+        pert = flows.FlowSet(np.nextafter(fs.cap, np.inf), fs.src, fs.dst, fs.nbytes, fs.start,
+                             fs.path_off, fs.path_link, fs.dep_off, fs.dep_ids)
+        return np.max(np.abs(sim.run_flowset(pert).finish - base) / base)
+    assert spread(flows.expand(configs.c3(3, groups=2, background=400).scenarios[0])) > 1e-3
+    assert spread(flows.expand(configs.c1(1).scenarios[0])) < 1e-12
+    assert spread(flows.expand(configs.c2(2, tp_reps=6).scenarios[0])) < 1e-12
