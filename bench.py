@@ -135,6 +135,8 @@ def main():
         "rounds_per_solve": st["rounds"] / max(st["solves"], 1),
         "wall_s_incl_state_reset": wall,
         "sim_time_s": st["sim_time"],
+        "phase_seconds": dict(zip(["next_event", "settle", "solve_setup", "sweep_b", "wait_b",
+                                   "sweep_c", "wait_c"], [round(x, 6) for x in st["phase_seconds"][:7]])),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
                      "kernel": "netsim_grid_kernel" if args.exec == "grid" else "netsim_block_kernel",

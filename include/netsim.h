@@ -133,6 +133,11 @@ typedef struct {
   double sim_time;           /* largest simulated time reached over scenarios    */
   double device_seconds;     /* device time of the last netsim_run (HIP events)  */
   double upload_seconds;     /* host->device preparation of the last run          */
+  /* Device time by phase, summed over scenarios, as seen by the first thread
+   * of the group running each scenario: [0] next-event search, [1] settling
+   * completions and releases, [2] solve set-up, [3] share/blocking sweep,
+   * [4] wait after it, [5] freezing sweep, [6] wait after it, [7] unused. */
+  double phase_seconds[8];
 } netsim_stats;
 
 /* Fills *opt with the defaults (device 0, auto layout, no limits). */

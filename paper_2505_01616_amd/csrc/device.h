@@ -21,13 +21,14 @@ struct ScenCtl {
   int64_t active_swept, pending_swept;
   int32_t status;          // 0 ran to the end, 1 stopped at a limit, < 0 fault
   int32_t fault_info;
+  int64_t ticks[8];        // wall-clock ticks per phase (first thread of the group)
   // list counters (kernel scratch; zero at launch)
   int32_t cnt_act[2];
   int32_t cnt_pend[2];
   int32_t cnt_comp[3];
   int32_t cnt_unf[2];
   int32_t changed[2];
-  int32_t pad;
+  int32_t rem3[3];         // shared-memory solve: unfrozen flows left, rotating
 };
 
 enum : int32_t {
@@ -45,7 +46,7 @@ struct Params {
   int64_t max_events;      // 0 = no limit
   double until;
   int32_t max_rounds;
-  int32_t pad;
+  int32_t lds_ok;          // every path fits the shared-memory solve (<= 6 links)
   double scale;            // fixed-point units per B/s (a power of two)
   double inv_scale;
   // static flow / link data (device order)
@@ -64,8 +65,7 @@ struct Params {
   double* rel;             // [F] release time (pending flows)
   int32_t* cnt;            // [F] predecessors not yet finished
   // dynamic link state
-  int64_t* Rres;           // [L] residual capacity (fixed point) during a solve
-  int32_t* nres;           // [L] unfrozen flows during a solve
+  int64_t* lst;            // [2L] per link: residual capacity (fixed point), unfrozen flows
   int32_t* nact;           // [L] active flows
   uint8_t* blocked0;       // [L] round flags (two, alternating)
   uint8_t* blocked1;
@@ -75,7 +75,7 @@ struct Params {
   int32_t* comp0; int32_t* comp1; int32_t* comp2;
   int32_t* unf0; int32_t* unf1;
   ScenCtl* ctl;            // [num_scen]
-  uint32_t* bar;           // grid barrier: [0] arrivals, [1] generation, [2] abort
+  uint32_t* bar;           // grid barrier words [1024] (layout in kernels.hip)
   uint64_t* slots;         // grid min-reduction slots [4]
 };
 

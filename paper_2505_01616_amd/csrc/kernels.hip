@@ -39,7 +39,7 @@ namespace {
 
 constexpr double THR = 1.000000000001;
 constexpr double INF = __builtin_huge_val();
-constexpr int FAST_DEG = 8;
+constexpr int FAST_DEG = 6;
 constexpr uint64_t BARRIER_TIMEOUT_TICKS = 1000000000ull;  // 10 s at 100 MHz
 
 __device__ __forceinline__ double wave_min(double v) {
@@ -56,7 +56,11 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 // ------------------------------------------------------------------ groups
 struct BlockG {
   double* lds;
+  int* ldsi;
   __device__ int tid() const { return threadIdx.x; }
+  __device__ int block_base() const { return 0; }
+  __device__ int nblocks() const { return 1; }
+  __device__ int block_id() const { return 0; }
   __device__ int nthr() const { return blockDim.x; }
   __device__ bool aborted() const { return false; }
   __device__ void sync() { __syncthreads(); }
@@ -87,46 +91,114 @@ struct BlockG {
   }
 };
 
+// Barrier words (uint32 indices into Params::bar, 64-byte lines apart):
+constexpr int BAR_COUNT = 0, BAR_GEN = 1, BAR_ABORT = 16, BAR_REG = 32, BAR_REG_GEN = 33;
+constexpr int BAR_XCD = 64;        // XCD x: arrivals at 64 + 32x, generation at 64 + 32x + 16
+constexpr int BAR_XCD_BLOCKS = 640;  // blocks resident on XCD x
+constexpr int BAR_WORDS = 1024;
+
+__device__ __forceinline__ unsigned xcc_id() {
+  return __builtin_amdgcn_s_getreg(6164) & 15u;  // hwreg(HW_REG_XCC_ID, 0, 4)
+}
+
 struct GridG {
   double* lds;
+  int* ldsi;
   int* flag;      // shared: abort state as seen by this block's thread 0
   uint32_t* bar;
   uint64_t* slots;
   uint32_t gen;
   uint32_t nred;
   bool ab;        // block-uniform copy of *flag, refreshed at every barrier
+  uint32_t xcc, mine, nx;  // this block's XCD, blocks on it, XCDs in use
   __device__ int tid() const { return blockIdx.x * blockDim.x + threadIdx.x; }
+  __device__ int block_base() const { return blockIdx.x * blockDim.x; }
+  __device__ int nblocks() const { return gridDim.x; }
+  __device__ int block_id() const { return blockIdx.x; }
   __device__ int nthr() const { return gridDim.x * blockDim.x; }
   __device__ bool aborted() const { return ab; }
-  // Generation barrier.  The last block to arrive resets the arrival count
-  // and publishes the next generation (release); the others wait for it
-  // (acquire).  A block waiting longer than BARRIER_TIMEOUT_TICKS raises the
-  // abort flag; a waiting block that sees the flag stops waiting.  Thread 0
-  // passes the flag to its block through shared memory, so every decision
-  // taken on it is uniform inside the block and all blocks leave their loops.
+
+  // Waits (thread 0 only) until *p != g; gives up on the abort flag or after
+  // BARRIER_TIMEOUT_TICKS, raising the flag.  Returns false if it gave up.
+  __device__ bool wait_change(uint32_t* p, uint32_t g) {
+    const uint64_t t0 = wall_clock64();
+    while (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == g) {
+      __builtin_amdgcn_s_sleep(1);
+      if (__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)
+        return false;
+      if (wall_clock64() - t0 > BARRIER_TIMEOUT_TICKS) {
+        __hip_atomic_store(&bar[BAR_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return false;
+      }
+    }
+    return true;
+  }
+
+  // Once per launch: every block counts itself on its XCD, then one flat
+  // barrier, after which each block knows how many blocks share its XCD.
+  __device__ void init() {
+    __shared__ uint32_t s_mine, s_nx;
+    if (threadIdx.x == 0) {
+      const uint32_t x = xcc_id();
+      __hip_atomic_fetch_add(&bar[BAR_XCD_BLOCKS + x], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t prev =
+          __hip_atomic_fetch_add(&bar[BAR_REG], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      if (prev == gridDim.x - 1) {
+        __hip_atomic_store(&bar[BAR_REG_GEN], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      } else {
+        wait_change(&bar[BAR_REG_GEN], 0u);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      }
+      uint32_t n = 0;
+      for (int k = 0; k < 16; ++k)
+        n += __hip_atomic_load(&bar[BAR_XCD_BLOCKS + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) > 0;
+      s_mine = __hip_atomic_load(&bar[BAR_XCD_BLOCKS + x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_nx = n;
+      *flag = (int)__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    xcc = xcc_id();
+    mine = s_mine;
+    nx = s_nx;
+    ab = *flag != 0;
+    __syncthreads();
+  }
+
+  // Two-level barrier.  The blocks of one XCD share its L2: the last of them
+  // to arrive writes that L2 back once (release) and arrives at the global
+  // count; the last XCD to arrive publishes the next generation.  Every block
+  // then acquires (invalidating its L1 and the XCD's L2) before going on.
+  // Writing an L2 back once per XCD instead of once per block is what makes
+  // this cheaper than a flat barrier.  A block waiting longer than
+  // BARRIER_TIMEOUT_TICKS raises the abort flag; thread 0 passes the flag to
+  // its block through shared memory, so decisions on it are block-uniform.
   __device__ void sync() {
     __syncthreads();
     if (threadIdx.x == 0) {
-      uint32_t a = __hip_atomic_load(&bar[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      uint32_t a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (a == 0) {
+        uint32_t* xc = &bar[BAR_XCD + 32 * xcc];
+        uint32_t* xg = &bar[BAR_XCD + 32 * xcc + 16];
         const uint32_t g = gen;
-        const uint32_t prev =
-            __hip_atomic_fetch_add(&bar[0], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        if (prev == gridDim.x - 1) {
-          __hip_atomic_store(&bar[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_store(&bar[1], g + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-          const uint64_t t0 = wall_clock64();
-          while (__hip_atomic_load(&bar[1], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == g) {
-            __builtin_amdgcn_s_sleep(1);
-            if (__hip_atomic_load(&bar[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) break;
-            if (wall_clock64() - t0 > BARRIER_TIMEOUT_TICKS) {
-              __hip_atomic_store(&bar[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              break;
-            }
+        const uint32_t prev = __hip_atomic_fetch_add(xc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (prev == mine - 1) {
+          __hip_atomic_store(xc, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+          const uint32_t gp =
+              __hip_atomic_fetch_add(&bar[BAR_COUNT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (gp == nx - 1) {
+            __hip_atomic_store(&bar[BAR_COUNT], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&bar[BAR_GEN], g + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          } else {
+            wait_change(&bar[BAR_GEN], g);
           }
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          __hip_atomic_store(xg, g + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+          wait_change(xg, g);
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         }
-        a = __hip_atomic_load(&bar[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       *flag = (int)a;
     }
@@ -186,8 +258,68 @@ __device__ __forceinline__ int wave_append(G& g, int32_t* counter, bool pred) {
   return pred ? base + (int)__popcll(mask & ((1ull << lane) - 1ull)) : -1;
 }
 
+// Appends to K lists at once with one atomic per list per workgroup: wave
+// ballots, per-wave counts in shared memory, a prefix over the waves and a
+// single fetch-add on each list counter.  Every thread of the workgroup must
+// call it (loops that use it run the same trip count in the whole block).
+template <int K, class G>
+__device__ __forceinline__ void block_append(G& g, int32_t* const* counters, const bool* pred,
+                                             int* slot) {
+  int* sh = g.ldsi;  // [K*16] per-wave counts, [48 + k] list bases
+  const int lane = lane_id(), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  uint64_t mask[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    mask[k] = __ballot(pred[k]);
+    if (lane == 0) sh[k * 16 + w] = (int)__popcll(mask[k]);
+  }
+  __syncthreads();
+  if (threadIdx.x < K) {
+    const int k = threadIdx.x;
+    int total = 0;
+    for (int j = 0; j < nw; ++j) {
+      const int c = sh[k * 16 + j];
+      sh[k * 16 + j] = total;
+      total += c;
+    }
+    sh[48 + k] = total ? g.add(counters[k], (int32_t)total) : 0;
+  }
+  __syncthreads();
+  const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+    slot[k] = pred[k] ? sh[48 + k] + sh[k * 16 + w] + (int)__popcll(mask[k] & below) : -1;
+  __syncthreads();
+}
+
+// Per-phase wall-clock accounting by the group's first thread, kept in
+// shared memory (acc[0..8) and the last reading in acc[8]).
+struct Clock {
+  bool on;
+  uint64_t* acc;
+  __device__ Clock(bool o, uint64_t* a) : on(o), acc(a) {
+    if (on) {
+      for (int k = 0; k < 8; ++k) acc[k] = 0;
+      acc[8] = wall_clock64();
+    }
+  }
+  __device__ __forceinline__ void lap(int k) {
+    if (on) {
+      const uint64_t now = wall_clock64();
+      acc[k] += now - acc[8];
+      acc[8] = now;
+    }
+  }
+};
+
+// A flow id read from a work list must lie in the scenario's range.
+__device__ __forceinline__ bool in_range(int f, int f0, int cap) {
+  return (unsigned)(f - f0) < (unsigned)cap;
+}
+
 __device__ __forceinline__ double share(const Params& P, int l) {
-  return ((double)P.Rres[l] / (double)P.nres[l]) * P.inv_scale;
+  const longlong2 v = *reinterpret_cast<const longlong2*>(P.lst + 2 * l);
+  return ((double)v.x / (double)v.y) * P.inv_scale;
 }
 
 // ------------------------------------------------------------- rate solve
@@ -196,13 +328,13 @@ __device__ __forceinline__ double share(const Params& P, int l) {
 template <class G>
 __device__ int solve(G& g, const Params& P, ScenCtl* C, const int32_t* list0, int n0,
                      int32_t* unf_a, int32_t* unf_b, int cap, int64_t& rounds, int64_t& fsw,
-                     int64_t& isw) {
+                     int64_t& isw, Clock& clk) {
   const int T = g.nthr();
   const int tid = g.tid();
-  const int w0 = tid - lane_id();
+  const int b0 = g.block_base();
   for (int l = C->l0 + tid; l < C->l1; l += T) {
-    P.Rres[l] = P.R0[l];
-    P.nres[l] = P.nact[l];
+    P.lst[2 * l] = P.R0[l];
+    P.lst[2 * l + 1] = P.nact[l];
     P.blocked0[l] = 0;
     P.blocked1[l] = 0;
   }
@@ -211,6 +343,7 @@ __device__ int solve(G& g, const Params& P, ScenCtl* C, const int32_t* list0, in
     g.store(&C->cnt_unf[1], 0);
   }
   g.sync();
+  clk.lap(2);
   const int32_t* in = list0;
   int n = n0;
   int r = 0;
@@ -222,50 +355,51 @@ __device__ int solve(G& g, const Params& P, ScenCtl* C, const int32_t* list0, in
     int32_t* out_cnt = &C->cnt_unf[r & 1];
     if (tid == 0 && r > 0) g.store(out_cnt, 0);
     // phase B: smallest share on each path; block links above it
-    for (int i0 = w0; i0 < n; i0 += T) {
-      const int i = i0 + lane_id();
-      if (i < n) {
-        const int f = in[i];
-        const int e0 = P.poff[f], e1 = P.poff[f + 1];
-        const int deg = e1 - e0;
-        isw += deg;
-        double m = INF;
-        if (deg <= FAST_DEG) {
-          double sv[FAST_DEG];
-          int lv[FAST_DEG];
+    for (int i = tid; i < n; i += T) {
+      const int f = in[i];
+      if (!in_range(f, C->f0, cap)) { bad = 2; continue; }
+      const int e0 = P.poff[f], e1 = P.poff[f + 1];
+      const int deg = e1 - e0;
+      isw += deg;
+      double m = INF;
+      if (deg <= FAST_DEG) {
+        double sv[FAST_DEG];
+        int lv[FAST_DEG];
 #pragma unroll
-          for (int k = 0; k < FAST_DEG; ++k) {
-            if (k < deg) {
-              lv[k] = P.plink[e0 + k];
-              sv[k] = share(P, lv[k]);
-              m = sv[k] < m ? sv[k] : m;
-            }
+        for (int k = 0; k < FAST_DEG; ++k) {
+          if (k < deg) {
+            lv[k] = P.plink[e0 + k];
+            sv[k] = share(P, lv[k]);
+            m = sv[k] < m ? sv[k] : m;
           }
-          const double thr = m * THR;
-#pragma unroll
-          for (int k = 0; k < FAST_DEG; ++k)
-            if (k < deg && sv[k] > thr) bl[lv[k]] = 1;
-        } else {
-          for (int e = e0; e < e1; ++e) {
-            const double s = share(P, P.plink[e]);
-            m = s < m ? s : m;
-          }
-          const double thr = m * THR;
-          for (int e = e0; e < e1; ++e)
-            if (share(P, P.plink[e]) > thr) bl[P.plink[e]] = 1;
         }
-        if (!(m > 0.0) || !(m < INF)) bad = 1;
-        P.mf[f] = m;
+        const double thr = m * THR;
+#pragma unroll
+        for (int k = 0; k < FAST_DEG; ++k)
+          if (k < deg && sv[k] > thr) bl[lv[k]] = 1;
+      } else {
+        for (int e = e0; e < e1; ++e) {
+          const double s = share(P, P.plink[e]);
+          m = s < m ? s : m;
+        }
+        const double thr = m * THR;
+        for (int e = e0; e < e1; ++e)
+          if (share(P, P.plink[e]) > thr) bl[P.plink[e]] = 1;
       }
+      if (!(m > 0.0) || !(m < INF)) bad = 1;
+      P.mf[f] = m;
     }
+    clk.lap(3);
     g.sync();
+    clk.lap(4);
     // phase C: freeze flows that cross an unblocked link
-    for (int i0 = w0; i0 < n; i0 += T) {
-      const int i = i0 + lane_id();
+    for (int base = b0; base < n; base += T) {
+      const int i = base + (int)threadIdx.x;
       bool keep = false;
       int f = -1;
-      if (i < n) {
-        f = in[i];
+      if (i < n) f = in[i];
+      if (i < n && !in_range(f, C->f0, cap)) bad = 2;
+      if (i < n && in_range(f, C->f0, cap)) {
         const int e0 = P.poff[f], e1 = P.poff[f + 1];
         bool frozen = false;
         for (int e = e0; e < e1; ++e) frozen |= (bl[P.plink[e]] == 0);
@@ -275,22 +409,27 @@ __device__ int solve(G& g, const Params& P, ScenCtl* C, const int32_t* list0, in
           const int64_t q = (int64_t)__builtin_rint(m * P.scale);
           for (int e = e0; e < e1; ++e) {
             const int l = P.plink[e];
-            g.add(&P.Rres[l], -q);
-            g.add(&P.nres[l], -1);
+            g.add(&P.lst[2 * l], -q);
+            g.add(&P.lst[2 * l + 1], (int64_t)-1);
           }
         } else {
           keep = true;
         }
       }
-      const int slot = wave_append(g, out_cnt, keep);
+      int32_t* const cnts[1] = {out_cnt};
+      const bool pr[1] = {keep};
+      int slot[1];
+      block_append<1>(g, cnts, pr, slot);
       if (keep) {
-        if (slot < cap) out[slot] = f;
+        if (slot[0] < cap) out[slot[0]] = f;
         else bad = 2;
       }
     }
     for (int l = C->l0 + tid; l < C->l1; l += T) bl_next[l] = 0;
     if (bad) g.store(&C->fault_info, bad);
+    clk.lap(5);
     g.sync();
+    clk.lap(6);
     rounds += 1;
     fsw += n;
     if (g.aborted()) return ST_BARRIER;
@@ -304,9 +443,177 @@ __device__ int solve(G& g, const Params& P, ScenCtl* C, const int32_t* list0, in
   }
 }
 
+// ---------------------------------------------- shared-memory-resident solve
+// Each workgroup takes a contiguous slice of the active list (at most
+// LDS_FLOWS flows), copies the flow ids and their padded paths into shared
+// memory once, and keeps its unfrozen flows as a shared-memory list.  Only
+// link state (residual capacity and count, blocked flags) and the rates go
+// through global memory, so a round costs one gather of link state, one of
+// flags and two barriers.
+constexpr int LDS_FLOWS = 1536;
+constexpr int LDS_DEG = 6;
+
+struct SolveLds {
+  int32_t fid[LDS_FLOWS];
+  int32_t link[LDS_FLOWS * LDS_DEG];
+  double mf[LDS_FLOWS];
+  uint16_t u[2][LDS_FLOWS];
+  int cnt;
+  uint64_t clk[9];
+};
+
+template <class G>
+__device__ int solve_lds(G& g, const Params& P, ScenCtl* C, const int32_t* list0, int n0,
+                         int64_t& rounds, int64_t& fsw, int64_t& isw, Clock& clk, SolveLds& S) {
+  const int T = g.nthr();
+  const int tid = g.tid();
+  const int nb = g.nblocks();
+  const int per = (n0 + nb - 1) / nb;
+  const int c0 = min(n0, g.block_id() * per);
+  const int nl = min(n0, c0 + per) - c0;
+  for (int l = C->l0 + tid; l < C->l1; l += T) {
+    P.lst[2 * l] = P.R0[l];
+    P.lst[2 * l + 1] = P.nact[l];
+    P.blocked0[l] = 0;
+    P.blocked1[l] = 0;
+  }
+  if (tid == 0)
+    for (int k = 0; k < 3; ++k) g.store(&C->rem3[k], 0);
+  int bad = 0;
+  for (int j = threadIdx.x; j < nl; j += blockDim.x) {
+    int f = list0[c0 + j];
+    if (!in_range(f, C->f0, C->f1 - C->f0)) { bad = 2; f = C->f0; }
+    const int e0 = P.poff[f], e1 = P.poff[f + 1];
+    S.fid[j] = f;
+#pragma unroll
+    for (int k = 0; k < LDS_DEG; ++k) S.link[j * LDS_DEG + k] = e0 + k < e1 ? P.plink[e0 + k] : -1;
+    S.u[0][j] = (uint16_t)j;
+  }
+  int nu = nl;
+  g.sync();
+  clk.lap(2);
+  int total = n0;
+  int r = 0;
+  for (;;) {
+    uint8_t* bl = (r & 1) ? P.blocked1 : P.blocked0;
+    uint8_t* bl_next = (r & 1) ? P.blocked0 : P.blocked1;
+    const uint16_t* uin = S.u[r & 1];
+    uint16_t* uout = S.u[(r & 1) ^ 1];
+    if (threadIdx.x == 0) S.cnt = 0;
+    if (tid == 0) g.store(&C->rem3[(r + 1) % 3], 0);
+    // phase B: smallest share on each path; block links above it
+    for (int x = threadIdx.x; x < nu; x += blockDim.x) {
+      const int j = uin[x];
+      double sv[LDS_DEG];
+      int lv[LDS_DEG];
+      double m = INF;
+#pragma unroll
+      for (int k = 0; k < LDS_DEG; ++k) {
+        lv[k] = S.link[j * LDS_DEG + k];
+        if (lv[k] >= 0) {
+          sv[k] = share(P, lv[k]);
+          m = sv[k] < m ? sv[k] : m;
+          isw += 1;
+        }
+      }
+      const double thr = m * THR;
+#pragma unroll
+      for (int k = 0; k < LDS_DEG; ++k)
+        if (lv[k] >= 0 && sv[k] > thr) bl[lv[k]] = 1;
+      if (!(m > 0.0) || !(m < INF)) bad = 1;
+      S.mf[j] = m;
+    }
+    clk.lap(3);
+    g.sync();
+    clk.lap(4);
+    // phase C: freeze flows crossing an unblocked link; keep the rest
+    for (int base = 0; base < nu; base += blockDim.x) {
+      const int x = base + (int)threadIdx.x;
+      bool keep = false;
+      int j = 0;
+      if (x < nu) {
+        j = uin[x];
+        bool frozen = false;
+#pragma unroll
+        for (int k = 0; k < LDS_DEG; ++k) {
+          const int l = S.link[j * LDS_DEG + k];
+          if (l >= 0) frozen |= (bl[l] == 0);
+        }
+        if (frozen) {
+          const double m = S.mf[j];
+          P.rate[S.fid[j]] = m;
+          const int64_t qv = (int64_t)__builtin_rint(m * P.scale);
+#pragma unroll
+          for (int k = 0; k < LDS_DEG; ++k) {
+            const int l = S.link[j * LDS_DEG + k];
+            if (l >= 0) {
+              g.add(&P.lst[2 * l], -qv);
+              g.add(&P.lst[2 * l + 1], (int64_t)-1);
+            }
+          }
+        } else {
+          keep = true;
+        }
+      }
+      const uint64_t mask = __ballot(keep);
+      if (mask) {
+        const int lane = lane_id();
+        const int leader = __ffsll((unsigned long long)mask) - 1;
+        int b = 0;
+        if (lane == leader) b = atomicAdd(&S.cnt, (int)__popcll(mask));
+        b = __shfl(b, leader, 64);
+        if (keep) uout[b + (int)__popcll(mask & ((1ull << lane) - 1ull))] = (uint16_t)j;
+      }
+    }
+    for (int l = C->l0 + tid; l < C->l1; l += T) bl_next[l] = 0;
+    if (bad) g.store(&C->fault_info, bad);
+    __syncthreads();
+    const int nu_new = S.cnt;
+    if (threadIdx.x == 0 && nu_new > 0) g.add(&C->rem3[r % 3], (int32_t)nu_new);
+    clk.lap(5);
+    g.sync();
+    clk.lap(6);
+    rounds += 1;
+    fsw += total;
+    if (g.aborted()) return ST_BARRIER;
+    if (g.load(&C->fault_info) != 0) return g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE;
+    const int left = g.load(&C->rem3[r % 3]);
+    if (left == 0) return 0;
+    if (left >= total) return ST_BAD_SHARE;  // a round must freeze something
+    if (++r > P.max_rounds) return ST_ROUNDS;
+    total = left;
+    nu = nu_new;
+  }
+}
+
+// Releases flow h whose last predecessor finished at t (called once per h).
+template <class G>
+__device__ __forceinline__ void release_one(G& g, const Params& P, ScenCtl* C, int h, double t,
+                                            int ob, int ib, int32_t* actOut, int32_t* pendOut,
+                                            int32_t* cout, int32_t* coutCnt, int cap, int& err) {
+  const double rl = P.start[h] + t;
+  if (rl <= t) {
+    if (P.nbytes[h] == 0.0) {
+      P.finish[h] = rl;
+      const int s = g.add(coutCnt, 1);
+      if (s < cap) cout[s] = h; else err = 1;
+    } else {
+      P.rem[h] = P.nbytes[h];
+      for (int j = P.poff[h]; j < P.poff[h + 1]; ++j) g.add(&P.nact[P.plink[j]], 1);
+      const int s = g.add(&C->cnt_act[ob], 1);
+      if (s < cap) actOut[s] = h; else err = 1;
+      g.store(&C->changed[ib], 1);
+    }
+  } else {
+    P.rel[h] = rl;
+    const int s = g.add(&C->cnt_pend[ob], 1);
+    if (s < cap) pendOut[s] = h; else err = 1;
+  }
+}
+
 // ------------------------------------------------------------- event loop
 template <class G>
-__device__ void event_loop(G& g, const Params& P, const int sc) {
+__device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
   ScenCtl* C = &P.ctl[sc];
   const int f0 = C->f0;
   const int cap = C->f1 - C->f0;
@@ -317,7 +624,9 @@ __device__ void event_loop(G& g, const Params& P, const int sc) {
   int32_t* unf_b = P.unf1 + f0;
   const int T = g.nthr();
   const int tid = g.tid();
+  const int b0 = g.block_base();
   const int w0 = tid - lane_id();
+  Clock clk(tid == 0, S.clk);
   double t = 0.0;
   int64_t events = 0, solves = 0, rounds = 0, fsw = 0, isw = 0, asw = 0, psw = 0;
   int nAct = 0;
@@ -340,18 +649,23 @@ __device__ void event_loop(G& g, const Params& P, const int sc) {
     double loc = INF;
     for (int i = tid; i < nAct; i += T) {
       const int f = actIn[i];
+      if (!in_range(f, f0, cap)) { g.store(&C->fault_info, 2); continue; }
       const double dt = P.rem[f] / P.rate[f];
       const double tau = t + dt;
       loc = tau < loc ? tau : loc;
     }
     for (int i = tid; i < nPend; i += T) {
-      const double rl = P.rel[pendIn[i]];
+      const int f = pendIn[i];
+      if (!in_range(f, f0, cap)) { g.store(&C->fault_info, 2); continue; }
+      const double rl = P.rel[f];
       loc = rl < loc ? rl : loc;
     }
     asw += nAct;
     psw += nPend;
     const double tn = g.min_all(loc);
+    clk.lap(0);
     if (g.aborted()) { status = ST_BARRIER; break; }
+    if (g.load(&C->fault_info) != 0) { status = ST_OVERFLOW; break; }
     if (!(tn < INF)) break;
     if ((P.max_events > 0 && events >= P.max_events) || tn > P.until) {
       status = ST_STOPPED;
@@ -365,12 +679,13 @@ __device__ void event_loop(G& g, const Params& P, const int sc) {
     if (tid == 0) g.store(&C->cnt_comp[(q + 1) % 3], 0);
     int err = 0;
     // completions and advance
-    for (int i0 = w0; i0 < nAct; i0 += T) {
-      const int i = i0 + lane_id();
+    for (int base = b0; base < nAct; base += T) {
+      const int i = base + (int)threadIdx.x;
       bool done = false, keep = false;
       int f = -1;
-      if (i < nAct) {
-        f = actIn[i];
+      if (i < nAct) f = actIn[i];
+      if (i < nAct && !in_range(f, f0, cap)) err = 1;
+      if (i < nAct && in_range(f, f0, cap)) {
         const double dt = P.rem[f] / P.rate[f];
         const double tau = t + dt;
         if (tau <= thr) {
@@ -383,19 +698,22 @@ __device__ void event_loop(G& g, const Params& P, const int sc) {
           P.rem[f] = P.rem[f] - moved;
         }
       }
-      const int sd = wave_append(g, compCnt, done);
-      const int sk = wave_append(g, &C->cnt_act[ob], keep);
-      if (done) { if (sd < cap) compOut[sd] = f; else err = 1; }
-      if (keep) { if (sk < cap) actOut[sk] = f; else err = 1; }
+      int32_t* const cnts[2] = {compCnt, &C->cnt_act[ob]};
+      const bool pr[2] = {done, keep};
+      int slot[2];
+      block_append<2>(g, cnts, pr, slot);
+      if (done) { if (slot[0] < cap) compOut[slot[0]] = f; else err = 1; }
+      if (keep) { if (slot[1] < cap) actOut[slot[1]] = f; else err = 1; }
       if (done) g.store(&C->changed[ib], 1);
     }
     // releases due now
-    for (int i0 = w0; i0 < nPend; i0 += T) {
-      const int i = i0 + lane_id();
+    for (int base = b0; base < nPend; base += T) {
+      const int i = base + (int)threadIdx.x;
       bool zero = false, start = false, keep = false;
       int f = -1;
-      if (i < nPend) {
-        f = pendIn[i];
+      if (i < nPend) f = pendIn[i];
+      if (i < nPend && !in_range(f, f0, cap)) err = 1;
+      if (i < nPend && in_range(f, f0, cap)) {
         const double rl = P.rel[f];
         if (rl <= tn) {
           if (P.nbytes[f] == 0.0) {
@@ -410,46 +728,56 @@ __device__ void event_loop(G& g, const Params& P, const int sc) {
           keep = true;
         }
       }
-      const int sz = wave_append(g, compCnt, zero);
-      const int ss = wave_append(g, &C->cnt_act[ob], start);
-      const int sk = wave_append(g, &C->cnt_pend[ob], keep);
-      if (zero) { if (sz < cap) compOut[sz] = f; else err = 1; }
-      if (start) { if (ss < cap) actOut[ss] = f; else err = 1; g.store(&C->changed[ib], 1); }
-      if (keep) { if (sk < cap) pendOut[sk] = f; else err = 1; }
+      int32_t* const cnts[3] = {compCnt, &C->cnt_act[ob], &C->cnt_pend[ob]};
+      const bool pr[3] = {zero, start, keep};
+      int slot[3];
+      block_append<3>(g, cnts, pr, slot);
+      if (zero) { if (slot[0] < cap) compOut[slot[0]] = f; else err = 1; }
+      if (start) { if (slot[1] < cap) actOut[slot[1]] = f; else err = 1; g.store(&C->changed[ib], 1); }
+      if (keep) { if (slot[2] < cap) pendOut[slot[2]] = f; else err = 1; }
     }
     if (err) g.store(&C->fault_info, 2);
     g.sync();
     t = tn;
     q += 1;
-    // dependants of finished flows, to a fixpoint through zero-byte flows
+    // dependants of finished flows, to a fixpoint through zero-byte flows.
+    // A lane releases the successors of its own finished flow when it has a
+    // few; long successor lists (a barrier's) are shared by the whole wave.
     int nc = g.load(&C->cnt_comp[(q - 1) % 3]);
     while (nc > 0) {
       const int32_t* cin = comp[(q - 1) % 3];
       int32_t* cout = comp[q % 3];
       int32_t* coutCnt = &C->cnt_comp[q % 3];
       if (tid == 0) g.store(&C->cnt_comp[(q + 1) % 3], 0);
-      for (int i = tid; i < nc; i += T) {
-        const int f = cin[i];
-        for (int k = P.soff[f]; k < P.soff[f + 1]; ++k) {
-          const int h = P.succ[k];
-          if (g.add(&P.cnt[h], -1) != 1) continue;
-          const double rl = P.start[h] + t;
-          if (rl <= t) {
-            if (P.nbytes[h] == 0.0) {
-              P.finish[h] = rl;
-              const int s = g.add(coutCnt, 1);
-              if (s < cap) cout[s] = h; else err = 1;
-            } else {
-              P.rem[h] = P.nbytes[h];
-              for (int j = P.poff[h]; j < P.poff[h + 1]; ++j) g.add(&P.nact[P.plink[j]], 1);
-              const int s = g.add(&C->cnt_act[ob], 1);
-              if (s < cap) actOut[s] = h; else err = 1;
-              g.store(&C->changed[ib], 1);
-            }
+      for (int i0 = w0; i0 < nc; i0 += T) {
+        const int i = i0 + lane_id();
+        int k0 = 0, k1 = 0;
+        if (i < nc) {
+          const int f = cin[i];
+          if (in_range(f, f0, cap)) {
+            k0 = P.soff[f];
+            k1 = P.soff[f + 1];
           } else {
-            P.rel[h] = rl;
-            const int s = g.add(&C->cnt_pend[ob], 1);
-            if (s < cap) pendOut[s] = h; else err = 1;
+            err = 1;
+          }
+        }
+        const bool big = k1 - k0 > 8;
+        if (!big) {
+          for (int k = k0; k < k1; ++k) {
+            const int h = P.succ[k];
+            if (g.add(&P.cnt[h], -1) == 1)
+              release_one(g, P, C, h, t, ob, ib, actOut, pendOut, cout, coutCnt, cap, err);
+          }
+        }
+        uint64_t mask = __ballot(big);
+        while (mask) {
+          const int j = __ffsll((unsigned long long)mask) - 1;
+          mask &= mask - 1;
+          const int a = __shfl(k0, j, 64), z = __shfl(k1, j, 64);
+          for (int k = a + lane_id(); k < z; k += 64) {
+            const int h = P.succ[k];
+            if (g.add(&P.cnt[h], -1) == 1)
+              release_one(g, P, C, h, t, ob, ib, actOut, pendOut, cout, coutCnt, cap, err);
           }
         }
       }
@@ -458,12 +786,15 @@ __device__ void event_loop(G& g, const Params& P, const int sc) {
       q += 1;
       nc = g.load(&C->cnt_comp[(q - 1) % 3]);
     }
+    clk.lap(1);
     if (g.aborted()) { status = ST_BARRIER; break; }
     if (g.load(&C->fault_info) != 0) { status = ST_OVERFLOW; break; }
     const int nNew = g.load(&C->cnt_act[ob]);
     const int pNew = g.load(&C->cnt_pend[ob]);
     if (g.load(&C->changed[ib]) && nNew > 0) {
-      const int rc = solve(g, P, C, actOut, nNew, unf_a, unf_b, cap, rounds, fsw, isw);
+      const int rc = (P.lds_ok && nNew <= g.nblocks() * LDS_FLOWS)
+                         ? solve_lds(g, P, C, actOut, nNew, rounds, fsw, isw, clk, S)
+                         : solve(g, P, C, actOut, nNew, unf_a, unf_b, cap, rounds, fsw, isw, clk);
       solves += 1;
       if (rc != 0) { status = rc; break; }
     }
@@ -481,24 +812,29 @@ __device__ void event_loop(G& g, const Params& P, const int sc) {
     C->active_swept = asw;
     C->pending_swept = psw;
     C->status = status;
+    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)clk.acc[k];
   }
 }
 
 template <class G>
-__device__ void solve_only(G& g, const Params& P, const int sc) {
+__device__ void solve_only(G& g, const Params& P, const int sc, SolveLds& S) {
   ScenCtl* C = &P.ctl[sc];
   const int f0 = C->f0;
   int64_t rounds = 0, fsw = 0, isw = 0;
+  Clock clk(g.tid() == 0, S.clk);
   int rc = 0;
   if (C->n_solve > 0)
-    rc = solve(g, P, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0, rounds,
-               fsw, isw);
+    rc = (P.lds_ok && C->n_solve <= g.nblocks() * LDS_FLOWS)
+             ? solve_lds(g, P, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, S)
+             : solve(g, P, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0,
+                     rounds, fsw, isw, clk);
   g.add(&C->incidences_swept, isw);
   if (g.tid() == 0) {
     C->solves = C->n_solve > 0 ? 1 : 0;
     C->rounds = rounds;
     C->flows_swept = fsw;
     C->status = rc;
+    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)clk.acc[k];
   }
 }
 
@@ -506,21 +842,26 @@ __device__ void solve_only(G& g, const Params& P, const int sc) {
 
 __global__ __launch_bounds__(1024) void netsim_block_kernel(Params P) {
   __shared__ double lds[32];
-  BlockG g{lds};
+  __shared__ int ldsi[64];
+  __shared__ SolveLds S;
+  BlockG g{lds, ldsi};
   for (int sc = blockIdx.x; sc < P.num_scen; sc += gridDim.x) {
-    if (P.mode == 0) event_loop(g, P, sc);
-    else solve_only(g, P, sc);
+    if (P.mode == 0) event_loop(g, P, sc, S);
+    else solve_only(g, P, sc, S);
     __syncthreads();
   }
 }
 
 __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   __shared__ double lds[32];
+  __shared__ int ldsi[64];
   __shared__ int flag;
-  GridG g{lds, &flag, P.bar, P.slots, 0u, 0u, false};
+  __shared__ SolveLds S;
+  GridG g{lds, ldsi, &flag, P.bar, P.slots, 0u, 0u, false, 0u, 0u, 0u};
+  g.init();
   for (int sc = 0; sc < P.num_scen; ++sc) {
-    if (P.mode == 0) event_loop(g, P, sc);
-    else solve_only(g, P, sc);
+    if (P.mode == 0) event_loop(g, P, sc, S);
+    else solve_only(g, P, sc, S);
     g.sync();
   }
 }

@@ -321,8 +321,7 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.mf, sizeof(double) * Fz},
       {(void**)&P.rel, sizeof(double) * Fz},
       {(void**)&P.cnt, sizeof(int32_t) * Fz},
-      {(void**)&P.Rres, sizeof(int64_t) * Lz},
-      {(void**)&P.nres, sizeof(int32_t) * Lz},
+      {(void**)&P.lst, sizeof(int64_t) * 2 * Lz},
       {(void**)&P.nact, sizeof(int32_t) * Lz},
       {(void**)&P.blocked0, Lz},
       {(void**)&P.blocked1, Lz},
@@ -336,7 +335,7 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.unf0, sizeof(int32_t) * Fz},
       {(void**)&P.unf1, sizeof(int32_t) * Fz},
       {(void**)&P.ctl, sizeof(ScenCtl) * (size_t)std::max<int32_t>(S, 1)},
-      {(void**)&P.bar, sizeof(uint32_t) * 64},
+      {(void**)&P.bar, sizeof(uint32_t) * 1024},
       {(void**)&P.slots, sizeof(uint64_t) * 8},
   };
   size_t total = 0;
@@ -368,6 +367,9 @@ netsim_status prepare(netsim_t* h) {
     if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (upload)");
   }
   P.num_scen = S;
+  int64_t max_deg = 0;
+  for (int64_t d = 0; d < F; ++d) max_deg = std::max<int64_t>(max_deg, poff[(size_t)d + 1] - poff[(size_t)d]);
+  P.lds_ok = max_deg <= 6 ? 1 : 0;
   P.scale = h->scale;
   P.inv_scale = 1.0 / h->scale;
   h->prepared = true;
@@ -399,7 +401,7 @@ netsim_status reset_state(netsim_t* h, hipStream_t st) {
   }
   he = hipMemsetAsync(P.nact, 0, sizeof(int32_t) * Lz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.rate, 0, sizeof(double) * Fz, st);
-  if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 64, st);
+  if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 1024, st);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemsetAsync (reset)");
   he = hipStreamSynchronize(st);
   if (he != hipSuccess) return hip_fail(h, he, "hipStreamSynchronize (reset)");
@@ -460,7 +462,7 @@ netsim_status collect(netsim_t* h, std::vector<ScenCtl>* ctl_out) {
     if (st < 0) {
       std::string why = st == netsim_dev::ST_ROUNDS ? "round watchdog fired"
                         : st == netsim_dev::ST_BARRIER ? "grid barrier timed out"
-                        : st == netsim_dev::ST_OVERFLOW ? "work list overflow"
+                        : st == netsim_dev::ST_OVERFLOW ? "work list fault"
                                                         : "non-positive fair share";
       return fail(h, st == netsim_dev::ST_ROUNDS ? NETSIM_E_LIMIT : NETSIM_E_DEVICE,
                   "device solver fault in scenario " + std::to_string(s) + ": " + why);
@@ -710,6 +712,11 @@ netsim_status netsim_run(netsim_t* h, void* hip_stream) {
     s.sim_time = std::max(s.sim_time, c.t);
     if (c.status != 0) s.complete = 0;
   }
+  int khz = 0;
+  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->opt.device) != hipSuccess || khz <= 0)
+    khz = 100000;
+  for (int32_t k = 0; k < S; ++k)
+    for (int j = 0; j < 8; ++j) s.phase_seconds[j] += (double)ctl[(size_t)k].ticks[j] / (1e3 * khz);
   s.device_seconds = ms * 1e-3;
   s.upload_seconds = std::chrono::duration<double>(t1 - t0).count();
   h->stats = s;
@@ -801,6 +808,10 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, con
   h->stats.incidences_swept = out[(size_t)scen].incidences_swept;
   h->stats.device_seconds = ms * 1e-3;
   h->stats.complete = 1;
+  int khz = 0;
+  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->opt.device) != hipSuccess || khz <= 0)
+    khz = 100000;
+  for (int j = 0; j < 8; ++j) h->stats.phase_seconds[j] = (double)out[(size_t)scen].ticks[j] / (1e3 * khz);
   return NETSIM_OK;
 }
 

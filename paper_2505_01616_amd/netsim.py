@@ -56,10 +56,12 @@ class netsim_stats(ctypes.Structure):
                 ("pending_swept", ctypes.c_int64), ("completed_flows", ctypes.c_int64),
                 ("complete", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("sim_time", ctypes.c_double), ("device_seconds", ctypes.c_double),
-                ("upload_seconds", ctypes.c_double)]
+                ("upload_seconds", ctypes.c_double), ("phase_seconds", ctypes.c_double * 8)]
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        d["phase_seconds"] = list(self.phase_seconds)
+        return d
 
 
 class NetsimError(RuntimeError):
