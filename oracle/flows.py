@@ -4,7 +4,7 @@ TEST INFRASTRUCTURE (see ``oracle/__init__.py``).
 
 The paper models each collective by the communication pattern NCCL would
 use, all-reduce as a ring (Section 4.1, netsim description; Section 6
-calls it the simple ring algorithm).  Reading taken here, for a ring over
+describes it as a plain ring algorithm).  Reading taken here, for a ring over
 ranks r_0..r_{p-1} of S bytes in total:
 
   * all-reduce has 2(p-1) steps, reduce-scatter and all-gather p-1 steps;

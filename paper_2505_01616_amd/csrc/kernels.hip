@@ -1,7 +1,7 @@
 // Device-resident event loop and max-min rate solver for gfx950.
 //
 // Model (paper Section 4.1, netsim; Section 4.2, time rollback and the
-// iterative water-filling solve): the active flows share link bandwidth
+// water-filling rate solve): the active flows share link bandwidth
 // max-min fairly; rates are constant between events; the loop jumps to the
 // next completion or release, settles completions, releases dependants and
 // re-solves.
