@@ -5,12 +5,12 @@
  * CPU-baseline leg load this file's library; the simulator library and its
  * GPU kernels share no code with it.
  *
- * What it computes (Section 4.1, netsim; Section 4.2, "Network simulator
- * with time rollback"): flows of given sizes are released over links of
- * given capacities; between consecutive events every flow keeps a constant
- * rate; the rates are the max-min fair (per-flow fairness) allocation of
- * the active flows, found by progressive filling ("iterative
- * water-filling": find the bottleneck, give its flows their share, repeat).
+ * What it computes (Section 4.1, netsim; Section 4.2, the paragraph on the
+ * network simulator with time rollback): flows of given sizes are released
+ * over links of given capacities; between consecutive events every flow
+ * keeps a constant rate; the rates are the max-min fair (per-flow fairness)
+ * allocation of the active flows, found by progressive filling
+ * (water-filling: find the bottleneck, give its flows their share, repeat).
  * The output is every flow's completion time.
  *
  * Rate solve, over the active set U with paths P_f and capacities c_l:
