@@ -3,8 +3,8 @@
  * sharing, solved on an AMD Instinct MI355X (gfx950).
  *
  * What is computed (the communication-time model of the paper's simulator:
- * Section 4.1, the "netsim" description, and Section 4.2, "Network
- * simulator with time rollback"):
+ * Section 4.1, the description of netsim, and Section 4.2, the paragraph on
+ * the network simulator with time rollback):
  *   - collectives are decomposed into point-to-point flows over a cluster
  *     topology (ring all-reduce / reduce-scatter / all-gather as NCCL's ring
  *     would run them, all-to-all, pipeline send/recv);
