@@ -29,6 +29,9 @@ struct ScenCtl {
   int32_t cnt_unf[2];
   int32_t changed[2];
   int32_t rem3[3];         // shared-memory solve: unfrozen flows left, rotating
+  int32_t cnt_arr;         // flows activated in the current event
+  int32_t succ_flag[2];    // a flow finished in this event has dependants
+  int32_t solve_rc;        // status of a solve run by one workgroup
 };
 
 enum : int32_t {
@@ -64,6 +67,7 @@ struct Params {
   double* mf;              // [F] smallest fair share on the path (current round)
   double* rel;             // [F] release time (pending flows)
   int32_t* cnt;            // [F] predecessors not yet finished
+  int32_t* born;           // [F] event index at activation (-1 before)
   // dynamic link state
   int64_t* lst;            // [2L] per link: residual capacity (fixed point), unfrozen flows
   int32_t* nact;           // [L] active flows
@@ -74,6 +78,7 @@ struct Params {
   int32_t* pend0; int32_t* pend1;
   int32_t* comp0; int32_t* comp1; int32_t* comp2;
   int32_t* unf0; int32_t* unf1;
+  int32_t* arr;            // flows activated in the current event
   ScenCtl* ctl;            // [num_scen]
   uint32_t* bar;           // grid barrier words [1024] (layout in kernels.hip)
   uint64_t* slots;         // grid min-reduction slots [4]

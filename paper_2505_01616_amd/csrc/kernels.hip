@@ -120,7 +120,7 @@ struct GridG {
 
   // Waits (thread 0 only) until *p != g; gives up on the abort flag or after
   // BARRIER_TIMEOUT_TICKS, raising the flag.  Returns false if it gave up.
-  __device__ bool wait_change(uint32_t* p, uint32_t g) {
+  __device__ __forceinline__ bool wait_change(uint32_t* p, uint32_t g) {
     const uint64_t t0 = wall_clock64();
     while (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == g) {
       __builtin_amdgcn_s_sleep(1);
@@ -136,7 +136,7 @@ struct GridG {
 
   // Once per launch: every block counts itself on its XCD, then one flat
   // barrier, after which each block knows how many blocks share its XCD.
-  __device__ void init() {
+  __device__ __forceinline__ void init() {
     __shared__ uint32_t s_mine, s_nx;
     if (threadIdx.x == 0) {
       const uint32_t x = xcc_id();
@@ -172,7 +172,7 @@ struct GridG {
   // this cheaper than a flat barrier.  A block waiting longer than
   // BARRIER_TIMEOUT_TICKS raises the abort flag; thread 0 passes the flag to
   // its block through shared memory, so decisions on it are block-uniform.
-  __device__ void sync() {
+  __device__ __forceinline__ void sync() {
     __syncthreads();
     if (threadIdx.x == 0) {
       uint32_t a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -209,7 +209,7 @@ struct GridG {
   // Grid-wide minimum of non-negative doubles: block minimum, then an
   // atomic min on the bit pattern (ordered like the values) in one of four
   // rotating slots; block 0 resets the slot used three reductions later.
-  __device__ double min_all(double v) {
+  __device__ __forceinline__ double min_all(double v) {
     v = wave_min(v);
     const int w = threadIdx.x >> 6;
     if (lane_id() == 0) lds[w] = v;
@@ -265,7 +265,7 @@ __device__ __forceinline__ int wave_append(G& g, int32_t* counter, bool pred) {
 template <int K, class G>
 __device__ __forceinline__ void block_append(G& g, int32_t* const* counters, const bool* pred,
                                              int* slot) {
-  int* sh = g.ldsi;  // [K*16] per-wave counts, [48 + k] list bases
+  int* sh = g.ldsi;  // [K*16] per-wave counts (K <= 4), [96 + k] list bases
   const int lane = lane_id(), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   uint64_t mask[K];
 #pragma unroll
@@ -274,21 +274,23 @@ __device__ __forceinline__ void block_append(G& g, int32_t* const* counters, con
     if (lane == 0) sh[k * 16 + w] = (int)__popcll(mask[k]);
   }
   __syncthreads();
-  if (threadIdx.x < K) {
-    const int k = threadIdx.x;
-    int total = 0;
-    for (int j = 0; j < nw; ++j) {
-      const int c = sh[k * 16 + j];
-      sh[k * 16 + j] = total;
-      total += c;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    if ((int)threadIdx.x == k) {
+      int total = 0;
+      for (int j = 0; j < nw; ++j) {
+        const int c = sh[k * 16 + j];
+        sh[k * 16 + j] = total;
+        total += c;
+      }
+      sh[96 + k] = total ? g.add(counters[k], (int32_t)total) : 0;
     }
-    sh[48 + k] = total ? g.add(counters[k], (int32_t)total) : 0;
   }
   __syncthreads();
   const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
   for (int k = 0; k < K; ++k)
-    slot[k] = pred[k] ? sh[48 + k] + sh[k * 16 + w] + (int)__popcll(mask[k] & below) : -1;
+    slot[k] = pred[k] ? sh[96 + k] + sh[k * 16 + w] + (int)__popcll(mask[k] & below) : -1;
   __syncthreads();
 }
 
@@ -326,15 +328,17 @@ __device__ __forceinline__ double share(const Params& P, int l) {
 // Max-min rates of the n0 flows listed in list0 (all active).  Link state is
 // initialised from nact.  Returns 0 or a negative status.
 template <class G>
-__device__ int solve(G& g, const Params& P, ScenCtl* C, const int32_t* list0, int n0,
+__device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const int32_t* list0, int n0,
                      int32_t* unf_a, int32_t* unf_b, int cap, int64_t& rounds, int64_t& fsw,
-                     int64_t& isw, Clock& clk) {
+                     int64_t& isw, Clock& clk, bool warm) {
   const int T = g.nthr();
   const int tid = g.tid();
   const int b0 = g.block_base();
   for (int l = C->l0 + tid; l < C->l1; l += T) {
-    P.lst[2 * l] = P.R0[l];
-    P.lst[2 * l + 1] = P.nact[l];
+    if (!warm) {
+      P.lst[2 * l] = P.R0[l];
+      P.lst[2 * l + 1] = P.nact[l];
+    }
     P.blocked0[l] = 0;
     P.blocked1[l] = 0;
   }
@@ -463,8 +467,9 @@ struct SolveLds {
 };
 
 template <class G>
-__device__ int solve_lds(G& g, const Params& P, ScenCtl* C, const int32_t* list0, int n0,
-                         int64_t& rounds, int64_t& fsw, int64_t& isw, Clock& clk, SolveLds& S) {
+__device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, const int32_t* list0, int n0,
+                         int64_t& rounds, int64_t& fsw, int64_t& isw, Clock& clk, SolveLds& S,
+                         bool warm) {
   const int T = g.nthr();
   const int tid = g.tid();
   const int nb = g.nblocks();
@@ -472,8 +477,10 @@ __device__ int solve_lds(G& g, const Params& P, ScenCtl* C, const int32_t* list0
   const int c0 = min(n0, g.block_id() * per);
   const int nl = min(n0, c0 + per) - c0;
   for (int l = C->l0 + tid; l < C->l1; l += T) {
-    P.lst[2 * l] = P.R0[l];
-    P.lst[2 * l + 1] = P.nact[l];
+    if (!warm) {
+      P.lst[2 * l] = P.R0[l];
+      P.lst[2 * l + 1] = P.nact[l];
+    }
     P.blocked0[l] = 0;
     P.blocked1[l] = 0;
   }
@@ -589,8 +596,9 @@ __device__ int solve_lds(G& g, const Params& P, ScenCtl* C, const int32_t* list0
 // Releases flow h whose last predecessor finished at t (called once per h).
 template <class G>
 __device__ __forceinline__ void release_one(G& g, const Params& P, ScenCtl* C, int h, double t,
-                                            int ob, int ib, int32_t* actOut, int32_t* pendOut,
-                                            int32_t* cout, int32_t* coutCnt, int cap, int& err) {
+                                            int ob, int ib, int ev, int32_t* actOut,
+                                            int32_t* pendOut, int32_t* arrOut, int32_t* cout,
+                                            int32_t* coutCnt, int cap, int& err) {
   const double rl = P.start[h] + t;
   if (rl <= t) {
     if (P.nbytes[h] == 0.0) {
@@ -599,9 +607,12 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, ScenCtl* C, i
       if (s < cap) cout[s] = h; else err = 1;
     } else {
       P.rem[h] = P.nbytes[h];
+      P.born[h] = ev;
       for (int j = P.poff[h]; j < P.poff[h + 1]; ++j) g.add(&P.nact[P.plink[j]], 1);
       const int s = g.add(&C->cnt_act[ob], 1);
       if (s < cap) actOut[s] = h; else err = 1;
+      const int a = g.add(&C->cnt_arr, 1);
+      if (a < cap) arrOut[a] = h; else err = 1;
       g.store(&C->changed[ib], 1);
     }
   } else {
@@ -612,8 +623,23 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, ScenCtl* C, i
 }
 
 // ------------------------------------------------------------- event loop
+// Incremental re-solve.  At the end of every solve all active flows are
+// frozen: each link holds R0 minus the fixed-point rates of its active flows
+// and an unfrozen count of zero.  When an event finishes flows with rates
+// r_c and activates flows g, progressive filling on the new active set agrees
+// with the previous one on every bottleneck level below
+//   theta = min( min_c r_c, min over links l of every g of c_l / n_l(new) ):
+// a finished flow's links were never bottlenecks below its rate, and a link
+// of a new flow cannot reach a share below its initial share.  So every flow
+// whose rate is below theta keeps it; the others (and the new flows) have
+// their contributions taken back and are re-solved from that state.  Rates
+// are identical to a full re-solve in exact arithmetic, and kept flows keep
+// their bits.  Re-solves that fit in one workgroup's shared memory run on
+// workgroup 0 alone, with workgroup barriers.
+constexpr double KEEP = 1.0 - 1e-9;  // safety margin below theta
+
 template <class G>
-__device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
+__device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
   ScenCtl* C = &P.ctl[sc];
   const int f0 = C->f0;
   const int cap = C->f1 - C->f0;
@@ -622,11 +648,19 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
   int32_t* comp[3] = {P.comp0 + f0, P.comp1 + f0, P.comp2 + f0};
   int32_t* unf_a = P.unf0 + f0;
   int32_t* unf_b = P.unf1 + f0;
+  int32_t* arrs = P.arr + f0;
   const int T = g.nthr();
   const int tid = g.tid();
   const int b0 = g.block_base();
   const int w0 = tid - lane_id();
   Clock clk(tid == 0, S.clk);
+  // links at rest: nothing active
+  for (int l = C->l0 + tid; l < C->l1; l += T) {
+    P.lst[2 * l] = P.R0[l];
+    P.lst[2 * l + 1] = 0;
+    P.blocked0[l] = 0;
+    P.blocked1[l] = 0;
+  }
   double t = 0.0;
   int64_t events = 0, solves = 0, rounds = 0, fsw = 0, isw = 0, asw = 0, psw = 0;
   int nAct = 0;
@@ -644,6 +678,8 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
       g.store(&C->cnt_act[ob], 0);
       g.store(&C->cnt_pend[ob], 0);
       g.store(&C->changed[ib], 0);
+      g.store(&C->succ_flag[ib], 0);
+      g.store(&C->cnt_arr, 0);
     }
     // next event time: earliest completion or release
     double loc = INF;
@@ -678,6 +714,7 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
     int32_t* compCnt = &C->cnt_comp[q % 3];
     if (tid == 0) g.store(&C->cnt_comp[(q + 1) % 3], 0);
     int err = 0;
+    double rmin_done = INF;  // smallest rate among flows finishing now
     // completions and advance
     for (int base = b0; base < nAct; base += T) {
       const int i = base + (int)threadIdx.x;
@@ -686,15 +723,23 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
       if (i < nAct) f = actIn[i];
       if (i < nAct && !in_range(f, f0, cap)) err = 1;
       if (i < nAct && in_range(f, f0, cap)) {
-        const double dt = P.rem[f] / P.rate[f];
+        const double r = P.rate[f];
+        const double dt = P.rem[f] / r;
         const double tau = t + dt;
         if (tau <= thr) {
           done = true;
           P.finish[f] = tn;
-          for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) g.add(&P.nact[P.plink[k]], -1);
+          rmin_done = r < rmin_done ? r : rmin_done;
+          const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
+          for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+            const int l = P.plink[k];
+            g.add(&P.nact[l], -1);
+            g.add(&P.lst[2 * l], qv);  // its share returns to the link
+          }
+          if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
         } else {
           keep = true;
-          const double moved = P.rate[f] * step;
+          const double moved = r * step;
           P.rem[f] = P.rem[f] - moved;
         }
       }
@@ -719,31 +764,37 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
           if (P.nbytes[f] == 0.0) {
             zero = true;
             P.finish[f] = rl;
+            if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
           } else {
             start = true;
             P.rem[f] = P.nbytes[f];
+            P.born[f] = e;
             for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) g.add(&P.nact[P.plink[k]], 1);
           }
         } else {
           keep = true;
         }
       }
-      int32_t* const cnts[3] = {compCnt, &C->cnt_act[ob], &C->cnt_pend[ob]};
-      const bool pr[3] = {zero, start, keep};
-      int slot[3];
-      block_append<3>(g, cnts, pr, slot);
+      int32_t* const cnts[4] = {compCnt, &C->cnt_act[ob], &C->cnt_pend[ob], &C->cnt_arr};
+      const bool pr[4] = {zero, start, keep, start};
+      int slot[4];
+      block_append<4>(g, cnts, pr, slot);
       if (zero) { if (slot[0] < cap) compOut[slot[0]] = f; else err = 1; }
-      if (start) { if (slot[1] < cap) actOut[slot[1]] = f; else err = 1; g.store(&C->changed[ib], 1); }
+      if (start) {
+        if (slot[1] < cap) actOut[slot[1]] = f; else err = 1;
+        if (slot[3] < cap) arrs[slot[3]] = f; else err = 1;
+        g.store(&C->changed[ib], 1);
+      }
       if (keep) { if (slot[2] < cap) pendOut[slot[2]] = f; else err = 1; }
     }
     if (err) g.store(&C->fault_info, 2);
-    g.sync();
+    const double rdone = g.min_all(rmin_done);
     t = tn;
     q += 1;
     // dependants of finished flows, to a fixpoint through zero-byte flows.
     // A lane releases the successors of its own finished flow when it has a
     // few; long successor lists (a barrier's) are shared by the whole wave.
-    int nc = g.load(&C->cnt_comp[(q - 1) % 3]);
+    int nc = g.load(&C->succ_flag[ib]) ? g.load(&C->cnt_comp[(q - 1) % 3]) : 0;
     while (nc > 0) {
       const int32_t* cin = comp[(q - 1) % 3];
       int32_t* cout = comp[q % 3];
@@ -766,7 +817,8 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
           for (int k = k0; k < k1; ++k) {
             const int h = P.succ[k];
             if (g.add(&P.cnt[h], -1) == 1)
-              release_one(g, P, C, h, t, ob, ib, actOut, pendOut, cout, coutCnt, cap, err);
+              release_one(g, P, C, h, t, ob, ib, e, actOut, pendOut, arrs, cout, coutCnt, cap,
+                          err);
           }
         }
         uint64_t mask = __ballot(big);
@@ -777,7 +829,8 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
           for (int k = a + lane_id(); k < z; k += 64) {
             const int h = P.succ[k];
             if (g.add(&P.cnt[h], -1) == 1)
-              release_one(g, P, C, h, t, ob, ib, actOut, pendOut, cout, coutCnt, cap, err);
+              release_one(g, P, C, h, t, ob, ib, e, actOut, pendOut, arrs, cout, coutCnt, cap,
+                          err);
           }
         }
       }
@@ -792,10 +845,76 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
     const int nNew = g.load(&C->cnt_act[ob]);
     const int pNew = g.load(&C->cnt_pend[ob]);
     if (g.load(&C->changed[ib]) && nNew > 0) {
-      const int rc = (P.lds_ok && nNew <= g.nblocks() * LDS_FLOWS)
-                         ? solve_lds(g, P, C, actOut, nNew, rounds, fsw, isw, clk, S)
-                         : solve(g, P, C, actOut, nNew, unf_a, unf_b, cap, rounds, fsw, isw, clk);
-      solves += 1;
+      // theta: below it every rate stays as it was
+      double theta = rdone;
+      const int nArr = g.load(&C->cnt_arr);
+      if (nArr > 0) {
+        double lo = INF;
+        for (int i = tid; i < nArr; i += T) {
+          const int f = arrs[i];
+          if (!in_range(f, f0, cap)) continue;
+          for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+            const int l = P.plink[k];
+            const double s0 = ((double)P.R0[l] / (double)P.nact[l]) * P.inv_scale;
+            lo = s0 < lo ? s0 : lo;
+          }
+        }
+        const double ta = g.min_all(lo);
+        theta = ta < theta ? ta : theta;
+      }
+      const double keep_below = theta * KEEP;
+      // take back the flows at or above theta (and the new ones) for re-solving
+      if (tid == 0) g.store(&C->cnt_unf[0], 0);
+      g.sync();
+      for (int base = b0; base < nNew; base += T) {
+        const int i = base + (int)threadIdx.x;
+        bool upper = false;
+        int f = -1;
+        if (i < nNew) {
+          f = actOut[i];
+          if (in_range(f, f0, cap)) {
+            const bool fresh = P.born[f] == e;
+            const double r = P.rate[f];
+            upper = fresh || !(r < keep_below);
+            if (upper) {
+              const int64_t qv = fresh ? 0 : (int64_t)__builtin_rint(r * P.scale);
+              for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+                const int l = P.plink[k];
+                if (!fresh) g.add(&P.lst[2 * l], qv);
+                g.add(&P.lst[2 * l + 1], (int64_t)1);
+              }
+            }
+          } else {
+            err = 1;
+          }
+        }
+        int32_t* const cnts[1] = {&C->cnt_unf[0]};
+        const bool pr[1] = {upper};
+        int slot[1];
+        block_append<1>(g, cnts, pr, slot);
+        if (upper) { if (slot[0] < cap) arrs[slot[0]] = f; else err = 1; }
+      }
+      if (err) g.store(&C->fault_info, 2);
+      g.sync();
+      clk.lap(7);
+      const int nSel = g.load(&C->cnt_unf[0]);
+      int rc = 0;
+      if (nSel > 0) {
+        if (P.lds_ok && nSel <= LDS_FLOWS) {
+          if (g.block_id() == 0) {
+            BlockG b{g.lds, g.ldsi};
+            const int r1 = solve_lds(b, P, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
+            if (threadIdx.x == 0) g.store(&C->solve_rc, r1);
+          }
+          g.sync();
+          rc = g.load(&C->solve_rc);
+        } else if (P.lds_ok && nSel <= g.nblocks() * LDS_FLOWS) {
+          rc = solve_lds(g, P, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
+        } else {
+          rc = solve(g, P, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
+        }
+      }
+      solves += 1;  // the active set changed: one rate solve (possibly empty)
       if (rc != 0) { status = rc; break; }
     }
     nAct = nNew;
@@ -812,12 +931,12 @@ __device__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
     C->active_swept = asw;
     C->pending_swept = psw;
     C->status = status;
-    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)clk.acc[k];
+    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)S.clk[k];
   }
 }
 
 template <class G>
-__device__ void solve_only(G& g, const Params& P, const int sc, SolveLds& S) {
+__device__ __forceinline__ void solve_only(G& g, const Params& P, const int sc, SolveLds& S) {
   ScenCtl* C = &P.ctl[sc];
   const int f0 = C->f0;
   int64_t rounds = 0, fsw = 0, isw = 0;
@@ -825,16 +944,16 @@ __device__ void solve_only(G& g, const Params& P, const int sc, SolveLds& S) {
   int rc = 0;
   if (C->n_solve > 0)
     rc = (P.lds_ok && C->n_solve <= g.nblocks() * LDS_FLOWS)
-             ? solve_lds(g, P, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, S)
+             ? solve_lds(g, P, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, S, false)
              : solve(g, P, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0,
-                     rounds, fsw, isw, clk);
+                     rounds, fsw, isw, clk, false);
   g.add(&C->incidences_swept, isw);
   if (g.tid() == 0) {
     C->solves = C->n_solve > 0 ? 1 : 0;
     C->rounds = rounds;
     C->flows_swept = fsw;
     C->status = rc;
-    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)clk.acc[k];
+    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)S.clk[k];
   }
 }
 
@@ -842,7 +961,7 @@ __device__ void solve_only(G& g, const Params& P, const int sc, SolveLds& S) {
 
 __global__ __launch_bounds__(1024) void netsim_block_kernel(Params P) {
   __shared__ double lds[32];
-  __shared__ int ldsi[64];
+  __shared__ int ldsi[128];
   __shared__ SolveLds S;
   BlockG g{lds, ldsi};
   for (int sc = blockIdx.x; sc < P.num_scen; sc += gridDim.x) {
@@ -854,7 +973,7 @@ __global__ __launch_bounds__(1024) void netsim_block_kernel(Params P) {
 
 __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   __shared__ double lds[32];
-  __shared__ int ldsi[64];
+  __shared__ int ldsi[128];
   __shared__ int flag;
   __shared__ SolveLds S;
   GridG g{lds, ldsi, &flag, P.bar, P.slots, 0u, 0u, false, 0u, 0u, 0u};

@@ -321,6 +321,8 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.mf, sizeof(double) * Fz},
       {(void**)&P.rel, sizeof(double) * Fz},
       {(void**)&P.cnt, sizeof(int32_t) * Fz},
+      {(void**)&P.born, sizeof(int32_t) * Fz},
+      {(void**)&P.arr, sizeof(int32_t) * Fz},
       {(void**)&P.lst, sizeof(int64_t) * 2 * Lz},
       {(void**)&P.nact, sizeof(int32_t) * Lz},
       {(void**)&P.blocked0, Lz},
@@ -400,6 +402,7 @@ netsim_status reset_state(netsim_t* h, hipStream_t st) {
     if (he != hipSuccess) return hip_fail(h, he, "hipMemcpyAsync (reset)");
   }
   he = hipMemsetAsync(P.nact, 0, sizeof(int32_t) * Lz, st);
+  if (he == hipSuccess) he = hipMemsetAsync(P.born, 0xFF, sizeof(int32_t) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.rate, 0, sizeof(double) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 1024, st);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemsetAsync (reset)");

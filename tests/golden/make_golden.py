@@ -1,0 +1,85 @@
+"""Writes the stored oracle values used by the full-size GPU parity tests.
+
+Calls only the oracle (``oracle/``) and the seeded workload generator.  Run
+from the repository root:  python tests/golden/make_golden.py [c3] [c5]
+
+c5_makespans.json   per-scenario makespan of all 256 C5 scenarios (fp64 oracle)
+c3_summary.json     C3 (full size): makespan, a seeded sample of per-flow
+                    finish times, and the oracle's own spread under one-ulp
+                    changes of every capacity (C3 is ill-conditioned in fp64)
+"""
+
+from __future__ import annotations
+
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+
+from oracle import flows as oflows  # noqa: E402
+from oracle import sim as osim  # noqa: E402
+from workloads import configs  # noqa: E402
+
+
+def c5():
+    prog = configs.c5(5)
+    out = []
+    t0 = time.time()
+    for s, sc in enumerate(prog.scenarios):
+        r = osim.run_scenario(sc)
+        out.append({"scenario": s, "makespan": r.makespan, "events": r.events,
+                    "solves": r.solves, "flows": int(len(r.finish))})
+    with open(os.path.join(HERE, "c5_makespans.json"), "w") as fh:
+        json.dump({"config": "c5 seed 5 (256 scenarios)", "writer": "tests/golden/make_golden.py",
+                   "scenarios": out}, fh, indent=0)
+    print(f"c5: {len(out)} scenarios in {time.time() - t0:.0f} s", flush=True)
+
+
+def _perturbed(fs, k):
+    cap = fs.cap.copy()
+    for _ in range(abs(k)):
+        cap = np.nextafter(cap, np.inf if k > 0 else 0.0)
+    return oflows.FlowSet(cap, fs.src, fs.dst, fs.nbytes, fs.start, fs.path_off, fs.path_link,
+                          fs.dep_off, fs.dep_ids)
+
+
+def c3():
+    t0 = time.time()
+    fs = oflows.expand(configs.c3(3).scenarios[0])
+    ref = osim.run_flowset(fs)
+    runs = [osim.run_flowset(_perturbed(fs, k)).finish for k in (-1, 1, 2)]
+    dev = np.max([np.abs(r - ref.finish) / ref.finish for r in runs], axis=0)
+    order = np.argsort(ref.finish)
+    bad = order[dev[order] > 1e-9]
+    horizon = float(ref.finish[bad[0]]) if len(bad) else float("inf")
+    rng = np.random.default_rng(33)
+    sample = np.sort(rng.choice(fs.F, size=4000, replace=False))
+    early = np.nonzero(ref.finish < horizon)[0]
+    early_sample = np.sort(rng.choice(early, size=min(2000, len(early)), replace=False))
+    data = {
+        "config": "c3 seed 3 (full size)", "writer": "tests/golden/make_golden.py",
+        "flows": int(fs.F), "events": ref.events, "solves": ref.solves,
+        "makespan": ref.makespan,
+        "ulp_spread_makespan": max(abs(float(np.max(r)) - ref.makespan) for r in runs) / ref.makespan,
+        "ulp_spread_q99": float(np.quantile(dev, 0.99)),
+        "horizon": horizon,
+        "sample_ids": sample.tolist(), "sample_finish": ref.finish[sample].tolist(),
+        "early_ids": early_sample.tolist(), "early_finish": ref.finish[early_sample].tolist(),
+    }
+    with open(os.path.join(HERE, "c3_summary.json"), "w") as fh:
+        json.dump(data, fh)
+    print(f"c3: {time.time() - t0:.0f} s, horizon {horizon:.4g}", flush=True)
+
+
+if __name__ == "__main__":
+    which = sys.argv[1:] or ["c5", "c3"]
+    if "c5" in which:
+        c5()
+    if "c3" in which:
+        c3()
