@@ -195,3 +195,52 @@ def test_c5_sample_batched():
     for s, sc in enumerate(program.scenarios):
         ref = osim.run_scenario(sc)
         assert _rel(fins[s], ref.finish) < TOL, s
+
+
+def _golden(name):
+    import json
+    import os
+    with open(os.path.join(os.path.dirname(__file__), "golden", name)) as fh:
+        return json.load(fh)
+
+
+def test_c5_full_batched():
+    """All 256 what-if scenarios in one batched run: per-scenario makespan
+    and event count against the stored oracle values."""
+    ns, pr = _gpu()
+    _say("test_c5_full_batched")
+    gold = _golden("c5_makespans.json")["scenarios"]
+    program = configs.c5(5)
+    ld = pr.load_program(program, ns.make_options())
+    try:
+        ns.netsim_run(ld.handle)
+        ms = ns.netsim_get_makespan(ld.handle, len(program.scenarios))
+        st = ns.netsim_get_stats(ld.handle)
+    finally:
+        ld.close()
+    want = np.array([g["makespan"] for g in gold])
+    assert _rel(ms, want) < TOL
+    assert st["events"] == sum(g["events"] for g in gold)
+    _say("c5 full: device s", st["device_seconds"], "events", st["events"])
+
+
+def test_c3_full_size():
+    """Full C3 (ill-conditioned in fp64): sampled flows finishing before the
+    oracle's one-ulp horizon agree to 1e-6; the makespan and the spread of a
+    seeded 4000-flow sample stay within 4x the oracle's own one-ulp spread."""
+    ns, pr = _gpu()
+    _say("test_c3_full_size")
+    gold = _golden("c3_summary.json")
+    program = configs.c3(3)
+    fins, st = pr.run_program(program, ns.make_options())
+    fin = fins[0]
+    assert len(fin) == gold["flows"]
+    early = np.array(gold["early_ids"])
+    assert _rel(fin[early], np.array(gold["early_finish"])) < TOL
+    gm = abs(np.max(fin) - gold["makespan"]) / gold["makespan"]
+    assert gm <= 4 * gold["ulp_spread_makespan"] + 1e-12
+    ids = np.array(gold["sample_ids"])
+    dev = np.abs(fin[ids] - np.array(gold["sample_finish"])) / np.array(gold["sample_finish"])
+    assert np.quantile(dev, 0.99) <= 4 * gold["ulp_spread_q99"] + 1e-12
+    _say(f"c3 full: makespan dev {gm:.2e} (oracle ulp spread {gold['ulp_spread_makespan']:.2e}), "
+         f"device s {st['device_seconds']:.2f}, events {st['events']} (oracle {gold['events']})")
