@@ -128,6 +128,8 @@ typedef struct {
   int64_t active_swept;      /* sum over events of active flows visited          */
   int64_t pending_swept;     /* sum over events of pending flows visited         */
   int64_t completed_flows;   /* flows with a finish time                         */
+  int64_t reselected;        /* sum over solves of flows whose rate was re-solved */
+  int64_t wide_solves;       /* solves too large for one workgroup's shared memory */
   int32_t complete;          /* 1 if every scenario ran to its end               */
   int32_t reserved;
   double sim_time;           /* largest simulated time reached over scenarios    */

@@ -14,11 +14,13 @@ struct ScenCtl {
   int32_t f0, f1;          // device flow range [f0, f1)
   int32_t l0, l1;          // device link range [l0, l1)
   int32_t n_pend0;         // flows initially pending (listed in pend0 + f0)
+  int32_t c0, nc;          // this scenario's components [c0, c0 + nc)
   int32_t n_solve;         // solve-once: active flows listed in act0 + f0
   // results
   double t;                // simulated time reached
   int64_t events, solves, rounds, flows_swept, incidences_swept;
   int64_t active_swept, pending_swept;
+  int64_t reselected, wide_solves;
   int32_t status;          // 0 ran to the end, 1 stopped at a limit, < 0 fault
   int32_t fault_info;
   int64_t ticks[8];        // wall-clock ticks per phase (first thread of the group)
@@ -68,6 +70,10 @@ struct Params {
   double* rel;             // [F] release time (pending flows)
   int32_t* cnt;            // [F] predecessors not yet finished
   int32_t* born;           // [F] event index at activation (-1 before)
+  const int32_t* comp;     // [F] component of the flow (flows of different
+                           //     components share no link)
+  uint64_t* theta;         // [C] per component: lowest level that may change
+                           //     in this event (bit pattern of a double)
   // dynamic link state
   int64_t* lst;            // [2L] per link: residual capacity (fixed point), unfrozen flows
   int32_t* nact;           // [L] active flows

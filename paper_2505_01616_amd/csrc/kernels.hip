@@ -89,6 +89,9 @@ struct BlockG {
   __device__ void store(T* p, T v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   }
+  __device__ void amin(uint64_t* p, uint64_t v) {
+    __hip_atomic_fetch_min(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
 };
 
 // Barrier words (uint32 indices into Params::bar, 64-byte lines apart):
@@ -241,6 +244,9 @@ struct GridG {
   template <class T>
   __device__ void store(T* p, T v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __device__ void amin(uint64_t* p, uint64_t v) {
+    __hip_atomic_fetch_min(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 };
 
@@ -454,7 +460,7 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
 // link state (residual capacity and count, blocked flags) and the rates go
 // through global memory, so a round costs one gather of link state, one of
 // flags and two barriers.
-constexpr int LDS_FLOWS = 1536;
+constexpr int LDS_FLOWS = 3584;
 constexpr int LDS_DEG = 6;
 
 struct SolveLds {
@@ -654,15 +660,18 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
   const int b0 = g.block_base();
   const int w0 = tid - lane_id();
   Clock clk(tid == 0, S.clk);
-  // links at rest: nothing active
+  // links at rest: nothing active; no component has changed yet
   for (int l = C->l0 + tid; l < C->l1; l += T) {
     P.lst[2 * l] = P.R0[l];
     P.lst[2 * l + 1] = 0;
     P.blocked0[l] = 0;
     P.blocked1[l] = 0;
   }
+  const uint64_t INF_BITS = (uint64_t)__double_as_longlong(INF);
+  for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
   double t = 0.0;
   int64_t events = 0, solves = 0, rounds = 0, fsw = 0, isw = 0, asw = 0, psw = 0;
+  int64_t sel = 0, wide = 0;
   int nAct = 0;
   int nPend = C->n_pend0;
   int e = 0;  // event index: lists act[e&1], pend[e&1] are this event's input
@@ -714,7 +723,6 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
     int32_t* compCnt = &C->cnt_comp[q % 3];
     if (tid == 0) g.store(&C->cnt_comp[(q + 1) % 3], 0);
     int err = 0;
-    double rmin_done = INF;  // smallest rate among flows finishing now
     // completions and advance
     for (int base = b0; base < nAct; base += T) {
       const int i = base + (int)threadIdx.x;
@@ -729,7 +737,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
         if (tau <= thr) {
           done = true;
           P.finish[f] = tn;
-          rmin_done = r < rmin_done ? r : rmin_done;
+          g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
           const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
           for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
             const int l = P.plink[k];
@@ -788,7 +796,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
       if (keep) { if (slot[2] < cap) pendOut[slot[2]] = f; else err = 1; }
     }
     if (err) g.store(&C->fault_info, 2);
-    const double rdone = g.min_all(rmin_done);
+    g.sync();
     t = tn;
     q += 1;
     // dependants of finished flows, to a fixpoint through zero-byte flows.
@@ -845,25 +853,23 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
     const int nNew = g.load(&C->cnt_act[ob]);
     const int pNew = g.load(&C->cnt_pend[ob]);
     if (g.load(&C->changed[ib]) && nNew > 0) {
-      // theta: below it every rate stays as it was
-      double theta = rdone;
+      // theta of each component: below it every rate stays as it was.
+      // Finished flows have fed it their rates; new flows feed the initial
+      // share of their links.
       const int nArr = g.load(&C->cnt_arr);
-      if (nArr > 0) {
+      for (int i = tid; i < nArr; i += T) {
+        const int f = arrs[i];
+        if (!in_range(f, f0, cap)) continue;
         double lo = INF;
-        for (int i = tid; i < nArr; i += T) {
-          const int f = arrs[i];
-          if (!in_range(f, f0, cap)) continue;
-          for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
-            const int l = P.plink[k];
-            const double s0 = ((double)P.R0[l] / (double)P.nact[l]) * P.inv_scale;
-            lo = s0 < lo ? s0 : lo;
-          }
+        for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+          const int l = P.plink[k];
+          const double s0 = ((double)P.R0[l] / (double)P.nact[l]) * P.inv_scale;
+          lo = s0 < lo ? s0 : lo;
         }
-        const double ta = g.min_all(lo);
-        theta = ta < theta ? ta : theta;
+        g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(lo));
       }
-      const double keep_below = theta * KEEP;
-      // take back the flows at or above theta (and the new ones) for re-solving
+      // take back the flows at or above their component's theta (and the new
+      // ones) for re-solving
       if (tid == 0) g.store(&C->cnt_unf[0], 0);
       g.sync();
       for (int base = b0; base < nNew; base += T) {
@@ -875,7 +881,8 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
           if (in_range(f, f0, cap)) {
             const bool fresh = P.born[f] == e;
             const double r = P.rate[f];
-            upper = fresh || !(r < keep_below);
+            const double th = __longlong_as_double((long long)g.load(&P.theta[P.comp[f]]));
+            upper = fresh || !(r < th * KEEP);
             if (upper) {
               const int64_t qv = fresh ? 0 : (int64_t)__builtin_rint(r * P.scale);
               for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
@@ -897,7 +904,10 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
       if (err) g.store(&C->fault_info, 2);
       g.sync();
       clk.lap(7);
+      for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
       const int nSel = g.load(&C->cnt_unf[0]);
+      sel += nSel;
+      wide += nSel > LDS_FLOWS ? 1 : 0;
       int rc = 0;
       if (nSel > 0) {
         if (P.lds_ok && nSel <= LDS_FLOWS) {
@@ -930,6 +940,8 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
     C->flows_swept = fsw;
     C->active_swept = asw;
     C->pending_swept = psw;
+    C->reselected = sel;
+    C->wide_solves = wide;
     C->status = status;
     for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)S.clk[k];
   }

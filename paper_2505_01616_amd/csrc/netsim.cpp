@@ -270,6 +270,46 @@ netsim_status prepare(netsim_t* h) {
     ndeps[(size_t)d] = (int32_t)(h->d_off[(size_t)id + 1] - h->d_off[(size_t)id]);
   }
   poff[(size_t)F] = (int32_t)e;
+  // components of the flow-link graph per scenario (union-find over links);
+  // flows of different components never share a link, so a change in one
+  // cannot move a rate in another.  More than kMaxComp components are merged
+  // into the last one (a coarser partition is still safe).
+  constexpr int32_t kMaxComp = 4096;
+  std::vector<int32_t> comp_of_dev((size_t)std::max<int64_t>(F, 1), 0);
+  int32_t ncomp_total = 0;
+  {
+    std::vector<int32_t> parent((size_t)std::max<int64_t>(ld, 1));
+    for (int64_t l = 0; l < ld; ++l) parent[(size_t)l] = (int32_t)l;
+    auto find = [&](int32_t x) {
+      while (parent[(size_t)x] != x) {
+        parent[(size_t)x] = parent[(size_t)parent[(size_t)x]];
+        x = parent[(size_t)x];
+      }
+      return x;
+    };
+    for (int64_t d = 0; d < F; ++d)
+      for (int32_t e = poff[(size_t)d] + 1; e < poff[(size_t)d + 1]; ++e) {
+        const int32_t a = find(plink[(size_t)poff[(size_t)d]]), b = find(plink[(size_t)e]);
+        if (a != b) parent[(size_t)std::max(a, b)] = std::min(a, b);
+      }
+    std::vector<int32_t> label((size_t)std::max<int64_t>(ld, 1), -1);
+    for (int32_t s = 0; s < S; ++s) {
+      ScenCtl& cs = ctl[(size_t)s];
+      int32_t n = 0;
+      for (int32_t d = cs.f0; d < cs.f1; ++d) {
+        int32_t k = 0;
+        if (poff[(size_t)d + 1] > poff[(size_t)d]) {
+          const int32_t r = find(plink[(size_t)poff[(size_t)d]]);
+          if (label[(size_t)r] < 0) label[(size_t)r] = n < kMaxComp ? n++ : kMaxComp - 1;
+          k = label[(size_t)r];
+        }
+        comp_of_dev[(size_t)d] = ncomp_total + k;
+      }
+      cs.c0 = ncomp_total;
+      cs.nc = std::max<int32_t>(n, 1);
+      ncomp_total += cs.nc;
+    }
+  }
   // successor lists (device ids)
   std::vector<int32_t> soff((size_t)F + 1, 0);
   for (int64_t id = 0; id < F; ++id)
@@ -322,6 +362,8 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.rel, sizeof(double) * Fz},
       {(void**)&P.cnt, sizeof(int32_t) * Fz},
       {(void**)&P.born, sizeof(int32_t) * Fz},
+      {(void**)&P.comp, sizeof(int32_t) * Fz},
+      {(void**)&P.theta, sizeof(uint64_t) * (size_t)std::max<int32_t>(ncomp_total, 1)},
       {(void**)&P.arr, sizeof(int32_t) * Fz},
       {(void**)&P.lst, sizeof(int64_t) * 2 * Lz},
       {(void**)&P.nact, sizeof(int32_t) * Lz},
@@ -363,6 +405,7 @@ netsim_status prepare(netsim_t* h) {
       {soff.data(), P.soff, sizeof(int32_t) * (size_t)(F + 1)},
       {succ.data(), P.succ, sizeof(int32_t) * succ.size()},
       {R0.data(), P.R0, sizeof(int64_t) * R0.size()},
+      {comp_of_dev.data(), P.comp, sizeof(int32_t) * comp_of_dev.size()},
   };
   for (const Up& u : ups) {
     he = hipMemcpy((void*)u.dst, u.src, u.bytes, hipMemcpyHostToDevice);
@@ -712,6 +755,8 @@ netsim_status netsim_run(netsim_t* h, void* hip_stream) {
     s.incidences_swept += c.incidences_swept;
     s.active_swept += c.active_swept;
     s.pending_swept += c.pending_swept;
+    s.reselected += c.reselected;
+    s.wide_solves += c.wide_solves;
     s.sim_time = std::max(s.sim_time, c.t);
     if (c.status != 0) s.complete = 0;
   }

@@ -54,6 +54,7 @@ class netsim_stats(ctypes.Structure):
                 ("rounds", ctypes.c_int64), ("flows_swept", ctypes.c_int64),
                 ("incidences_swept", ctypes.c_int64), ("active_swept", ctypes.c_int64),
                 ("pending_swept", ctypes.c_int64), ("completed_flows", ctypes.c_int64),
+                ("reselected", ctypes.c_int64), ("wide_solves", ctypes.c_int64),
                 ("complete", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("sim_time", ctypes.c_double), ("device_seconds", ctypes.c_double),
                 ("upload_seconds", ctypes.c_double), ("phase_seconds", ctypes.c_double * 8)]
