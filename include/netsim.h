@@ -71,6 +71,8 @@ typedef struct {
   double until;              /* do not process events later than this time (s); +inf = none */
   int32_t max_rounds;        /* per-solve round watchdog; 0 = number of flows + 1 */
   int32_t block_threads;     /* threads per workgroup in block mode; 0 = 1024    */
+  int32_t debug;             /* 1: internal consistency checks on the device     */
+  int32_t reserved;
 } netsim_options;
 
 /*

@@ -24,6 +24,7 @@ struct ScenCtl {
   int32_t status;          // 0 ran to the end, 1 stopped at a limit, < 0 fault
   int32_t fault_info;
   int64_t ticks[8];        // wall-clock ticks per phase (first thread of the group)
+  int64_t dbg[4];          // debug checks (options.debug)
   // list counters (kernel scratch; zero at launch)
   int32_t cnt_act[2];
   int32_t cnt_pend[2];
@@ -32,6 +33,7 @@ struct ScenCtl {
   int32_t changed[2];
   int32_t rem3[3];         // shared-memory solve: unfrozen flows left, rotating
   int32_t cnt_arr;         // flows activated in the current event
+  int32_t cnt_sel;         // flows taken back for re-solving in the current event
   int32_t succ_flag[2];    // a flow finished in this event has dependants
   int32_t solve_rc;        // status of a solve run by one workgroup
 };
@@ -52,6 +54,7 @@ struct Params {
   double until;
   int32_t max_rounds;
   int32_t lds_ok;          // every path fits the shared-memory solve (<= 6 links)
+  int32_t debug;           // run internal consistency checks
   double scale;            // fixed-point units per B/s (a power of two)
   double inv_scale;
   // static flow / link data (device order)

@@ -340,13 +340,14 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
   const int T = g.nthr();
   const int tid = g.tid();
   const int b0 = g.block_base();
-  for (int l = C->l0 + tid; l < C->l1; l += T) {
-    if (!warm) {
+  const bool one = g.nblocks() == 1;
+  if (!warm) {
+    for (int l = C->l0 + tid; l < C->l1; l += T) {
       P.lst[2 * l] = P.R0[l];
       P.lst[2 * l + 1] = P.nact[l];
+      P.blocked0[l] = 0;
+      P.blocked1[l] = 0;
     }
-    P.blocked0[l] = 0;
-    P.blocked1[l] = 0;
   }
   if (tid == 0) {
     g.store(&C->cnt_unf[0], 0);
@@ -435,7 +436,20 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
         else bad = 2;
       }
     }
-    for (int l = C->l0 + tid; l < C->l1; l += T) bl_next[l] = 0;
+    // Blocked flags are clean outside solves.  Several workgroups: clear the
+    // next round's array now (its last readers passed a barrier) and this
+    // round's after the final barrier.  One workgroup: clear exactly the
+    // links this round may have flagged, once every thread has read them.
+    if (!one) {
+      for (int l = C->l0 + tid; l < C->l1; l += T) bl_next[l] = 0;
+    } else {
+      __syncthreads();
+      for (int i = tid; i < n; i += T) {
+        const int f = in[i];
+        if (in_range(f, C->f0, cap))
+          for (int e = P.poff[f]; e < P.poff[f + 1]; ++e) bl[P.plink[e]] = 0;
+      }
+    }
     if (bad) g.store(&C->fault_info, bad);
     clk.lap(5);
     g.sync();
@@ -445,7 +459,11 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
     if (g.aborted()) return ST_BARRIER;
     const int nout = g.load(out_cnt);
     if (g.load(&C->fault_info) != 0) return g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE;
-    if (nout == 0) return 0;
+    if (nout == 0) {
+      if (!one)
+        for (int l = C->l0 + tid; l < C->l1; l += T) bl[l] = 0;
+      return 0;
+    }
     if (nout >= n) return ST_BAD_SHARE;  // a round must freeze something
     if (++r > P.max_rounds) return ST_ROUNDS;
     in = out;
@@ -482,13 +500,14 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
   const int per = (n0 + nb - 1) / nb;
   const int c0 = min(n0, g.block_id() * per);
   const int nl = min(n0, c0 + per) - c0;
-  for (int l = C->l0 + tid; l < C->l1; l += T) {
-    if (!warm) {
+  const bool one = nb == 1;
+  if (!warm) {
+    for (int l = C->l0 + tid; l < C->l1; l += T) {
       P.lst[2 * l] = P.R0[l];
       P.lst[2 * l + 1] = P.nact[l];
+      P.blocked0[l] = 0;
+      P.blocked1[l] = 0;
     }
-    P.blocked0[l] = 0;
-    P.blocked1[l] = 0;
   }
   if (tid == 0)
     for (int k = 0; k < 3; ++k) g.store(&C->rem3[k], 0);
@@ -578,10 +597,22 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
         if (keep) uout[b + (int)__popcll(mask & ((1ull << lane) - 1ull))] = (uint16_t)j;
       }
     }
-    for (int l = C->l0 + tid; l < C->l1; l += T) bl_next[l] = 0;
+    if (!one)
+      for (int l = C->l0 + tid; l < C->l1; l += T) bl_next[l] = 0;
     if (bad) g.store(&C->fault_info, bad);
     __syncthreads();
     const int nu_new = S.cnt;
+    if (one) {
+      // clear exactly what this round may have flagged (every read is done)
+      for (int x = threadIdx.x; x < nu; x += blockDim.x) {
+        const int j = uin[x];
+#pragma unroll
+        for (int k = 0; k < LDS_DEG; ++k) {
+          const int l = S.link[j * LDS_DEG + k];
+          if (l >= 0) bl[l] = 0;
+        }
+      }
+    }
     if (threadIdx.x == 0 && nu_new > 0) g.add(&C->rem3[r % 3], (int32_t)nu_new);
     clk.lap(5);
     g.sync();
@@ -591,7 +622,11 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
     if (g.aborted()) return ST_BARRIER;
     if (g.load(&C->fault_info) != 0) return g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE;
     const int left = g.load(&C->rem3[r % 3]);
-    if (left == 0) return 0;
+    if (left == 0) {
+      if (!one)
+        for (int l = C->l0 + tid; l < C->l1; l += T) bl[l] = 0;
+      return 0;
+    }
     if (left >= total) return ST_BAD_SHARE;  // a round must freeze something
     if (++r > P.max_rounds) return ST_ROUNDS;
     total = left;
@@ -689,6 +724,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
       g.store(&C->changed[ib], 0);
       g.store(&C->succ_flag[ib], 0);
       g.store(&C->cnt_arr, 0);
+      g.store(&C->cnt_sel, 0);
     }
     // next event time: earliest completion or release
     double loc = INF;
@@ -870,7 +906,6 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
       }
       // take back the flows at or above their component's theta (and the new
       // ones) for re-solving
-      if (tid == 0) g.store(&C->cnt_unf[0], 0);
       g.sync();
       for (int base = b0; base < nNew; base += T) {
         const int i = base + (int)threadIdx.x;
@@ -895,7 +930,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
             err = 1;
           }
         }
-        int32_t* const cnts[1] = {&C->cnt_unf[0]};
+        int32_t* const cnts[1] = {&C->cnt_sel};
         const bool pr[1] = {upper};
         int slot[1];
         block_append<1>(g, cnts, pr, slot);
@@ -905,11 +940,22 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
       g.sync();
       clk.lap(7);
       for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
-      const int nSel = g.load(&C->cnt_unf[0]);
+      const int nSel = g.load(&C->cnt_sel);
+      if (P.debug) {
+        // blocked flags must be clean between solves
+        for (int l = C->l0 + tid; l < C->l1; l += T)
+          if (P.blocked0[l] | P.blocked1[l]) {
+            g.store(&C->dbg[0], (int64_t)(e + 1));
+            g.store(&C->dbg[1], (int64_t)l);
+          }
+        g.sync();
+        if (g.load(&C->dbg[0]) != 0 && status == ST_DONE) { status = -8; break; }
+      }
       sel += nSel;
       wide += nSel > LDS_FLOWS ? 1 : 0;
       int rc = 0;
       if (nSel > 0) {
+        if (P.debug && tid == 0) g.store(&C->dbg[2], (int64_t)(nSel <= LDS_FLOWS ? 1 : nSel <= g.nblocks() * LDS_FLOWS ? 2 : 3));
         if (P.lds_ok && nSel <= LDS_FLOWS) {
           if (g.block_id() == 0) {
             BlockG b{g.lds, g.ldsi};

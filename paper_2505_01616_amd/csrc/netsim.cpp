@@ -459,6 +459,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms) {
   P.mode = solve_only ? 1 : 0;
   P.max_events = solve_only ? 0 : h->opt.max_events;
   P.until = std::isnan(h->opt.until) ? std::numeric_limits<double>::infinity() : h->opt.until;
+  P.debug = h->opt.debug;
   P.max_rounds = h->opt.max_rounds > 0 ? h->opt.max_rounds
                                        : (int32_t)std::min<int64_t>(h->F + 1, std::numeric_limits<int32_t>::max());
   const int32_t S = (int32_t)h->scen.size();
@@ -506,6 +507,11 @@ netsim_status collect(netsim_t* h, std::vector<ScenCtl>* ctl_out) {
   for (int32_t s = 0; s < S; ++s) {
     const int32_t st = ctl[(size_t)s].status;
     if (st < 0) {
+      if (st == -8)
+        return fail(h, NETSIM_E_DEVICE, "debug check failed in scenario " + std::to_string(s) +
+                                            ": event " + std::to_string(ctl[(size_t)s].dbg[0] - 1) +
+                                            " link " + std::to_string(ctl[(size_t)s].dbg[1]) +
+                                            " last solve path " + std::to_string(ctl[(size_t)s].dbg[2]));
       std::string why = st == netsim_dev::ST_ROUNDS ? "round watchdog fired"
                         : st == netsim_dev::ST_BARRIER ? "grid barrier timed out"
                         : st == netsim_dev::ST_OVERFLOW ? "work list fault"

@@ -33,7 +33,8 @@ STATUS_NAMES = {OK: "NETSIM_OK", E_INVALID: "NETSIM_E_INVALID", E_NOMEM: "NETSIM
 class netsim_options(ctypes.Structure):
     _fields_ = [("device", ctypes.c_int32), ("exec", ctypes.c_int32),
                 ("max_events", ctypes.c_int64), ("until", ctypes.c_double),
-                ("max_rounds", ctypes.c_int32), ("block_threads", ctypes.c_int32)]
+                ("max_rounds", ctypes.c_int32), ("block_threads", ctypes.c_int32),
+                ("debug", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class netsim_topology(ctypes.Structure):
@@ -141,10 +142,10 @@ def netsim_default_options() -> netsim_options:
 
 
 def make_options(device=0, exec=EXEC_AUTO, max_events=0, until=math.inf, max_rounds=0,
-                 block_threads=0) -> netsim_options:
+                 block_threads=0, debug=0) -> netsim_options:
     o = netsim_default_options()
     o.device, o.exec, o.max_events, o.until = device, exec, max_events, until
-    o.max_rounds, o.block_threads = max_rounds, block_threads
+    o.max_rounds, o.block_threads, o.debug = max_rounds, block_threads, debug
     return o
 
 
