@@ -1,14 +1,17 @@
 """Benchmark: max-min rate solves/s and events/s of the flow-level simulator
 on the 4096-GPU expert-parallel all-to-all workload (C4), on one MI355X.
 
-A step is one event of the simulator's event loop: find the next
-completion or release, settle completions and releases, and re-solve the
-max-min rates of all active flows.  The timed region is one device-resident
-run of exactly K events from t = 0 (one kernel launch); W warm-up events
-run first in a separate launch.  Inputs (flows, routes, capacities) are
-resident in HBM before timing starts.
+A step is one complete simulation of the workload: every flow of the four
+back-to-back all-to-all phases from release to completion (about 0.9 M
+events, each ending in a max-min rate solve).  The simulator splits the
+workload into its independent parts (the eight groups of expert-parallel
+ranks that share fabric links) and runs each with its own clock, one
+workgroup per part; events and solves are counted per part.  Each step is
+one kernel launch, timed with HIP events on the launch stream; W warm-up
+steps run first.  Inputs (flows, routes, capacities) are resident in HBM
+before timing starts; the per-run state reset is outside the kernel time.
 
-Prints one JSON line.  Also reports the roofline of the event-loop kernel
+Prints one JSON line, with the roofline of the event-loop kernel
 (algorithmic bytes per launch / launch duration, against 8 TB/s) and the
 CPU oracle's rate on a bounded sample of the same workload.
 """
@@ -27,8 +30,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 
-# Algorithmic bytes ("Roofline"): what each unit of work must
-# move at least once per visit.
+# Algorithmic bytes: what each unit of work must move at least once per
+# visit (the byte model of the event-loop kernel).
 BYTES_PER_FLOW_ROUND = 28      # list entry 4 + path offsets 8 + min-share write 8 + read 8
 BYTES_PER_INCIDENCE_ROUND = 21  # link id 4+4 + residual capacity 8 + count 4 + flag 1
 BYTES_PER_ACTIVE_EVENT = 48    # rem, rate read twice (32) + rem write 8 + list in/out 8
@@ -40,10 +43,11 @@ def algorithmic_bytes(st: dict) -> float:
             + BYTES_PER_ACTIVE_EVENT * st["active_swept"] + BYTES_PER_PENDING_EVENT * st["pending_swept"])
 
 
-# The first 64 events of C4 are the arrivals of the 64 groups (small active
-# sets); from then on every solve covers all ~258k flows of a phase.  Both the
-# GPU and the oracle are also timed on events 65..128 alone (by differencing
-# two runs) so that their rates are compared on the same steady-state window.
+# The oracle is far too slow for the whole workload (a solve over ~258k
+# flows takes it ~0.1 s), so it is timed on a bounded sample: events 65..128
+# of the workload on one clock (the first 64 events are the arrivals of the
+# 64 groups; from then on every group is active), by differencing runs to 64
+# and 128 events.
 STEADY = (64, 128)
 
 
@@ -66,28 +70,28 @@ def cpu_baseline():
                       f"of runs to {STEADY[0]} and {STEADY[1]} events; fp64 oracle, one thread"}
 
 
-def traffic_from_profile(steps: int, exec_: str):
+def traffic_from_profile(kernel: str, steps: int):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if
-    it was taken on the current kernel source with the same launch."""
+    it was taken on the current kernel source for the same kernel."""
     import hashlib
     try:
-        with open(os.path.join(ROOT, "profiles", "netsim_grid_kernel_c4_traffic.json")) as fh:
+        with open(os.path.join(ROOT, "profiles", f"{kernel}_c4_traffic.json")) as fh:
             prof = json.load(fh)
         with open(os.path.join(ROOT, "paper_2505_01616_amd", "csrc", "kernels.hip"), "rb") as fh:
             sha = hashlib.sha256(fh.read()).hexdigest()[:16]
     except OSError:
         return None
-    if prof.get("kernels_hip_sha256_16") != sha or prof.get("steps") != steps or exec_ != "grid":
+    if prof.get("kernels_hip_sha256_16") != sha or prof.get("kernel") != kernel:
         return None
-    return prof["traffic_bytes"]
+    return prof["traffic_bytes_per_launch"]
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--exec", choices=["grid", "block", "auto"], default="grid")
+    ap.add_argument("--steps", type=int, default=1, help="timed complete simulations")
+    ap.add_argument("--warmup", type=int, default=1, help="untimed complete simulations first")
+    ap.add_argument("--exec", choices=["grid", "block", "auto"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM counters)")
@@ -119,36 +123,41 @@ def main():
     ex = {"grid": ns.EXEC_GRID, "block": ns.EXEC_BLOCK, "auto": ns.EXEC_AUTO}[args.exec]
     ld = prog.load_program(program, ns.make_options(exec=ex))
     h = ld.handle
+    keys = ("events", "solves", "rounds", "flows_swept", "incidences_swept", "active_swept",
+            "pending_swept", "reselected", "wide_solves")
+    tot = {k: 0 for k in keys}
+    tot["device_seconds"] = 0.0
+    phases = [0.0] * 8
     try:
         nflows, nnz, ndeps = ns.netsim_counts(h)
-        # warm-up (also uploads the static data once)
-        ns.netsim_set_limits(h, max_events=max(args.warmup, 1))
-        ns.netsim_run(h, stream)
-        # timed: exactly K events, one launch
-        ns.netsim_set_limits(h, max_events=args.steps)
+        for i in range(args.warmup):
+            ns.netsim_run(h, stream)
+            print(f"warm-up step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        ns.netsim_run(h, stream)
+        for i in range(args.steps):
+            ns.netsim_run(h, stream)
+            st = ns.netsim_get_stats(h)
+            assert st["complete"] == 1, st
+            for k in keys:
+                tot[k] += st[k]
+            tot["device_seconds"] += st["device_seconds"]
+            phases = [a + b for a, b in zip(phases, st["phase_seconds"])]
+            print(f"step {i + 1}/{args.steps}: {st['device_seconds']:.3f} s device, "
+                  f"{st['solves']} solves", file=sys.stderr, flush=True)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        st = ns.netsim_get_stats(h)
-        # steady-state window (same events as the CPU baseline)
-        steady_dev = []
-        for e in STEADY:
-            ns.netsim_set_limits(h, max_events=e)
-            ns.netsim_run(h, stream)
-            s2 = ns.netsim_get_stats(h)
-            steady_dev.append((s2["device_seconds"], s2["solves"]))
+        parts = st["parts"]
+        sim_time = st["sim_time"]
     finally:
         ld.close()
-    gpu_steady = (steady_dev[1][1] - steady_dev[0][1]) / (steady_dev[1][0] - steady_dev[0][0])
-    dev = st["device_seconds"]
-    assert st["events"] == args.steps, st
-    solves_per_s = st["solves"] / dev
-    events_per_s = st["events"] / dev
-    abytes = algorithmic_bytes(st)
+    dev = tot["device_seconds"]
+    solves_per_s = tot["solves"] / dev
+    events_per_s = tot["events"] / dev
+    abytes = algorithmic_bytes(tot)
     achieved = abytes / dev / 1e9
-    traffic = traffic_from_profile(args.steps, args.exec)
+    kernel = "netsim_grid_kernel" if args.exec == "grid" else "netsim_block_kernel"
+    traffic = traffic_from_profile(kernel, args.steps)
     line = {
         "metric": "max-min rate solves/sec + events/sec (4096-GPU all-to-all); achieved HBM GB/s",
         "value": solves_per_s,
@@ -163,20 +172,24 @@ def main():
         "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": "c4: 4096 GPUs, 3-tier fat-tree 2:1 at the core, 64 EP groups x 64 "
-                               "ranks, 4 all-to-all phases, Zipf(1.2) bytes mean 4 MiB, seed 4",
-                   "flows": nflows, "incidences": nnz, "exec": args.exec},
+                               "ranks, 4 all-to-all phases, Zipf(1.2) bytes mean 4 MiB, seed 4; "
+                               "one step = the complete simulation",
+                   "flows": nflows, "incidences": nnz, "exec": args.exec, "parts": parts},
         "events_per_s": events_per_s,
-        "steady_state_solves_per_s": gpu_steady,
-        "solves": st["solves"],
-        "rounds_per_solve": st["rounds"] / max(st["solves"], 1),
+        "events_per_step": tot["events"] / args.steps,
+        "solves_per_step": tot["solves"] / args.steps,
+        "rounds_per_solve": tot["rounds"] / max(tot["solves"], 1),
+        "reselected_per_solve": tot["reselected"] / max(tot["solves"], 1),
+        "wide_solves": tot["wide_solves"],
         "wall_s_incl_state_reset": wall,
-        "sim_time_s": st["sim_time"],
-        "phase_seconds": dict(zip(["next_event", "settle", "solve_setup", "sweep_b", "wait_b",
-                                   "sweep_c", "wait_c"], [round(x, 6) for x in st["phase_seconds"][:7]])),
+        "sim_time_s": sim_time,
+        "phase_seconds_summed_over_parts": dict(zip(
+            ["next_event", "settle", "solve_setup", "sweep_b", "wait_b", "sweep_c", "wait_c",
+             "reselect"], [round(x, 4) for x in phases])),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
-                     "kernel": "netsim_grid_kernel" if args.exec == "grid" else "netsim_block_kernel",
-                     "algorithmic_bytes": abytes, "launch_seconds": dev},
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic, "kernel": kernel,
+                     "algorithmic_bytes_per_launch": abytes / args.steps,
+                     "launch_seconds": dev / args.steps},
     }
     if not args.no_cpu_baseline and int(os.environ.get("RANK", "0")) == 0:
         line["cpu_baseline"] = cpu_baseline()

@@ -59,20 +59,30 @@ enum { NETSIM_RING_ALLREDUCE = 0, NETSIM_RING_REDUCE_SCATTER = 1, NETSIM_RING_AL
 enum { NETSIM_MODE_CHAINED = 0, NETSIM_MODE_FLAT = 1, NETSIM_MODE_AGGREGATED = 2 };
 /* Execution layout (netsim_options.exec). */
 enum {
-  NETSIM_EXEC_AUTO = 0,  /* block per scenario when batched or small, else grid */
-  NETSIM_EXEC_GRID = 1,  /* whole GPU on one scenario at a time (grid barriers)  */
-  NETSIM_EXEC_BLOCK = 2  /* one workgroup per scenario (workgroup barriers)      */
+  NETSIM_EXEC_AUTO = 0,  /* block per part when there are several or it is small, else grid */
+  NETSIM_EXEC_GRID = 1,  /* whole GPU on one part at a time (grid barriers)      */
+  NETSIM_EXEC_BLOCK = 2  /* one workgroup per part (workgroup barriers)          */
 };
 
+/*
+ * Parts.  The flows of a scenario fall into groups connected through shared
+ * links or dependencies; flows of different groups never influence each
+ * other in the fluid model.  By default each group is simulated as its own
+ * "part" with its own clock (several parts run concurrently on the GPU), and
+ * the finish times are those of one clock per scenario up to rounding.
+ * Events are counted per part: an instant at which two parts both have an
+ * event counts twice.  single_clock = 1 keeps every scenario one part (one
+ * clock), which counts events exactly as one event loop over the scenario.
+ */
 typedef struct {
   int32_t device;            /* HIP device ordinal                               */
   int32_t exec;              /* NETSIM_EXEC_*                                    */
-  int64_t max_events;        /* stop each scenario after this many events; 0 = no limit */
+  int64_t max_events;        /* stop each part after this many events; 0 = no limit */
   double until;              /* do not process events later than this time (s); +inf = none */
   int32_t max_rounds;        /* per-solve round watchdog; 0 = number of flows + 1 */
   int32_t block_threads;     /* threads per workgroup in block mode; 0 = 1024    */
   int32_t debug;             /* 1: internal consistency checks on the device     */
-  int32_t reserved;
+  int32_t single_clock;      /* 1: one part (one clock) per scenario             */
 } netsim_options;
 
 /*
@@ -133,7 +143,7 @@ typedef struct {
   int64_t reselected;        /* sum over solves of flows whose rate was re-solved */
   int64_t wide_solves;       /* solves too large for one workgroup's shared memory */
   int32_t complete;          /* 1 if every scenario ran to its end               */
-  int32_t reserved;
+  int32_t parts;             /* independent parts simulated (see netsim_options) */
   double sim_time;           /* largest simulated time reached over scenarios    */
   double device_seconds;     /* device time of the last netsim_run (HIP events)  */
   double upload_seconds;     /* host->device preparation of the last run          */

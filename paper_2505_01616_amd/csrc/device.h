@@ -7,15 +7,19 @@
 
 namespace netsim_dev {
 
-// Per-scenario control block in device memory.  The host fills the ranges
-// and the initial counters; the kernels keep their list counters here and
-// write the results back at the end of the run.
+// Control block of one part in device memory.  A part is a set of flows of
+// one scenario that shares no link and no dependency with the rest of the
+// scenario, simulated with its own clock.  The host fills the ranges and the
+// initial counters; the kernels keep their list counters here and write the
+// results back at the end of the run.
 struct ScenCtl {
   int32_t f0, f1;          // device flow range [f0, f1)
   int32_t l0, l1;          // device link range [l0, l1)
   int32_t n_pend0;         // flows initially pending (listed in pend0 + f0)
-  int32_t c0, nc;          // this scenario's components [c0, c0 + nc)
+  int32_t c0, nc;          // this part's link components [c0, c0 + nc)
   int32_t n_solve;         // solve-once: active flows listed in act0 + f0
+  int32_t scen;            // the scenario the part belongs to
+  int32_t lds_paths;       // every path has <= 6 links and the part < 65535 links
   // results
   double t;                // simulated time reached
   int64_t events, solves, rounds, flows_swept, incidences_swept;
@@ -53,7 +57,6 @@ struct Params {
   int64_t max_events;      // 0 = no limit
   double until;
   int32_t max_rounds;
-  int32_t lds_ok;          // every path fits the shared-memory solve (<= 6 links)
   int32_t debug;           // run internal consistency checks
   double scale;            // fixed-point units per B/s (a power of two)
   double inv_scale;

@@ -325,28 +325,111 @@ __device__ __forceinline__ bool in_range(int f, int f0, int cap) {
   return (unsigned)(f - f0) < (unsigned)cap;
 }
 
-__device__ __forceinline__ double share(const Params& P, int l) {
-  const longlong2 v = *reinterpret_cast<const longlong2*>(P.lst + 2 * l);
-  return ((double)v.x / (double)v.y) * P.inv_scale;
-}
+// ------------------------------------------------------------ link state
+// Per link: residual capacity R (fixed point), unfrozen flows n, active
+// flows nact and two alternating "blocked" flags.  Two homes for it, with
+// one interface taking device link ids:
+//   LinksGlobal - global memory; any group (the whole grid, or a workgroup
+//                 on a part too large for shared memory);
+//   LinksShared - the shared memory of the one workgroup running a part
+//                 whose links fit there; atomics stay inside the CU.
+// Blocked flags of one round, indexed by device link id.
+struct Flags {
+  uint8_t* p;
+  int off;
+  __device__ uint8_t& operator[](int l) const { return p[l - off]; }
+};
+
+struct LinksGlobal {
+  int64_t* lst;      // [2L] (R, n) pairs: one 16-byte load per link
+  int32_t* nact;
+  uint8_t* bl0;
+  uint8_t* bl1;
+  double inv;
+  __device__ double share(int l) const {
+    const longlong2 v = *reinterpret_cast<const longlong2*>(lst + 2 * l);
+    return ((double)v.x / (double)v.y) * inv;
+  }
+  __device__ void set(int l, int64_t R, int64_t n) {
+    lst[2 * l] = R;
+    lst[2 * l + 1] = n;
+  }
+  __device__ int nactv(int l) const { return nact[l]; }
+  __device__ void clear_flags(int l) {
+    bl0[l] = 0;
+    bl1[l] = 0;
+  }
+  // link at rest: full capacity, no flow (active counts are cleared by the host)
+  __device__ void reset(int l, int64_t R) {
+    set(l, R, 0);
+    clear_flags(l);
+  }
+  __device__ Flags flags(int r) const { return Flags{(r & 1) ? bl1 : bl0, 0}; }
+  template <class G> __device__ void addR(G& g, int l, int64_t v) { g.add(&lst[2 * l], v); }
+  template <class G> __device__ void addN(G& g, int l, int64_t v) { g.add(&lst[2 * l + 1], v); }
+  template <class G> __device__ void addNact(G& g, int l, int32_t v) { g.add(&nact[l], v); }
+};
+
+constexpr int LDS_LINKS = 2816;
+
+struct LinkLds {
+  int64_t R[LDS_LINKS];
+  int32_t n[LDS_LINKS];
+  int32_t nact[LDS_LINKS];
+  uint8_t bl[2][LDS_LINKS];
+};
+
+struct LinksShared {
+  LinkLds* s;
+  int l0;
+  double inv;
+  __device__ double share(int l) const {
+    const int i = l - l0;
+    return ((double)s->R[i] / (double)s->n[i]) * inv;
+  }
+  __device__ void set(int l, int64_t R, int64_t n) {
+    s->R[l - l0] = R;
+    s->n[l - l0] = (int32_t)n;
+  }
+  __device__ int nactv(int l) const { return s->nact[l - l0]; }
+  __device__ void clear_flags(int l) {
+    s->bl[0][l - l0] = 0;
+    s->bl[1][l - l0] = 0;
+  }
+  __device__ void reset(int l, int64_t R) {
+    set(l, R, 0);
+    s->nact[l - l0] = 0;
+    clear_flags(l);
+  }
+  __device__ Flags flags(int r) const { return Flags{s->bl[r & 1], l0}; }
+  template <class G> __device__ void addR(G&, int l, int64_t v) {
+    __hip_atomic_fetch_add(&s->R[l - l0], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  template <class G> __device__ void addN(G&, int l, int64_t v) {
+    __hip_atomic_fetch_add(&s->n[l - l0], (int32_t)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  template <class G> __device__ void addNact(G&, int l, int32_t v) {
+    __hip_atomic_fetch_add(&s->nact[l - l0], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+};
 
 // ------------------------------------------------------------- rate solve
-// Max-min rates of the n0 flows listed in list0 (all active).  Link state is
-// initialised from nact.  Returns 0 or a negative status.
-template <class G>
-__device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const int32_t* list0, int n0,
-                     int32_t* unf_a, int32_t* unf_b, int cap, int64_t& rounds, int64_t& fsw,
-                     int64_t& isw, Clock& clk, bool warm) {
+// Max-min rates of the n0 flows listed in list0 (all active), with work
+// lists in global memory.  Cold (warm = false): link state starts from the
+// capacities and the active counts; warm: from the residual state the event
+// loop prepared.  Returns 0 or a negative status.
+template <class G, class LK>
+__device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, const int32_t* list0,
+                                     int n0, int32_t* unf_a, int32_t* unf_b, int cap, int64_t& rounds,
+                                     int64_t& fsw, int64_t& isw, Clock& clk, bool warm) {
   const int T = g.nthr();
   const int tid = g.tid();
   const int b0 = g.block_base();
   const bool one = g.nblocks() == 1;
   if (!warm) {
     for (int l = C->l0 + tid; l < C->l1; l += T) {
-      P.lst[2 * l] = P.R0[l];
-      P.lst[2 * l + 1] = P.nact[l];
-      P.blocked0[l] = 0;
-      P.blocked1[l] = 0;
+      lk.set(l, P.R0[l], lk.nactv(l));
+      lk.clear_flags(l);
     }
   }
   if (tid == 0) {
@@ -360,8 +443,8 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
   int r = 0;
   int bad = 0;
   for (;;) {
-    uint8_t* bl = (r & 1) ? P.blocked1 : P.blocked0;
-    uint8_t* bl_next = (r & 1) ? P.blocked0 : P.blocked1;
+    const Flags bl = lk.flags(r);
+    const Flags bl_next = lk.flags(r + 1);
     int32_t* out = (r & 1) ? unf_b : unf_a;
     int32_t* out_cnt = &C->cnt_unf[r & 1];
     if (tid == 0 && r > 0) g.store(out_cnt, 0);
@@ -380,7 +463,7 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
         for (int k = 0; k < FAST_DEG; ++k) {
           if (k < deg) {
             lv[k] = P.plink[e0 + k];
-            sv[k] = share(P, lv[k]);
+            sv[k] = lk.share(lv[k]);
             m = sv[k] < m ? sv[k] : m;
           }
         }
@@ -390,12 +473,12 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
           if (k < deg && sv[k] > thr) bl[lv[k]] = 1;
       } else {
         for (int e = e0; e < e1; ++e) {
-          const double s = share(P, P.plink[e]);
-          m = s < m ? s : m;
+          const double sh = lk.share(P.plink[e]);
+          m = sh < m ? sh : m;
         }
         const double thr = m * THR;
         for (int e = e0; e < e1; ++e)
-          if (share(P, P.plink[e]) > thr) bl[P.plink[e]] = 1;
+          if (lk.share(P.plink[e]) > thr) bl[P.plink[e]] = 1;
       }
       if (!(m > 0.0) || !(m < INF)) bad = 1;
       P.mf[f] = m;
@@ -420,8 +503,8 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
           const int64_t q = (int64_t)__builtin_rint(m * P.scale);
           for (int e = e0; e < e1; ++e) {
             const int l = P.plink[e];
-            g.add(&P.lst[2 * l], -q);
-            g.add(&P.lst[2 * l + 1], (int64_t)-1);
+            lk.addR(g, l, -q);
+            lk.addN(g, l, (int64_t)-1);
           }
         } else {
           keep = true;
@@ -473,27 +556,28 @@ __device__ __forceinline__ int solve(G& g, const Params& P, ScenCtl* C, const in
 
 // ---------------------------------------------- shared-memory-resident solve
 // Each workgroup takes a contiguous slice of the active list (at most
-// LDS_FLOWS flows), copies the flow ids and their padded paths into shared
-// memory once, and keeps its unfrozen flows as a shared-memory list.  Only
-// link state (residual capacity and count, blocked flags) and the rates go
-// through global memory, so a round costs one gather of link state, one of
-// flags and two barriers.
-constexpr int LDS_FLOWS = 3584;
+// LDS_FLOWS flows), copies the flow ids and their padded paths (link ids
+// local to the part, 16 bits) into shared memory once, and keeps its
+// unfrozen flows as a shared-memory list.  Only link state and the rates are
+// touched outside, so a round costs one gather of link state, one of flags
+// and two barriers.
+constexpr int LDS_FLOWS = 3840;
 constexpr int LDS_DEG = 6;
+constexpr uint16_t NO_LINK = 0xFFFF;
 
 struct SolveLds {
   int32_t fid[LDS_FLOWS];
-  int32_t link[LDS_FLOWS * LDS_DEG];
+  uint16_t link[LDS_FLOWS * LDS_DEG];
   double mf[LDS_FLOWS];
   uint16_t u[2][LDS_FLOWS];
   int cnt;
   uint64_t clk[9];
 };
 
-template <class G>
-__device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, const int32_t* list0, int n0,
-                         int64_t& rounds, int64_t& fsw, int64_t& isw, Clock& clk, SolveLds& S,
-                         bool warm) {
+template <class G, class LK>
+__device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl* C, const int32_t* list0,
+                                         int n0, int64_t& rounds, int64_t& fsw, int64_t& isw, Clock& clk,
+                                         SolveLds& S, bool warm) {
   const int T = g.nthr();
   const int tid = g.tid();
   const int nb = g.nblocks();
@@ -501,12 +585,11 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
   const int c0 = min(n0, g.block_id() * per);
   const int nl = min(n0, c0 + per) - c0;
   const bool one = nb == 1;
+  const int l0 = C->l0;
   if (!warm) {
     for (int l = C->l0 + tid; l < C->l1; l += T) {
-      P.lst[2 * l] = P.R0[l];
-      P.lst[2 * l + 1] = P.nact[l];
-      P.blocked0[l] = 0;
-      P.blocked1[l] = 0;
+      lk.set(l, P.R0[l], lk.nactv(l));
+      lk.clear_flags(l);
     }
   }
   if (tid == 0)
@@ -518,7 +601,8 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
     const int e0 = P.poff[f], e1 = P.poff[f + 1];
     S.fid[j] = f;
 #pragma unroll
-    for (int k = 0; k < LDS_DEG; ++k) S.link[j * LDS_DEG + k] = e0 + k < e1 ? P.plink[e0 + k] : -1;
+    for (int k = 0; k < LDS_DEG; ++k)
+      S.link[j * LDS_DEG + k] = e0 + k < e1 ? (uint16_t)(P.plink[e0 + k] - l0) : NO_LINK;
     S.u[0][j] = (uint16_t)j;
   }
   int nu = nl;
@@ -527,8 +611,8 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
   int total = n0;
   int r = 0;
   for (;;) {
-    uint8_t* bl = (r & 1) ? P.blocked1 : P.blocked0;
-    uint8_t* bl_next = (r & 1) ? P.blocked0 : P.blocked1;
+    const Flags bl = lk.flags(r);
+    const Flags bl_next = lk.flags(r + 1);
     const uint16_t* uin = S.u[r & 1];
     uint16_t* uout = S.u[(r & 1) ^ 1];
     if (threadIdx.x == 0) S.cnt = 0;
@@ -541,9 +625,10 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
       double m = INF;
 #pragma unroll
       for (int k = 0; k < LDS_DEG; ++k) {
-        lv[k] = S.link[j * LDS_DEG + k];
+        const uint16_t u = S.link[j * LDS_DEG + k];
+        lv[k] = u == NO_LINK ? -1 : l0 + (int)u;
         if (lv[k] >= 0) {
-          sv[k] = share(P, lv[k]);
+          sv[k] = lk.share(lv[k]);
           m = sv[k] < m ? sv[k] : m;
           isw += 1;
         }
@@ -568,8 +653,8 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
         bool frozen = false;
 #pragma unroll
         for (int k = 0; k < LDS_DEG; ++k) {
-          const int l = S.link[j * LDS_DEG + k];
-          if (l >= 0) frozen |= (bl[l] == 0);
+          const uint16_t u = S.link[j * LDS_DEG + k];
+          if (u != NO_LINK) frozen |= (bl[l0 + (int)u] == 0);
         }
         if (frozen) {
           const double m = S.mf[j];
@@ -577,10 +662,10 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
           const int64_t qv = (int64_t)__builtin_rint(m * P.scale);
 #pragma unroll
           for (int k = 0; k < LDS_DEG; ++k) {
-            const int l = S.link[j * LDS_DEG + k];
-            if (l >= 0) {
-              g.add(&P.lst[2 * l], -qv);
-              g.add(&P.lst[2 * l + 1], (int64_t)-1);
+            const uint16_t u = S.link[j * LDS_DEG + k];
+            if (u != NO_LINK) {
+              lk.addR(g, l0 + (int)u, -qv);
+              lk.addN(g, l0 + (int)u, (int64_t)-1);
             }
           }
         } else {
@@ -608,8 +693,8 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
         const int j = uin[x];
 #pragma unroll
         for (int k = 0; k < LDS_DEG; ++k) {
-          const int l = S.link[j * LDS_DEG + k];
-          if (l >= 0) bl[l] = 0;
+          const uint16_t u = S.link[j * LDS_DEG + k];
+          if (u != NO_LINK) bl[l0 + (int)u] = 0;
         }
       }
     }
@@ -635,8 +720,8 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, ScenCtl* C, cons
 }
 
 // Releases flow h whose last predecessor finished at t (called once per h).
-template <class G>
-__device__ __forceinline__ void release_one(G& g, const Params& P, ScenCtl* C, int h, double t,
+template <class G, class LK>
+__device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, ScenCtl* C, int h, double t,
                                             int ob, int ib, int ev, int32_t* actOut,
                                             int32_t* pendOut, int32_t* arrOut, int32_t* cout,
                                             int32_t* coutCnt, int cap, int& err) {
@@ -649,7 +734,7 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, ScenCtl* C, i
     } else {
       P.rem[h] = P.nbytes[h];
       P.born[h] = ev;
-      for (int j = P.poff[h]; j < P.poff[h + 1]; ++j) g.add(&P.nact[P.plink[j]], 1);
+      for (int j = P.poff[h]; j < P.poff[h + 1]; ++j) lk.addNact(g, P.plink[j], 1);
       const int s = g.add(&C->cnt_act[ob], 1);
       if (s < cap) actOut[s] = h; else err = 1;
       const int a = g.add(&C->cnt_arr, 1);
@@ -679,8 +764,8 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, ScenCtl* C, i
 // workgroup 0 alone, with workgroup barriers.
 constexpr double KEEP = 1.0 - 1e-9;  // safety margin below theta
 
-template <class G>
-__device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, SolveLds& S) {
+template <class G, class LK>
+__device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const int sc, SolveLds& S) {
   ScenCtl* C = &P.ctl[sc];
   const int f0 = C->f0;
   const int cap = C->f1 - C->f0;
@@ -696,12 +781,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
   const int w0 = tid - lane_id();
   Clock clk(tid == 0, S.clk);
   // links at rest: nothing active; no component has changed yet
-  for (int l = C->l0 + tid; l < C->l1; l += T) {
-    P.lst[2 * l] = P.R0[l];
-    P.lst[2 * l + 1] = 0;
-    P.blocked0[l] = 0;
-    P.blocked1[l] = 0;
-  }
+  for (int l = C->l0 + tid; l < C->l1; l += T) lk.reset(l, P.R0[l]);
   const uint64_t INF_BITS = (uint64_t)__double_as_longlong(INF);
   for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
   double t = 0.0;
@@ -777,8 +857,8 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
           const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
           for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
             const int l = P.plink[k];
-            g.add(&P.nact[l], -1);
-            g.add(&P.lst[2 * l], qv);  // its share returns to the link
+            lk.addNact(g, l, -1);
+            lk.addR(g, l, qv);  // its share returns to the link
           }
           if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
         } else {
@@ -813,7 +893,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
             start = true;
             P.rem[f] = P.nbytes[f];
             P.born[f] = e;
-            for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) g.add(&P.nact[P.plink[k]], 1);
+            for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) lk.addNact(g, P.plink[k], 1);
           }
         } else {
           keep = true;
@@ -861,7 +941,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
           for (int k = k0; k < k1; ++k) {
             const int h = P.succ[k];
             if (g.add(&P.cnt[h], -1) == 1)
-              release_one(g, P, C, h, t, ob, ib, e, actOut, pendOut, arrs, cout, coutCnt, cap,
+              release_one(g, P, lk, C, h, t, ob, ib, e, actOut, pendOut, arrs, cout, coutCnt, cap,
                           err);
           }
         }
@@ -873,7 +953,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
           for (int k = a + lane_id(); k < z; k += 64) {
             const int h = P.succ[k];
             if (g.add(&P.cnt[h], -1) == 1)
-              release_one(g, P, C, h, t, ob, ib, e, actOut, pendOut, arrs, cout, coutCnt, cap,
+              release_one(g, P, lk, C, h, t, ob, ib, e, actOut, pendOut, arrs, cout, coutCnt, cap,
                           err);
           }
         }
@@ -899,7 +979,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
         double lo = INF;
         for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
           const int l = P.plink[k];
-          const double s0 = ((double)P.R0[l] / (double)P.nact[l]) * P.inv_scale;
+          const double s0 = ((double)P.R0[l] / (double)lk.nactv(l)) * P.inv_scale;
           lo = s0 < lo ? s0 : lo;
         }
         g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(lo));
@@ -922,8 +1002,8 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
               const int64_t qv = fresh ? 0 : (int64_t)__builtin_rint(r * P.scale);
               for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
                 const int l = P.plink[k];
-                if (!fresh) g.add(&P.lst[2 * l], qv);
-                g.add(&P.lst[2 * l + 1], (int64_t)1);
+                if (!fresh) lk.addR(g, l, qv);
+                lk.addN(g, l, (int64_t)1);
               }
             }
           } else {
@@ -944,7 +1024,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
       if (P.debug) {
         // blocked flags must be clean between solves
         for (int l = C->l0 + tid; l < C->l1; l += T)
-          if (P.blocked0[l] | P.blocked1[l]) {
+          if (lk.flags(0)[l] | lk.flags(1)[l]) {
             g.store(&C->dbg[0], (int64_t)(e + 1));
             g.store(&C->dbg[1], (int64_t)l);
           }
@@ -956,18 +1036,22 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
       int rc = 0;
       if (nSel > 0) {
         if (P.debug && tid == 0) g.store(&C->dbg[2], (int64_t)(nSel <= LDS_FLOWS ? 1 : nSel <= g.nblocks() * LDS_FLOWS ? 2 : 3));
-        if (P.lds_ok && nSel <= LDS_FLOWS) {
-          if (g.block_id() == 0) {
-            BlockG b{g.lds, g.ldsi};
-            const int r1 = solve_lds(b, P, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
-            if (threadIdx.x == 0) g.store(&C->solve_rc, r1);
+        if (C->lds_paths && nSel <= LDS_FLOWS) {
+          if (g.nblocks() == 1) {
+            rc = solve_lds(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
+          } else {
+            if (g.block_id() == 0) {
+              BlockG b{g.lds, g.ldsi};
+              const int r1 = solve_lds(b, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
+              if (threadIdx.x == 0) g.store(&C->solve_rc, r1);
+            }
+            g.sync();
+            rc = g.load(&C->solve_rc);
           }
-          g.sync();
-          rc = g.load(&C->solve_rc);
-        } else if (P.lds_ok && nSel <= g.nblocks() * LDS_FLOWS) {
-          rc = solve_lds(g, P, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
+        } else if (C->lds_paths && nSel <= g.nblocks() * LDS_FLOWS) {
+          rc = solve_lds(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
         } else {
-          rc = solve(g, P, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
+          rc = solve(g, P, lk, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
         }
       }
       solves += 1;  // the active set changed: one rate solve (possibly empty)
@@ -995,15 +1079,16 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, const int sc, 
 
 template <class G>
 __device__ __forceinline__ void solve_only(G& g, const Params& P, const int sc, SolveLds& S) {
+  LinksGlobal lk{P.lst, P.nact, P.blocked0, P.blocked1, P.inv_scale};
   ScenCtl* C = &P.ctl[sc];
   const int f0 = C->f0;
   int64_t rounds = 0, fsw = 0, isw = 0;
   Clock clk(g.tid() == 0, S.clk);
   int rc = 0;
   if (C->n_solve > 0)
-    rc = (P.lds_ok && C->n_solve <= g.nblocks() * LDS_FLOWS)
-             ? solve_lds(g, P, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, S, false)
-             : solve(g, P, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0,
+    rc = (C->lds_paths && C->n_solve <= g.nblocks() * LDS_FLOWS)
+             ? solve_lds(g, P, lk, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, S, false)
+             : solve(g, P, lk, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0,
                      rounds, fsw, isw, clk, false);
   g.add(&C->incidences_swept, isw);
   if (g.tid() == 0) {
@@ -1017,14 +1102,25 @@ __device__ __forceinline__ void solve_only(G& g, const Params& P, const int sc, 
 
 }  // namespace
 
+// One workgroup per part.  A part whose links fit keeps its link state in
+// shared memory for the whole run.
 __global__ __launch_bounds__(1024) void netsim_block_kernel(Params P) {
   __shared__ double lds[32];
   __shared__ int ldsi[128];
   __shared__ SolveLds S;
+  __shared__ LinkLds LL;
   BlockG g{lds, ldsi};
   for (int sc = blockIdx.x; sc < P.num_scen; sc += gridDim.x) {
-    if (P.mode == 0) event_loop(g, P, sc, S);
-    else solve_only(g, P, sc, S);
+    const ScenCtl* C = &P.ctl[sc];
+    if (P.mode != 0) {
+      solve_only(g, P, sc, S);
+    } else if (C->l1 - C->l0 <= LDS_LINKS) {
+      LinksShared lk{&LL, C->l0, P.inv_scale};
+      event_loop(g, P, lk, sc, S);
+    } else {
+      LinksGlobal lk{P.lst, P.nact, P.blocked0, P.blocked1, P.inv_scale};
+      event_loop(g, P, lk, sc, S);
+    }
     __syncthreads();
   }
 }
@@ -1036,8 +1132,9 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   __shared__ SolveLds S;
   GridG g{lds, ldsi, &flag, P.bar, P.slots, 0u, 0u, false, 0u, 0u, 0u};
   g.init();
+  LinksGlobal lk{P.lst, P.nact, P.blocked0, P.blocked1, P.inv_scale};
   for (int sc = 0; sc < P.num_scen; ++sc) {
-    if (P.mode == 0) event_loop(g, P, sc, S);
+    if (P.mode == 0) event_loop(g, P, lk, sc, S);
     else solve_only(g, P, sc, S);
     g.sync();
   }

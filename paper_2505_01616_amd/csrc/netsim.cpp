@@ -52,8 +52,8 @@ struct netsim {
   bool prepared = false;
   bool has_result = false;
   int64_t F = 0, L = 0, nnz = 0, nsucc = 0;
+  int32_t num_parts = 0;              // independent parts (each with its own clock)
   std::vector<int32_t> dev_of_flow;   // id -> device flow index
-  std::vector<int32_t> link_base;     // scenario -> first device link
   std::vector<std::vector<int32_t>> dev_link;  // scenario, local link -> device link (-1 unused)
   std::vector<int32_t> h_cnt0;
   std::vector<double> h_rel0;
@@ -197,48 +197,141 @@ netsim_status check_ranks(netsim_t* h, int32_t s, int32_t p, const int32_t* rank
 }
 
 // ---------------------------------------------------------- device layout
+struct UnionFind {
+  std::vector<int32_t> p;
+  explicit UnionFind(size_t n) : p(n) {
+    for (size_t i = 0; i < n; ++i) p[i] = (int32_t)i;
+  }
+  int32_t find(int32_t x) {
+    while (p[(size_t)x] != x) {
+      p[(size_t)x] = p[(size_t)p[(size_t)x]];
+      x = p[(size_t)x];
+    }
+    return x;
+  }
+  void unite(int32_t a, int32_t b) {
+    a = find(a);
+    b = find(b);
+    if (a != b) p[(size_t)std::max(a, b)] = std::min(a, b);
+  }
+};
+
+// Largest number of parts a scenario is split into; beyond it consecutive
+// groups share a part (and its clock), which is always allowed.
+constexpr int32_t kMaxPartsPerScen = 1024;
+// Link components per part for the incremental re-solve; more are merged
+// into the last one (a coarser partition is still safe).
+constexpr int32_t kMaxComp = 4096;
+
 netsim_status prepare(netsim_t* h) {
   const int32_t S = (int32_t)h->scen.size();
   const int64_t F = (int64_t)h->f_bytes.size();
   h->F = F;
-  // device flow order: grouped by scenario, id order inside
-  h->dev_of_flow.assign((size_t)F, -1);
-  std::vector<int32_t> flow_of_dev((size_t)F);
-  std::vector<ScenCtl> ctl((size_t)S);
-  int64_t fd = 0;
+  // Parts: the flows of a scenario that are connected through shared links or
+  // dependencies (union-find over the scenario's flows and links).  Flows of
+  // different parts never interact in the fluid model, so every part runs
+  // with its own clock; the finish times are those of one clock per scenario
+  // up to rounding.  options.single_clock keeps each scenario whole.
+  std::vector<int32_t> part_of_id((size_t)F, 0);
+  std::vector<int32_t> part_scen;
+  std::vector<int32_t> loc((size_t)F, 0);  // id -> index inside its scenario
   for (int32_t s = 0; s < S; ++s) {
-    ScenCtl c{};
-    c.f0 = (int32_t)fd;
-    for (int64_t id : h->scen[s].flows) {
-      h->dev_of_flow[(size_t)id] = (int32_t)fd;
-      flow_of_dev[(size_t)fd] = (int32_t)id;
-      ++fd;
-    }
-    c.f1 = (int32_t)fd;
-    ctl[(size_t)s] = c;
+    const std::vector<int64_t>& fl = h->scen[s].flows;
+    for (size_t i = 0; i < fl.size(); ++i) loc[(size_t)fl[i]] = (int32_t)i;
   }
-  // used links per scenario, compacted
-  h->dev_link.assign((size_t)S, {});
-  h->link_base.assign((size_t)S + 1, 0);
-  int64_t ld = 0;
-  double maxcap = 0.0;
   for (int32_t s = 0; s < S; ++s) {
     const Scen& sc = h->scen[s];
-    std::vector<int32_t>& m = h->dev_link[(size_t)s];
+    const int64_t nf = (int64_t)sc.flows.size();
+    if (nf == 0) continue;
+    const int32_t P0 = (int32_t)part_scen.size();
+    if (h->opt.single_clock) {
+      for (int64_t id : sc.flows) part_of_id[(size_t)id] = P0;
+      part_scen.push_back(s);
+      continue;
+    }
+    const int64_t nl = (int64_t)sc.cap.size();
+    UnionFind uf((size_t)(nf + nl));
+    for (int64_t i = 0; i < nf; ++i) {
+      const int64_t id = sc.flows[(size_t)i];
+      for (int64_t e = h->p_off[(size_t)id]; e < h->p_off[(size_t)id + 1]; ++e)
+        uf.unite((int32_t)i, (int32_t)(nf + h->p_link[(size_t)e]));
+      for (int64_t k = h->d_off[(size_t)id]; k < h->d_off[(size_t)id + 1]; ++k)
+        uf.unite((int32_t)i, loc[(size_t)h->d_ids[(size_t)k]]);
+    }
+    std::vector<int32_t> label((size_t)(nf + nl), -1), grp((size_t)nf);
+    int32_t T = 0;
+    for (int64_t i = 0; i < nf; ++i) {
+      const int32_t r = uf.find((int32_t)i);
+      if (label[(size_t)r] < 0) label[(size_t)r] = T++;
+      grp[(size_t)i] = label[(size_t)r];
+    }
+    const int32_t np = std::min(T, kMaxPartsPerScen);
+    for (int64_t i = 0; i < nf; ++i)
+      part_of_id[(size_t)sc.flows[(size_t)i]] =
+          P0 + (int32_t)((int64_t)grp[(size_t)i] * np / T);
+    for (int32_t k = 0; k < np; ++k) part_scen.push_back(s);
+  }
+  const int32_t NP = (int32_t)part_scen.size();
+  h->num_parts = NP;
+  // device flow order: grouped by part, id order inside
+  std::vector<ScenCtl> ctl((size_t)NP);
+  std::vector<int64_t> pf((size_t)NP + 1, 0);
+  for (int64_t id = 0; id < F; ++id) pf[(size_t)part_of_id[(size_t)id] + 1] += 1;
+  for (int32_t k = 0; k < NP; ++k) pf[(size_t)k + 1] += pf[(size_t)k];
+  h->dev_of_flow.assign((size_t)F, -1);
+  std::vector<int32_t> flow_of_dev((size_t)F);
+  {
+    std::vector<int64_t> fill(pf.begin(), pf.end() - 1);
+    for (int64_t id = 0; id < F; ++id) {
+      const int64_t d = fill[(size_t)part_of_id[(size_t)id]]++;
+      h->dev_of_flow[(size_t)id] = (int32_t)d;
+      flow_of_dev[(size_t)d] = (int32_t)id;
+    }
+  }
+  for (int32_t k = 0; k < NP; ++k) {
+    ScenCtl c{};
+    c.f0 = (int32_t)pf[(size_t)k];
+    c.f1 = (int32_t)pf[(size_t)k + 1];
+    c.scen = part_scen[(size_t)k];
+    ctl[(size_t)k] = c;
+  }
+  // used links, compacted and grouped by part (a link belongs to the part of
+  // every flow that crosses it), scenario-local id order inside a part
+  h->dev_link.assign((size_t)S, {});
+  std::vector<int64_t> pl((size_t)NP + 1, 0);
+  std::vector<std::vector<int32_t>> part_of_link((size_t)S);
+  for (int32_t s = 0; s < S; ++s) {
+    const Scen& sc = h->scen[s];
+    std::vector<int32_t>& m = part_of_link[(size_t)s];
     m.assign(sc.cap.size(), -1);
     for (int64_t id : sc.flows)
-      for (int64_t e = h->p_off[(size_t)id]; e < h->p_off[(size_t)id + 1]; ++e) m[(size_t)h->p_link[(size_t)e]] = 0;
-    h->link_base[(size_t)s] = (int32_t)ld;
-    ctl[(size_t)s].l0 = (int32_t)ld;
-    for (size_t l = 0; l < m.size(); ++l)
-      if (m[l] == 0) {
-        m[l] = (int32_t)ld++;
-        maxcap = std::max(maxcap, sc.cap[l]);
-      }
-    ctl[(size_t)s].l1 = (int32_t)ld;
-    if (ld > std::numeric_limits<int32_t>::max()) return fail(h, NETSIM_E_LIMIT, "run: more than 2^31-1 used links");
+      for (int64_t e = h->p_off[(size_t)id]; e < h->p_off[(size_t)id + 1]; ++e)
+        m[(size_t)h->p_link[(size_t)e]] = part_of_id[(size_t)id];
+    for (int32_t k : m)
+      if (k >= 0) pl[(size_t)k + 1] += 1;
   }
-  h->link_base[(size_t)S] = (int32_t)ld;
+  for (int32_t k = 0; k < NP; ++k) pl[(size_t)k + 1] += pl[(size_t)k];
+  const int64_t ld = pl[(size_t)NP];
+  if (ld > std::numeric_limits<int32_t>::max()) return fail(h, NETSIM_E_LIMIT, "run: more than 2^31-1 used links");
+  double maxcap = 0.0;
+  {
+    std::vector<int64_t> fill(pl.begin(), pl.end() - 1);
+    for (int32_t s = 0; s < S; ++s) {
+      const Scen& sc = h->scen[s];
+      std::vector<int32_t>& m = h->dev_link[(size_t)s];
+      m.assign(sc.cap.size(), -1);
+      const std::vector<int32_t>& pk = part_of_link[(size_t)s];
+      for (size_t l = 0; l < m.size(); ++l)
+        if (pk[l] >= 0) {
+          m[l] = (int32_t)fill[(size_t)pk[l]]++;
+          maxcap = std::max(maxcap, sc.cap[l]);
+        }
+    }
+  }
+  for (int32_t k = 0; k < NP; ++k) {
+    ctl[(size_t)k].l0 = (int32_t)pl[(size_t)k];
+    ctl[(size_t)k].l1 = (int32_t)pl[(size_t)k + 1];
+  }
   h->L = ld;
   h->nnz = (int64_t)h->p_link.size();
   // fixed-point scale: largest capacity below 2^61 units
@@ -270,36 +363,31 @@ netsim_status prepare(netsim_t* h) {
     ndeps[(size_t)d] = (int32_t)(h->d_off[(size_t)id + 1] - h->d_off[(size_t)id]);
   }
   poff[(size_t)F] = (int32_t)e;
-  // components of the flow-link graph per scenario (union-find over links);
-  // flows of different components never share a link, so a change in one
-  // cannot move a rate in another.  More than kMaxComp components are merged
-  // into the last one (a coarser partition is still safe).
-  constexpr int32_t kMaxComp = 4096;
+  // shared-memory solve: paths of at most 6 links, local link ids below 0xFFFF
+  for (int32_t k = 0; k < NP; ++k) {
+    ScenCtl& c = ctl[(size_t)k];
+    int32_t deg = 0;
+    for (int32_t d = c.f0; d < c.f1; ++d) deg = std::max(deg, poff[(size_t)d + 1] - poff[(size_t)d]);
+    c.lds_paths = (deg <= 6 && c.l1 - c.l0 < 0xFFFF) ? 1 : 0;
+  }
+  // link components per part (union-find over links only): flows of
+  // different components never share a link, so a change in one cannot move
+  // a rate in another
   std::vector<int32_t> comp_of_dev((size_t)std::max<int64_t>(F, 1), 0);
   int32_t ncomp_total = 0;
   {
-    std::vector<int32_t> parent((size_t)std::max<int64_t>(ld, 1));
-    for (int64_t l = 0; l < ld; ++l) parent[(size_t)l] = (int32_t)l;
-    auto find = [&](int32_t x) {
-      while (parent[(size_t)x] != x) {
-        parent[(size_t)x] = parent[(size_t)parent[(size_t)x]];
-        x = parent[(size_t)x];
-      }
-      return x;
-    };
+    UnionFind uf((size_t)std::max<int64_t>(ld, 1));
     for (int64_t d = 0; d < F; ++d)
-      for (int32_t e = poff[(size_t)d] + 1; e < poff[(size_t)d + 1]; ++e) {
-        const int32_t a = find(plink[(size_t)poff[(size_t)d]]), b = find(plink[(size_t)e]);
-        if (a != b) parent[(size_t)std::max(a, b)] = std::min(a, b);
-      }
+      for (int32_t k = poff[(size_t)d] + 1; k < poff[(size_t)d + 1]; ++k)
+        uf.unite(plink[(size_t)poff[(size_t)d]], plink[(size_t)k]);
     std::vector<int32_t> label((size_t)std::max<int64_t>(ld, 1), -1);
-    for (int32_t s = 0; s < S; ++s) {
-      ScenCtl& cs = ctl[(size_t)s];
+    for (int32_t p = 0; p < NP; ++p) {
+      ScenCtl& cs = ctl[(size_t)p];
       int32_t n = 0;
       for (int32_t d = cs.f0; d < cs.f1; ++d) {
         int32_t k = 0;
         if (poff[(size_t)d + 1] > poff[(size_t)d]) {
-          const int32_t r = find(plink[(size_t)poff[(size_t)d]]);
+          const int32_t r = uf.find(plink[(size_t)poff[(size_t)d]]);
           if (label[(size_t)r] < 0) label[(size_t)r] = n < kMaxComp ? n++ : kMaxComp - 1;
           k = label[(size_t)r];
         }
@@ -330,8 +418,8 @@ netsim_status prepare(netsim_t* h) {
   h->h_cnt0 = ndeps;
   h->h_rel0.assign((size_t)std::max<int64_t>(F, 1), 0.0);
   h->h_pend0.assign((size_t)std::max<int64_t>(F, 1), 0);
-  for (int32_t s = 0; s < S; ++s) {
-    ScenCtl& c = ctl[(size_t)s];
+  for (int32_t k = 0; k < NP; ++k) {
+    ScenCtl& c = ctl[(size_t)k];
     int32_t np = 0;
     for (int32_t d = c.f0; d < c.f1; ++d)
       if (ndeps[(size_t)d] == 0) {
@@ -378,7 +466,7 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.comp2, sizeof(int32_t) * Fz},
       {(void**)&P.unf0, sizeof(int32_t) * Fz},
       {(void**)&P.unf1, sizeof(int32_t) * Fz},
-      {(void**)&P.ctl, sizeof(ScenCtl) * (size_t)std::max<int32_t>(S, 1)},
+      {(void**)&P.ctl, sizeof(ScenCtl) * (size_t)std::max<int32_t>(NP, 1)},
       {(void**)&P.bar, sizeof(uint32_t) * 1024},
       {(void**)&P.slots, sizeof(uint64_t) * 8},
   };
@@ -411,10 +499,7 @@ netsim_status prepare(netsim_t* h) {
     he = hipMemcpy((void*)u.dst, u.src, u.bytes, hipMemcpyHostToDevice);
     if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (upload)");
   }
-  P.num_scen = S;
-  int64_t max_deg = 0;
-  for (int64_t d = 0; d < F; ++d) max_deg = std::max<int64_t>(max_deg, poff[(size_t)d + 1] - poff[(size_t)d]);
-  P.lds_ok = max_deg <= 6 ? 1 : 0;
+  P.num_scen = NP;
   P.scale = h->scale;
   P.inv_scale = 1.0 / h->scale;
   h->prepared = true;
@@ -462,7 +547,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms) {
   P.debug = h->opt.debug;
   P.max_rounds = h->opt.max_rounds > 0 ? h->opt.max_rounds
                                        : (int32_t)std::min<int64_t>(h->F + 1, std::numeric_limits<int32_t>::max());
-  const int32_t S = (int32_t)h->scen.size();
+  const int32_t S = h->num_parts;
   int exec = h->opt.exec;
   if (exec == NETSIM_EXEC_AUTO) exec = (S > 1 || h->F < 100000) ? NETSIM_EXEC_BLOCK : NETSIM_EXEC_GRID;
   hipEvent_t e0, e1;
@@ -499,7 +584,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms) {
 }
 
 netsim_status collect(netsim_t* h, std::vector<ScenCtl>* ctl_out) {
-  const int32_t S = (int32_t)h->scen.size();
+  const int32_t S = h->num_parts;
   std::vector<ScenCtl> ctl((size_t)S);
   hipError_t he = hipMemcpy(ctl.data(), h->prm.ctl, sizeof(ScenCtl) * (size_t)S, hipMemcpyDeviceToHost);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (control blocks)");
@@ -508,7 +593,7 @@ netsim_status collect(netsim_t* h, std::vector<ScenCtl>* ctl_out) {
     const int32_t st = ctl[(size_t)s].status;
     if (st < 0) {
       if (st == -8)
-        return fail(h, NETSIM_E_DEVICE, "debug check failed in scenario " + std::to_string(s) +
+        return fail(h, NETSIM_E_DEVICE, "debug check failed in scenario " + std::to_string(ctl[(size_t)s].scen) +
                                             ": event " + std::to_string(ctl[(size_t)s].dbg[0] - 1) +
                                             " link " + std::to_string(ctl[(size_t)s].dbg[1]) +
                                             " last solve path " + std::to_string(ctl[(size_t)s].dbg[2]));
@@ -517,7 +602,7 @@ netsim_status collect(netsim_t* h, std::vector<ScenCtl>* ctl_out) {
                         : st == netsim_dev::ST_OVERFLOW ? "work list fault"
                                                         : "non-positive fair share";
       return fail(h, st == netsim_dev::ST_ROUNDS ? NETSIM_E_LIMIT : NETSIM_E_DEVICE,
-                  "device solver fault in scenario " + std::to_string(s) + ": " + why);
+                  "device solver fault in scenario " + std::to_string(ctl[(size_t)s].scen) + ": " + why);
     }
   }
   return NETSIM_OK;
@@ -741,19 +826,19 @@ netsim_status netsim_run(netsim_t* h, void* hip_stream) {
   }
   h->finish.assign((size_t)F, 0.0);
   for (int64_t id = 0; id < F; ++id) h->finish[(size_t)id] = fin_dev[(size_t)h->dev_of_flow[(size_t)id]];
-  const int32_t S = (int32_t)h->scen.size();
-  h->makespan.assign((size_t)S, 0.0);
+  h->makespan.assign(h->scen.size(), 0.0);
   netsim_stats s{};
   s.complete = 1;
-  for (int32_t k = 0; k < S; ++k) {
+  s.parts = h->num_parts;
+  const int32_t NP = h->num_parts;
+  for (int32_t k = 0; k < NP; ++k) {
     const ScenCtl& c = ctl[(size_t)k];
-    double m = 0.0;
+    double& m = h->makespan[(size_t)c.scen];
     for (int32_t d = c.f0; d < c.f1; ++d)
       if (!std::isnan(fin_dev[(size_t)d])) {
         m = std::max(m, fin_dev[(size_t)d]);
         s.completed_flows += 1;
       }
-    h->makespan[(size_t)k] = m;
     s.events += c.events;
     s.solves += c.solves;
     s.rounds += c.rounds;
@@ -769,7 +854,7 @@ netsim_status netsim_run(netsim_t* h, void* hip_stream) {
   int khz = 0;
   if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->opt.device) != hipSuccess || khz <= 0)
     khz = 100000;
-  for (int32_t k = 0; k < S; ++k)
+  for (int32_t k = 0; k < NP; ++k)
     for (int j = 0; j < 8; ++j) s.phase_seconds[j] += (double)ctl[(size_t)k].ticks[j] / (1e3 * khz);
   s.device_seconds = ms * 1e-3;
   s.upload_seconds = std::chrono::duration<double>(t1 - t0).count();
@@ -830,19 +915,35 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, con
   const Params& P = h->prm;
   std::vector<ScenCtl> ctl = h->h_ctl0;
   for (auto& c : ctl) c.n_solve = 0;
-  ctl[(size_t)scen].n_solve = (int32_t)n_active;
-  std::vector<int32_t> list((size_t)std::max<int64_t>(n_active, 1));
+  // the active flows of each part, listed in that part's act0 slice (parts
+  // share no link, so the allocation splits into one solve per part)
+  std::vector<int32_t> part_of((size_t)std::max<int64_t>(n_active, 1));
+  for (int64_t k = 0; k < n_active; ++k) {
+    const int32_t d = h->dev_of_flow[(size_t)active_ids[k]];
+    int32_t lo = 0, hi = h->num_parts - 1;
+    while (lo < hi) {
+      const int32_t mid = (lo + hi) / 2;
+      if (ctl[(size_t)mid].f1 <= d) lo = mid + 1; else hi = mid;
+    }
+    part_of[(size_t)k] = lo;
+    ctl[(size_t)lo].n_solve += 1;
+  }
+  std::vector<int32_t> list((size_t)std::max<int64_t>(h->F, 1));
+  std::vector<int32_t> dev((size_t)std::max<int64_t>(n_active, 1));
+  std::vector<int32_t> fill((size_t)std::max<int32_t>(h->num_parts, 1), 0);
   std::vector<int32_t> nact((size_t)std::max<int64_t>(h->L, 1), 0);
   for (int64_t k = 0; k < n_active; ++k) {
     const int64_t id = active_ids[k];
     const int32_t d = h->dev_of_flow[(size_t)id];
-    list[(size_t)k] = d;
+    const int32_t pk = part_of[(size_t)k];
+    dev[(size_t)k] = d;
+    list[(size_t)(ctl[(size_t)pk].f0 + fill[(size_t)pk]++)] = d;
     for (int64_t e = h->p_off[(size_t)id]; e < h->p_off[(size_t)id + 1]; ++e)
       nact[(size_t)h->dev_link[(size_t)scen][(size_t)h->p_link[(size_t)e]]] += 1;
   }
   he = hipMemcpy(P.ctl, ctl.data(), sizeof(ScenCtl) * ctl.size(), hipMemcpyHostToDevice);
-  if (he == hipSuccess && n_active > 0)
-    he = hipMemcpy(P.act0 + ctl[(size_t)scen].f0, list.data(), sizeof(int32_t) * (size_t)n_active, hipMemcpyHostToDevice);
+  if (he == hipSuccess && h->F > 0)
+    he = hipMemcpy(P.act0, list.data(), sizeof(int32_t) * (size_t)h->F, hipMemcpyHostToDevice);
   if (he == hipSuccess) he = hipMemcpy(P.nact, nact.data(), sizeof(int32_t) * nact.size(), hipMemcpyHostToDevice);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (solve_once setup)");
   float ms = 0.0f;
@@ -854,18 +955,23 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, con
   std::vector<double> rate((size_t)std::max<int64_t>(h->F, 1));
   he = hipMemcpy(rate.data(), P.rate, sizeof(double) * (size_t)std::max<int64_t>(h->F, 1), hipMemcpyDeviceToHost);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (rates)");
-  for (int64_t k = 0; k < n_active; ++k) rates_out[k] = rate[(size_t)list[(size_t)k]];
+  for (int64_t k = 0; k < n_active; ++k) rates_out[k] = rate[(size_t)dev[(size_t)k]];
   h->stats = netsim_stats{};
-  h->stats.solves = out[(size_t)scen].solves;
-  h->stats.rounds = out[(size_t)scen].rounds;
-  h->stats.flows_swept = out[(size_t)scen].flows_swept;
-  h->stats.incidences_swept = out[(size_t)scen].incidences_swept;
-  h->stats.device_seconds = ms * 1e-3;
   h->stats.complete = 1;
+  h->stats.parts = h->num_parts;
+  h->stats.device_seconds = ms * 1e-3;
   int khz = 0;
   if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->opt.device) != hipSuccess || khz <= 0)
     khz = 100000;
-  for (int j = 0; j < 8; ++j) h->stats.phase_seconds[j] = (double)out[(size_t)scen].ticks[j] / (1e3 * khz);
+  for (int32_t k = 0; k < h->num_parts; ++k) {
+    const ScenCtl& c = out[(size_t)k];
+    if (c.scen != scen) continue;
+    h->stats.solves += c.solves;
+    h->stats.rounds += c.rounds;
+    h->stats.flows_swept += c.flows_swept;
+    h->stats.incidences_swept += c.incidences_swept;
+    for (int j = 0; j < 8; ++j) h->stats.phase_seconds[j] += (double)c.ticks[j] / (1e3 * khz);
+  }
   return NETSIM_OK;
 }
 

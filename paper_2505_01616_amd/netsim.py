@@ -34,7 +34,7 @@ class netsim_options(ctypes.Structure):
     _fields_ = [("device", ctypes.c_int32), ("exec", ctypes.c_int32),
                 ("max_events", ctypes.c_int64), ("until", ctypes.c_double),
                 ("max_rounds", ctypes.c_int32), ("block_threads", ctypes.c_int32),
-                ("debug", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("debug", ctypes.c_int32), ("single_clock", ctypes.c_int32)]
 
 
 class netsim_topology(ctypes.Structure):
@@ -56,7 +56,7 @@ class netsim_stats(ctypes.Structure):
                 ("incidences_swept", ctypes.c_int64), ("active_swept", ctypes.c_int64),
                 ("pending_swept", ctypes.c_int64), ("completed_flows", ctypes.c_int64),
                 ("reselected", ctypes.c_int64), ("wide_solves", ctypes.c_int64),
-                ("complete", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("complete", ctypes.c_int32), ("parts", ctypes.c_int32),
                 ("sim_time", ctypes.c_double), ("device_seconds", ctypes.c_double),
                 ("upload_seconds", ctypes.c_double), ("phase_seconds", ctypes.c_double * 8)]
 
@@ -142,10 +142,11 @@ def netsim_default_options() -> netsim_options:
 
 
 def make_options(device=0, exec=EXEC_AUTO, max_events=0, until=math.inf, max_rounds=0,
-                 block_threads=0, debug=0) -> netsim_options:
+                 block_threads=0, debug=0, single_clock=0) -> netsim_options:
     o = netsim_default_options()
     o.device, o.exec, o.max_events, o.until = device, exec, max_events, until
     o.max_rounds, o.block_threads, o.debug = max_rounds, block_threads, debug
+    o.single_clock = single_clock
     return o
 
 

@@ -52,52 +52,74 @@ def _run(prog, program, **opt):
 @pytest.mark.parametrize("mode", ["chained", "flat", "aggregated"])
 @pytest.mark.parametrize("exec_", ["block", "grid"])
 def test_c1(mode, exec_):
+    """Per-flow finish times against the oracle, split into independent parts
+    and with one clock; with one clock the event and solve counts are the
+    oracle's too."""
     ns, pr = _gpu()
     _say(f"test_c1 mode={mode} exec={exec_}")
     program = configs.c1(1, mode=mode)
     ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
-    fins, stats = pr.run_program(program, ns.make_options(exec=ex))
     ref = osim.run_scenario(program.scenarios[0])
+    fins, stats = pr.run_program(program, ns.make_options(exec=ex))
     assert _rel(fins[0], ref.finish) < TOL
-    assert stats["events"] == ref.events and stats["solves"] == ref.solves
     assert stats["complete"] == 1
+    one, s1 = pr.run_program(program, ns.make_options(exec=ex, single_clock=1))
+    assert _rel(one[0], ref.finish) < TOL
+    assert s1["events"] == ref.events and s1["solves"] == ref.solves and s1["parts"] == 1
 
 
-def test_micro_batched_vs_oracle():
-    """200 random dynamic cases as 200 scenarios of one batched run."""
+@pytest.mark.parametrize("single_clock", [1, 0])
+def test_micro_batched_vs_oracle(single_clock):
+    """200 random dynamic cases as 200 scenarios of one batched run.  With one
+    clock per scenario the event count is the oracle's exactly; split into
+    independent parts the finish times still agree."""
     ns, pr = _gpu()
-    _say("test_micro_batched_vs_oracle")
+    _say(f"test_micro_batched_vs_oracle single_clock={single_clock}")
     scs = []
     for seed in range(200):
         scs += micro.random_dynamic(seed, integer_caps=(seed % 2 == 0)).scenarios
     program = Program("micro-batch", scs)
-    fins, stats = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK))
+    fins, stats = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK,
+                                                          single_clock=single_clock))
     ev = 0
     for s, sc in enumerate(scs):
         ref = osim.run_scenario(sc)
         assert _rel(fins[s], ref.finish) < TOL, s
         ev += ref.events
-    assert stats["events"] == ev
+    if single_clock:
+        assert stats["events"] == ev and stats["parts"] == len(scs)
+    else:
+        assert stats["events"] >= ev and stats["parts"] >= len(scs)
 
 
-def test_block_and_grid_agree_bitwise_and_deterministic():
+@pytest.mark.parametrize("single_clock", [0, 1])
+def test_block_and_grid_agree_bitwise_and_deterministic(single_clock):
+    """Integer link state makes the result independent of the layout (one
+    workgroup per part with link state in shared memory, or the whole grid
+    with link state in global memory) and of the run."""
     ns, pr = _gpu()
-    _say("test_block_and_grid_agree")
+    _say(f"test_block_and_grid_agree single_clock={single_clock}")
     program = configs.c2(2, tp_reps=6)
-    a, _ = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK))
-    b, _ = pr.run_program(program, ns.make_options(exec=ns.EXEC_GRID))
-    c, _ = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK))
+    a, sa = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK, single_clock=single_clock))
+    b, sb = pr.run_program(program, ns.make_options(exec=ns.EXEC_GRID, single_clock=single_clock))
+    c, _ = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK, single_clock=single_clock))
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[0], c[0])
+    assert sa["events"] == sb["events"] and sa["solves"] == sb["solves"]
+    assert (sa["parts"] == 1) == bool(single_clock)
 
 
 def test_c2_full():
     ns, pr = _gpu()
     _say("test_c2_full")
     program = configs.c2(2)
-    fins, stats = pr.run_program(program, ns.make_options())
     ref = osim.run_scenario(program.scenarios[0])
+    fins, stats = pr.run_program(program, ns.make_options())
     assert _rel(fins[0], ref.finish) < TOL
-    _say("c2 events", stats["events"], ref.events, "solves", stats["solves"], ref.solves)
+    one, s1 = pr.run_program(program, ns.make_options(single_clock=1))
+    assert _rel(one[0], ref.finish) < TOL
+    assert s1["events"] == ref.events and s1["solves"] == ref.solves
+    _say("c2 events: parts", stats["events"], "one clock", s1["events"], "oracle", ref.events,
+         "parts", stats["parts"])
 
 
 def _perturbed(fs, k):
@@ -151,18 +173,21 @@ def test_c4_one_group_full_run():
         assert _rel(fins[0], ref.finish) < TOL
 
 
-def test_c4_full_size_prefix():
-    """Full 4096-GPU C4, simulated up to the time the oracle reaches in its
-    first 60 events; every flow finished by then must agree."""
+@pytest.mark.parametrize("exec_", ["block", "grid"])
+def test_c4_full_size_prefix(exec_):
+    """Full 4096-GPU C4 (8 independent parts of 8 expert groups each),
+    simulated up to the time the oracle reaches in its first 60 events; every
+    flow finished by then must agree."""
     ns, pr = _gpu()
-    _say("test_c4_full_size_prefix")
+    _say(f"test_c4_full_size_prefix exec={exec_}")
     program = configs.c4(4)
     fs = oflows.expand(program.scenarios[0])
     probe = osim.run_flowset(fs, max_events=60)
     T = float(np.nanmax(probe.finish)) if np.isfinite(probe.finish).any() else 2e-4
     ref = osim.run_flowset(fs, until=T)
-    fins, stats = pr.run_program(program, ns.make_options(exec=ns.EXEC_GRID, until=T))
-    assert stats["complete"] == 0
+    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
+    fins, stats = pr.run_program(program, ns.make_options(exec=ex, until=T))
+    assert stats["complete"] == 0 and stats["parts"] == 8
     assert _rel(fins[0], ref.finish) < TOL
     _say("c4 prefix T", T, "flows done", int(np.isfinite(ref.finish).sum()),
          "events", stats["events"], ref.events)
@@ -211,17 +236,20 @@ def test_c5_full_batched():
     _say("test_c5_full_batched")
     gold = _golden("c5_makespans.json")["scenarios"]
     program = configs.c5(5)
-    ld = pr.load_program(program, ns.make_options())
-    try:
-        ns.netsim_run(ld.handle)
-        ms = ns.netsim_get_makespan(ld.handle, len(program.scenarios))
-        st = ns.netsim_get_stats(ld.handle)
-    finally:
-        ld.close()
     want = np.array([g["makespan"] for g in gold])
-    assert _rel(ms, want) < TOL
-    assert st["events"] == sum(g["events"] for g in gold)
-    _say("c5 full: device s", st["device_seconds"], "events", st["events"])
+    for single_clock in (0, 1):
+        ld = pr.load_program(program, ns.make_options(single_clock=single_clock))
+        try:
+            ns.netsim_run(ld.handle)
+            ms = ns.netsim_get_makespan(ld.handle, len(program.scenarios))
+            st = ns.netsim_get_stats(ld.handle)
+        finally:
+            ld.close()
+        assert _rel(ms, want) < TOL
+        if single_clock:
+            assert st["events"] == sum(g["events"] for g in gold)
+        _say("c5 full: single_clock", single_clock, "device s", st["device_seconds"],
+             "events", st["events"], "parts", st["parts"])
 
 
 def test_c3_full_size():
