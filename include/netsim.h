@@ -141,7 +141,7 @@ typedef struct {
   int64_t pending_swept;     /* sum over events of pending flows visited         */
   int64_t completed_flows;   /* flows with a finish time                         */
   int64_t reselected;        /* sum over solves of flows whose rate was re-solved */
-  int64_t wide_solves;       /* solves too large for one workgroup's shared memory */
+  int64_t wide_solves;       /* solves that needed work lists in global memory     */
   int32_t complete;          /* 1 if every scenario ran to its end               */
   int32_t parts;             /* independent parts simulated (see netsim_options) */
   double sim_time;           /* largest simulated time reached over scenarios    */

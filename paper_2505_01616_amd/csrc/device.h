@@ -40,6 +40,7 @@ struct ScenCtl {
   int32_t cnt_sel;         // flows taken back for re-solving in the current event
   int32_t succ_flag[2];    // a flow finished in this event has dependants
   int32_t solve_rc;        // status of a solve run by one workgroup
+  uint32_t stamp;          // last freezing-round number used by the part's solves
 };
 
 enum : int32_t {
@@ -68,6 +69,8 @@ struct Params {
   const int32_t* soff;     // [F+1] successor offsets
   const int32_t* succ;     // [nsucc]
   const int64_t* R0;       // [L] capacity in fixed point
+  const uint4* path16;     // [F] path as six 16-bit part-local link ids (0xFFFF =
+                           //     none; valid in parts with lds_paths)
   // dynamic flow state
   double* rem;             // [F] bytes left (active flows)
   double* rate;            // [F] current rate
@@ -83,8 +86,7 @@ struct Params {
   // dynamic link state
   int64_t* lst;            // [2L] per link: residual capacity (fixed point), unfrozen flows
   int32_t* nact;           // [L] active flows
-  uint8_t* blocked0;       // [L] round flags (two, alternating)
-  uint8_t* blocked1;
+  uint32_t* fl;            // [L] number of the freezing round that blocked the link
   // work lists, each [F], used per scenario on [f0, f1)
   int32_t* act0; int32_t* act1;
   int32_t* pend0; int32_t* pend1;

@@ -64,7 +64,7 @@ struct BlockG {
   __device__ int nthr() const { return blockDim.x; }
   __device__ bool aborted() const { return false; }
   __device__ void sync() { __syncthreads(); }
-  __device__ double min_all(double v) {
+  __device__ __forceinline__ double min_all(double v) {
     v = wave_min(v);
     const int w = threadIdx.x >> 6;
     if (lane_id() == 0) lds[w] = v;
@@ -250,6 +250,9 @@ struct GridG {
   }
 };
 
+template <class G> struct IsGrid { static constexpr bool value = false; };
+template <> struct IsGrid<GridG> { static constexpr bool value = true; };
+
 // Appends the lanes with `pred` to a list: one atomic per wave.  Must be
 // reached by every lane of the wave.  Returns the slot (or -1 without pred).
 template <class G>
@@ -300,12 +303,96 @@ __device__ __forceinline__ void block_append(G& g, int32_t* const* counters, con
   __syncthreads();
 }
 
+// One workgroup: the first slot of each thread in each of NL lists, given the
+// items each thread puts there as bit masks.  A wave-level inclusive scan,
+// the wave totals in shared memory, and one fetch-add per list on its
+// counter.  Every thread of the workgroup must call it (NL <= 4).
+template <int NL>
+__device__ __forceinline__ void block_reserve(BlockG& g, const uint64_t* mask, int32_t* const* counters,
+                                              int* first) {
+  int* sh = g.ldsi;  // [k*16 + w] wave totals, then offsets; [96 + k] list bases
+  const int lane = lane_id(), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int incl[NL];
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    int x = (int)__popcll(mask[k]);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    incl[k] = x;
+    if (lane == 63) sh[k * 16 + w] = x;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < NL) {
+    const int k = threadIdx.x;
+    int total = 0;
+    for (int j = 0; j < nw; ++j) {
+      const int c = sh[k * 16 + j];
+      sh[k * 16 + j] = total;
+      total += c;
+    }
+    sh[96 + k] = total ? g.add(counters[k], (int32_t)total) : 0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < NL; ++k) first[k] = sh[96 + k] + sh[k * 16 + w] + incl[k] - (int)__popcll(mask[k]);
+  __syncthreads();
+}
+
+// Runs decide(i, pred) for every item i < n of the group (pred[k]: the item
+// goes to list k, counted by counters[k]) and then put(k, slot, i) for every
+// list it goes to.  One workgroup with n <= 64 * blockDim.x keeps the
+// decisions as per-thread bit masks (items t + j*T) and takes all slots from
+// one prefix sum; otherwise chunks of one item per thread are appended with
+// block_append.  Every thread of the group must call it.
+template <int NL, class G, class Decide, class Put>
+__device__ __forceinline__ void sweep_append(G& g, int n, int32_t* const* counters, Decide decide,
+                                             Put put) {
+  const int T = g.nthr();
+  if constexpr (!IsGrid<G>::value) {
+    if (n <= 64 * T) {
+      uint64_t mask[NL];
+#pragma unroll
+      for (int k = 0; k < NL; ++k) mask[k] = 0;
+      for (int j = 0; j * T < n; ++j) {
+        const int i = (int)threadIdx.x + j * T;
+        if (i < n) {
+          bool pr[NL] = {};
+          decide(i, pr);
+#pragma unroll
+          for (int k = 0; k < NL; ++k)
+            if (pr[k]) mask[k] |= 1ull << j;
+        }
+      }
+      int first[NL];
+      block_reserve<NL>(g, mask, counters, first);
+#pragma unroll
+      for (int k = 0; k < NL; ++k)
+        for (uint64_t m = mask[k]; m; m &= m - 1)
+          put(k, first[k]++, (int)threadIdx.x + (__ffsll((unsigned long long)m) - 1) * T);
+      return;
+    }
+  }
+  for (int base = g.block_base(); base < n; base += T) {
+    const int i = base + (int)threadIdx.x;
+    bool pr[NL] = {};
+    if (i < n) decide(i, pr);
+    int slot[NL];
+    block_append<NL>(g, counters, pr, slot);
+#pragma unroll
+    for (int k = 0; k < NL; ++k)
+      if (pr[k]) put(k, slot[k], i);
+  }
+}
+
 // Per-phase wall-clock accounting by the group's first thread, kept in
 // shared memory (acc[0..8) and the last reading in acc[8]).
 struct Clock {
   bool on;
   uint64_t* acc;
-  __device__ Clock(bool o, uint64_t* a) : on(o), acc(a) {
+  __device__ __forceinline__ Clock(bool o, uint64_t* a) : on(o), acc(a) {
     if (on) {
       for (int k = 0; k < 8; ++k) acc[k] = 0;
       acc[8] = wall_clock64();
@@ -320,104 +407,205 @@ struct Clock {
   }
 };
 
+// Counters of a part's run, in shared memory, advanced by each workgroup's
+// first thread only (they are the same for every thread of the group).
+struct Tally {
+  uint64_t clk[9];
+  int64_t solves, rounds, fsw, asw, psw, sel, wide;
+};
+
 // A flow id read from a work list must lie in the scenario's range.
 __device__ __forceinline__ bool in_range(int f, int f0, int cap) {
   return (unsigned)(f - f0) < (unsigned)cap;
 }
 
 // ------------------------------------------------------------ link state
-// Per link: residual capacity R (fixed point), unfrozen flows n, active
-// flows nact and two alternating "blocked" flags.  Two homes for it, with
-// one interface taking device link ids:
+// Per link: residual capacity R (fixed point), unfrozen flows n, active flows
+// nact and a "blocked" stamp: a link is blocked in a freezing round iff its
+// stamp equals that round's number, so flags never need clearing (round
+// numbers keep growing through a part's solves; see next_rounds).  Two homes
+// for the state, with one interface taking device link ids:
 //   LinksGlobal - global memory; any group (the whole grid, or a workgroup
 //                 on a part too large for shared memory);
 //   LinksShared - the shared memory of the one workgroup running a part
-//                 whose links fit there; atomics stay inside the CU.
-// Blocked flags of one round, indexed by device link id.
-struct Flags {
-  uint8_t* p;
-  int off;
-  __device__ uint8_t& operator[](int l) const { return p[l - off]; }
-};
-
+//                 whose links fit there; its atomics stay inside the CU.
 struct LinksGlobal {
+  static constexpr bool kTable = false;  // shares computed where they are needed
   int64_t* lst;      // [2L] (R, n) pairs: one 16-byte load per link
   int32_t* nact;
-  uint8_t* bl0;
-  uint8_t* bl1;
+  uint32_t* fl;
   double inv;
-  __device__ double share(int l) const {
+  __device__ __forceinline__ double share(int l) const {
     const longlong2 v = *reinterpret_cast<const longlong2*>(lst + 2 * l);
     return ((double)v.x / (double)v.y) * inv;
   }
-  __device__ void set(int l, int64_t R, int64_t n) {
+  __device__ __forceinline__ void set(int l, int64_t R, int64_t n) {
     lst[2 * l] = R;
     lst[2 * l + 1] = n;
   }
-  __device__ int nactv(int l) const { return nact[l]; }
-  __device__ void clear_flags(int l) {
-    bl0[l] = 0;
-    bl1[l] = 0;
-  }
+  __device__ __forceinline__ int64_t nfree(int l) const { return lst[2 * l + 1]; }
+  __device__ __forceinline__ int nactv(int l) const { return nact[l]; }
+  __device__ __forceinline__ void clear_flag(int l) { fl[l] = 0; }
   // link at rest: full capacity, no flow (active counts are cleared by the host)
-  __device__ void reset(int l, int64_t R) {
+  __device__ __forceinline__ void reset(int l, int64_t R) {
     set(l, R, 0);
-    clear_flags(l);
+    fl[l] = 0;
   }
-  __device__ Flags flags(int r) const { return Flags{(r & 1) ? bl1 : bl0, 0}; }
-  template <class G> __device__ void addR(G& g, int l, int64_t v) { g.add(&lst[2 * l], v); }
-  template <class G> __device__ void addN(G& g, int l, int64_t v) { g.add(&lst[2 * l + 1], v); }
-  template <class G> __device__ void addNact(G& g, int l, int32_t v) { g.add(&nact[l], v); }
+  __device__ __forceinline__ void block(int l, uint32_t st) { fl[l] = st; }
+  __device__ __forceinline__ bool blocked(int l, uint32_t st) const { return fl[l] == st; }
+  template <class G> __device__ __forceinline__ void addR(G& g, int l, int64_t v) { g.add(&lst[2 * l], v); }
+  template <class G> __device__ __forceinline__ void addN(G& g, int l, int64_t v) { g.add(&lst[2 * l + 1], v); }
+  template <class G> __device__ __forceinline__ void addNact(G& g, int l, int32_t v) { g.add(&nact[l], v); }
 };
 
-constexpr int LDS_LINKS = 2816;
-
-struct LinkLds {
-  int64_t R[LDS_LINKS];
-  int32_t n[LDS_LINKS];
-  int32_t nact[LDS_LINKS];
-  uint8_t bl[2][LDS_LINKS];
-};
+// Shared-memory pool of the block kernel: a part whose links fit keeps its
+// link state there (LINK_LDS_BYTES per link) and uses the rest as a cache of
+// path records for the flows of its solves (FLOW_LDS_BYTES per flow).
+constexpr int POOL_BYTES = 152 * 1024;
+constexpr int LINK_LDS_BYTES = 28;  // R 8, n 4, nact 4, stamp 4, share 8
+constexpr int FLOW_LDS_BYTES = 20;  // path record 16, flow id 4
 
 struct LinksShared {
-  LinkLds* s;
+  static constexpr bool kTable = true;  // shares of a round in a table (link pass)
+  int64_t* R;
+  double* sh;
+  int32_t* n;
+  int32_t* nact;
+  uint32_t* fl;
   int l0;
   double inv;
-  __device__ double share(int l) const {
+  // Carves the link arrays for nl links out of the pool (16-byte aligned).
+  __device__ __forceinline__ LinksShared(unsigned char* pool, int first, int nl, double inv_scale)
+      : l0(first), inv(inv_scale) {
+    const int nl2 = (nl + 1) & ~1;
+    R = reinterpret_cast<int64_t*>(pool);
+    sh = reinterpret_cast<double*>(pool + 8 * nl2);
+    n = reinterpret_cast<int32_t*>(pool + 16 * nl2);
+    nact = n + nl2;
+    fl = reinterpret_cast<uint32_t*>(nact + nl2);
+  }
+  __device__ __forceinline__ double share(int l) const {
     const int i = l - l0;
-    return ((double)s->R[i] / (double)s->n[i]) * inv;
+    return ((double)R[i] / (double)n[i]) * inv;
   }
-  __device__ void set(int l, int64_t R, int64_t n) {
-    s->R[l - l0] = R;
-    s->n[l - l0] = (int32_t)n;
+  __device__ __forceinline__ double table(int l) const { return sh[l - l0]; }
+  // link pass of a round: the share of every link with an unfrozen flow
+  __device__ __forceinline__ void fill_table(int tid, int T, int nl) {
+    for (int i = tid; i < nl; i += T)
+      if (n[i] > 0) sh[i] = ((double)R[i] / (double)n[i]) * inv;
   }
-  __device__ int nactv(int l) const { return s->nact[l - l0]; }
-  __device__ void clear_flags(int l) {
-    s->bl[0][l - l0] = 0;
-    s->bl[1][l - l0] = 0;
+  __device__ __forceinline__ void set(int l, int64_t Rv, int64_t nv) {
+    R[l - l0] = Rv;
+    n[l - l0] = (int32_t)nv;
   }
-  __device__ void reset(int l, int64_t R) {
-    set(l, R, 0);
-    s->nact[l - l0] = 0;
-    clear_flags(l);
+  __device__ __forceinline__ int64_t nfree(int l) const { return n[l - l0]; }
+  __device__ __forceinline__ int nactv(int l) const { return nact[l - l0]; }
+  __device__ __forceinline__ void clear_flag(int l) { fl[l - l0] = 0; }
+  __device__ __forceinline__ void reset(int l, int64_t Rv) {
+    set(l, Rv, 0);
+    nact[l - l0] = 0;
+    fl[l - l0] = 0;
   }
-  __device__ Flags flags(int r) const { return Flags{s->bl[r & 1], l0}; }
-  template <class G> __device__ void addR(G&, int l, int64_t v) {
-    __hip_atomic_fetch_add(&s->R[l - l0], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  __device__ __forceinline__ void block(int l, uint32_t st) { fl[l - l0] = st; }
+  __device__ __forceinline__ bool blocked(int l, uint32_t st) const { return fl[l - l0] == st; }
+  template <class G> __device__ __forceinline__ void addR(G&, int l, int64_t v) {
+    __hip_atomic_fetch_add(&R[l - l0], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   }
-  template <class G> __device__ void addN(G&, int l, int64_t v) {
-    __hip_atomic_fetch_add(&s->n[l - l0], (int32_t)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  template <class G> __device__ __forceinline__ void addN(G&, int l, int64_t v) {
+    __hip_atomic_fetch_add(&n[l - l0], (int32_t)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   }
-  template <class G> __device__ void addNact(G&, int l, int32_t v) {
-    __hip_atomic_fetch_add(&s->nact[l - l0], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  template <class G> __device__ __forceinline__ void addNact(G&, int l, int32_t v) {
+    __hip_atomic_fetch_add(&nact[l - l0], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   }
 };
+
+// Bytes of the pool taken by the link arrays of nl links.
+__host__ __device__ constexpr int link_pool_bytes(int nl) { return LINK_LDS_BYTES * ((nl + 1) & ~1); }
+
+// First round number of a solve of part C (read by every thread after a
+// group barrier).  Far from wrapping every stamp is cleared and numbering
+// restarts, so a stale stamp can never equal a live round number.
+template <class G, class LK>
+__device__ __forceinline__ uint32_t first_round(G& g, const Params& P, LK& lk, ScenCtl* C) {
+  uint32_t base = g.load(&C->stamp);
+  if (base > 0x7FFFFFFFu) {
+    for (int l = C->l0 + g.tid(); l < C->l1; l += g.nthr()) lk.clear_flag(l);
+    g.sync();
+    base = 0;
+  }
+  return base + 1;
+}
+
+// Cold start of a solve (no event loop before it): capacities, the active
+// counts as unfrozen counts, no stamps.
+template <class G, class LK>
+__device__ __forceinline__ void cold_links(G& g, const Params& P, LK& lk, ScenCtl* C) {
+  for (int l = C->l0 + g.tid(); l < C->l1; l += g.nthr()) {
+    lk.set(l, P.R0[l], lk.nactv(l));
+    lk.clear_flag(l);
+  }
+}
+
+// Phase B for one flow: the smallest fair share on its path, and a stamp on
+// every link of the path whose share exceeds it by more than the tie band.
+// Returns the smallest share (bad = 1 when it is not a positive finite
+// number).
+template <class LK>
+__device__ __forceinline__ double share_of(const LK& lk, int l) {
+  if constexpr (LK::kTable) return lk.table(l);
+  else return lk.share(l);
+}
+
+// Link pass of a round when the link store keeps a share table: every
+// link's share, computed once, then read by all flows of the round.
+template <class G, class LK>
+__device__ __forceinline__ void round_table(G& g, LK& lk, const ScenCtl* C) {
+  if constexpr (LK::kTable) {
+    lk.fill_table(g.tid(), g.nthr(), C->l1 - C->l0);
+    g.sync();
+  }
+}
+
+template <class LK>
+__device__ __forceinline__ double share_and_block(LK& lk, const int* lv, int deg, uint32_t st,
+                                                  int& bad) {
+  double sv[6];
+  double m = INF;
+#pragma unroll
+  for (int k = 0; k < 6; ++k)
+    if (k < deg) {
+      sv[k] = share_of(lk, lv[k]);
+      m = sv[k] < m ? sv[k] : m;
+    }
+  const double thr = m * THR;
+#pragma unroll
+  for (int k = 0; k < 6; ++k)
+    if (k < deg && sv[k] > thr) lk.block(lv[k], st);
+  if (!(m > 0.0) || !(m < INF)) bad = 1;
+  return m;
+}
+
+// Unpacks a 16-byte path record: up to six link ids local to the part (16
+// bits each, NO_LINK = unused) into device link ids; returns the degree.
+constexpr uint32_t NO_LINK = 0xFFFFu;
+__device__ __forceinline__ int unpack_path(const uint4 rec, int l0, int* lv) {
+  const uint32_t w[3] = {rec.x, rec.y, rec.z};
+  int deg = 0;
+#pragma unroll
+  for (int k = 0; k < 6; ++k) {
+    const uint32_t u = (w[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+    lv[k] = l0 + (int)u;
+    deg += u != NO_LINK;
+  }
+  return deg;  // links are packed first, so lv[0..deg) are the path
+}
 
 // ------------------------------------------------------------- rate solve
 // Max-min rates of the n0 flows listed in list0 (all active), with work
-// lists in global memory.  Cold (warm = false): link state starts from the
-// capacities and the active counts; warm: from the residual state the event
-// loop prepared.  Returns 0 or a negative status.
+// lists in global memory (any group, any path length).  Cold (warm = false):
+// link state starts from the capacities and the active counts; warm: from
+// the residual state the event loop prepared.  Returns 0 or a negative
+// status.
 template <class G, class LK>
 __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, const int32_t* list0,
                                      int n0, int32_t* unf_a, int32_t* unf_b, int cap, int64_t& rounds,
@@ -425,29 +613,25 @@ __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, 
   const int T = g.nthr();
   const int tid = g.tid();
   const int b0 = g.block_base();
-  const bool one = g.nblocks() == 1;
-  if (!warm) {
-    for (int l = C->l0 + tid; l < C->l1; l += T) {
-      lk.set(l, P.R0[l], lk.nactv(l));
-      lk.clear_flags(l);
-    }
-  }
+  if (!warm) cold_links(g, P, lk, C);
   if (tid == 0) {
     g.store(&C->cnt_unf[0], 0);
     g.store(&C->cnt_unf[1], 0);
   }
   g.sync();
+  const uint32_t st0 = first_round(g, P, lk, C);
   clk.lap(2);
   const int32_t* in = list0;
   int n = n0;
   int r = 0;
   int bad = 0;
+  int rc = 0;
   for (;;) {
-    const Flags bl = lk.flags(r);
-    const Flags bl_next = lk.flags(r + 1);
+    const uint32_t st = st0 + (uint32_t)r;
     int32_t* out = (r & 1) ? unf_b : unf_a;
     int32_t* out_cnt = &C->cnt_unf[r & 1];
     if (tid == 0 && r > 0) g.store(out_cnt, 0);
+    round_table(g, lk, C);
     // phase B: smallest share on each path; block links above it
     for (int i = tid; i < n; i += T) {
       const int f = in[i];
@@ -455,32 +639,23 @@ __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, 
       const int e0 = P.poff[f], e1 = P.poff[f + 1];
       const int deg = e1 - e0;
       isw += deg;
-      double m = INF;
-      if (deg <= FAST_DEG) {
-        double sv[FAST_DEG];
-        int lv[FAST_DEG];
+      double m;
+      if (deg <= 6) {
+        int lv[6];
 #pragma unroll
-        for (int k = 0; k < FAST_DEG; ++k) {
-          if (k < deg) {
-            lv[k] = P.plink[e0 + k];
-            sv[k] = lk.share(lv[k]);
-            m = sv[k] < m ? sv[k] : m;
-          }
-        }
-        const double thr = m * THR;
-#pragma unroll
-        for (int k = 0; k < FAST_DEG; ++k)
-          if (k < deg && sv[k] > thr) bl[lv[k]] = 1;
+        for (int k = 0; k < 6; ++k) lv[k] = k < deg ? P.plink[e0 + k] : 0;
+        m = share_and_block(lk, lv, deg, st, bad);
       } else {
+        m = INF;
         for (int e = e0; e < e1; ++e) {
-          const double sh = lk.share(P.plink[e]);
+          const double sh = share_of(lk, P.plink[e]);
           m = sh < m ? sh : m;
         }
         const double thr = m * THR;
         for (int e = e0; e < e1; ++e)
-          if (lk.share(P.plink[e]) > thr) bl[P.plink[e]] = 1;
+          if (share_of(lk, P.plink[e]) > thr) lk.block(P.plink[e], st);
+        if (!(m > 0.0) || !(m < INF)) bad = 1;
       }
-      if (!(m > 0.0) || !(m < INF)) bad = 1;
       P.mf[f] = m;
     }
     clk.lap(3);
@@ -496,7 +671,7 @@ __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, 
       if (i < n && in_range(f, C->f0, cap)) {
         const int e0 = P.poff[f], e1 = P.poff[f + 1];
         bool frozen = false;
-        for (int e = e0; e < e1; ++e) frozen |= (bl[P.plink[e]] == 0);
+        for (int e = e0; e < e1; ++e) frozen |= !lk.blocked(P.plink[e], st);
         if (frozen) {
           const double m = P.mf[f];
           P.rate[f] = m;
@@ -519,126 +694,204 @@ __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, 
         else bad = 2;
       }
     }
-    // Blocked flags are clean outside solves.  Several workgroups: clear the
-    // next round's array now (its last readers passed a barrier) and this
-    // round's after the final barrier.  One workgroup: clear exactly the
-    // links this round may have flagged, once every thread has read them.
-    if (!one) {
-      for (int l = C->l0 + tid; l < C->l1; l += T) bl_next[l] = 0;
-    } else {
-      __syncthreads();
-      for (int i = tid; i < n; i += T) {
-        const int f = in[i];
-        if (in_range(f, C->f0, cap))
-          for (int e = P.poff[f]; e < P.poff[f + 1]; ++e) bl[P.plink[e]] = 0;
-      }
-    }
     if (bad) g.store(&C->fault_info, bad);
     clk.lap(5);
     g.sync();
     clk.lap(6);
-    rounds += 1;
-    fsw += n;
+    if (threadIdx.x == 0) {
+      rounds += 1;
+      fsw += n;
+    }
     if (g.aborted()) return ST_BARRIER;
     const int nout = g.load(out_cnt);
-    if (g.load(&C->fault_info) != 0) return g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE;
-    if (nout == 0) {
-      if (!one)
-        for (int l = C->l0 + tid; l < C->l1; l += T) bl[l] = 0;
-      return 0;
-    }
-    if (nout >= n) return ST_BAD_SHARE;  // a round must freeze something
-    if (++r > P.max_rounds) return ST_ROUNDS;
+    if (g.load(&C->fault_info) != 0) { rc = g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
+    if (nout == 0) break;
+    if (nout >= n) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
+    if (++r > P.max_rounds) { rc = ST_ROUNDS; break; }
     in = out;
     n = nout;
   }
+  if (tid == 0) g.store(&C->stamp, st0 + (uint32_t)r);
+  return rc;
+}
+
+// ---------------------------------------- one workgroup, unfrozen set as bit masks
+// Path records and ids of the first `cap` flows of a solve, in shared memory.
+struct FlowCache {
+  uint4* path;
+  int32_t* fid;
+  int cap;
+};
+
+// Thread t of the workgroup owns the flows list[t + k*T], k < 64, and keeps
+// which of them are still unfrozen as a 64-bit mask, so a round needs no list
+// compaction: the workgroup barriers, the path reads (one 16-byte record per
+// flow, from the shared-memory cache for the first fc.cap flows), the
+// link-state gathers and the freezing atomics.  With a share table the
+// smallest share of a frozen flow is read again from the table in phase C
+// (the table does not change within a round).  Paths must fit the record
+// (<= 6 links, part-local ids below 0xFFFF); n <= 64*T.
+template <class LK>
+__device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, ScenCtl* C,
+                                          const int32_t* list, int n, int64_t& rounds, int64_t& fsw,
+                                          int64_t& isw, Clock& clk, bool warm, const FlowCache& fc) {
+  const int T = blockDim.x;
+  const int l0 = C->l0;
+  const int f0 = C->f0, cap = C->f1 - C->f0;
+  int* cntr = g.ldsi + 112;  // three rotating counters of unfrozen flows
+  if (!warm) cold_links(g, P, lk, C);
+  uint64_t alive = 0;
+  for (int k = 0; k < 64; ++k)
+    if ((int)threadIdx.x + k * T < n) alive |= 1ull << k;
+  const int nc = min(n, fc.cap);
+  for (int i = threadIdx.x; i < nc; i += T) {
+    const int f = list[i];
+    fc.fid[i] = f;
+    fc.path[i] = in_range(f, f0, cap) ? P.path16[f] : make_uint4(~0u, ~0u, ~0u, ~0u);
+  }
+  if (threadIdx.x < 3) cntr[threadIdx.x] = 0;
+  __syncthreads();
+  const uint32_t st0 = first_round(g, P, lk, C);
+  clk.lap(2);
+  int total = n;
+  int r = 0;
+  int bad = 0;
+  int rc = 0;
+  for (;;) {
+    const uint32_t st = st0 + (uint32_t)r;
+    if (threadIdx.x == 0) cntr[(r + 1) % 3] = 0;
+    round_table(g, lk, C);
+    // phase B: smallest share on each path; block links above it
+    for (uint64_t m = alive; m; m &= m - 1) {
+      const int i = (int)threadIdx.x + (__ffsll((unsigned long long)m) - 1) * T;
+      const int f = i < nc ? fc.fid[i] : list[i];
+      if (!in_range(f, f0, cap)) { bad = 2; continue; }
+      int lv[6];
+      const int deg = unpack_path(i < nc ? fc.path[i] : P.path16[f], l0, lv);
+      isw += deg;
+      const double mv = share_and_block(lk, lv, deg, st, bad);
+      if constexpr (!LK::kTable) P.mf[f] = mv;
+    }
+    clk.lap(3);
+    __syncthreads();
+    clk.lap(4);
+    // phase C: freeze flows crossing an unblocked link
+    for (uint64_t m = alive; m; m &= m - 1) {
+      const int k = __ffsll((unsigned long long)m) - 1;
+      const int i = (int)threadIdx.x + k * T;
+      const int f = i < nc ? fc.fid[i] : list[i];
+      if (!in_range(f, f0, cap)) { bad = 2; continue; }
+      int lv[6];
+      const int deg = unpack_path(i < nc ? fc.path[i] : P.path16[f], l0, lv);
+      bool frozen = false;
+#pragma unroll
+      for (int j = 0; j < 6; ++j)
+        if (j < deg) frozen |= !lk.blocked(lv[j], st);
+      if (frozen) {
+        double mv;
+        if constexpr (LK::kTable) {
+          mv = INF;
+#pragma unroll
+          for (int j = 0; j < 6; ++j)
+            if (j < deg) {
+              const double sv = lk.table(lv[j]);
+              mv = sv < mv ? sv : mv;
+            }
+        } else {
+          mv = P.mf[f];
+        }
+        P.rate[f] = mv;
+        const int64_t qv = (int64_t)__builtin_rint(mv * P.scale);
+#pragma unroll
+        for (int j = 0; j < 6; ++j)
+          if (j < deg) {
+            lk.addR(g, lv[j], -qv);
+            lk.addN(g, lv[j], (int64_t)-1);
+          }
+        alive &= ~(1ull << k);
+      }
+    }
+    int c = __popcll(alive);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+    if (lane_id() == 0 && c > 0) atomicAdd(&cntr[r % 3], c);
+    if (bad) g.store(&C->fault_info, bad);
+    clk.lap(5);
+    __syncthreads();
+    clk.lap(6);
+    if (threadIdx.x == 0) {
+      rounds += 1;
+      fsw += total;
+    }
+    if (g.load(&C->fault_info) != 0) { rc = g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
+    const int left = cntr[r % 3];
+    if (left == 0) break;
+    if (left >= total) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
+    if (++r > P.max_rounds) { rc = ST_ROUNDS; break; }
+    total = left;
+  }
+  if (threadIdx.x == 0) g.store(&C->stamp, st0 + (uint32_t)r);
+  return rc;
 }
 
 // ---------------------------------------------- shared-memory-resident solve
-// Each workgroup takes a contiguous slice of the active list (at most
-// LDS_FLOWS flows), copies the flow ids and their padded paths (link ids
-// local to the part, 16 bits) into shared memory once, and keeps its
-// unfrozen flows as a shared-memory list.  Only link state and the rates are
-// touched outside, so a round costs one gather of link state, one of flags
-// and two barriers.
+// Grid layout: each workgroup takes a contiguous slice of the active list (at
+// most LDS_FLOWS flows), copies the flow ids and their path records into
+// shared memory once, and keeps its unfrozen flows as a shared-memory list.
+// Only link state and the rates are touched outside, so a round costs one
+// gather of link state, one of stamps and two grid barriers.
 constexpr int LDS_FLOWS = 3840;
-constexpr int LDS_DEG = 6;
-constexpr uint16_t NO_LINK = 0xFFFF;
 
 struct SolveLds {
   int32_t fid[LDS_FLOWS];
-  uint16_t link[LDS_FLOWS * LDS_DEG];
+  uint4 path[LDS_FLOWS];
   double mf[LDS_FLOWS];
   uint16_t u[2][LDS_FLOWS];
   int cnt;
-  uint64_t clk[9];
 };
 
 template <class G, class LK>
 __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl* C, const int32_t* list0,
                                          int n0, int64_t& rounds, int64_t& fsw, int64_t& isw, Clock& clk,
                                          SolveLds& S, bool warm) {
-  const int T = g.nthr();
   const int tid = g.tid();
   const int nb = g.nblocks();
   const int per = (n0 + nb - 1) / nb;
   const int c0 = min(n0, g.block_id() * per);
   const int nl = min(n0, c0 + per) - c0;
-  const bool one = nb == 1;
   const int l0 = C->l0;
-  if (!warm) {
-    for (int l = C->l0 + tid; l < C->l1; l += T) {
-      lk.set(l, P.R0[l], lk.nactv(l));
-      lk.clear_flags(l);
-    }
-  }
+  if (!warm) cold_links(g, P, lk, C);
   if (tid == 0)
     for (int k = 0; k < 3; ++k) g.store(&C->rem3[k], 0);
   int bad = 0;
   for (int j = threadIdx.x; j < nl; j += blockDim.x) {
     int f = list0[c0 + j];
     if (!in_range(f, C->f0, C->f1 - C->f0)) { bad = 2; f = C->f0; }
-    const int e0 = P.poff[f], e1 = P.poff[f + 1];
     S.fid[j] = f;
-#pragma unroll
-    for (int k = 0; k < LDS_DEG; ++k)
-      S.link[j * LDS_DEG + k] = e0 + k < e1 ? (uint16_t)(P.plink[e0 + k] - l0) : NO_LINK;
+    S.path[j] = P.path16[f];
     S.u[0][j] = (uint16_t)j;
   }
   int nu = nl;
   g.sync();
+  const uint32_t st0 = first_round(g, P, lk, C);
   clk.lap(2);
   int total = n0;
   int r = 0;
+  int rc = 0;
   for (;;) {
-    const Flags bl = lk.flags(r);
-    const Flags bl_next = lk.flags(r + 1);
+    const uint32_t st = st0 + (uint32_t)r;
     const uint16_t* uin = S.u[r & 1];
     uint16_t* uout = S.u[(r & 1) ^ 1];
     if (threadIdx.x == 0) S.cnt = 0;
     if (tid == 0) g.store(&C->rem3[(r + 1) % 3], 0);
+    round_table(g, lk, C);
     // phase B: smallest share on each path; block links above it
     for (int x = threadIdx.x; x < nu; x += blockDim.x) {
       const int j = uin[x];
-      double sv[LDS_DEG];
-      int lv[LDS_DEG];
-      double m = INF;
-#pragma unroll
-      for (int k = 0; k < LDS_DEG; ++k) {
-        const uint16_t u = S.link[j * LDS_DEG + k];
-        lv[k] = u == NO_LINK ? -1 : l0 + (int)u;
-        if (lv[k] >= 0) {
-          sv[k] = lk.share(lv[k]);
-          m = sv[k] < m ? sv[k] : m;
-          isw += 1;
-        }
-      }
-      const double thr = m * THR;
-#pragma unroll
-      for (int k = 0; k < LDS_DEG; ++k)
-        if (lv[k] >= 0 && sv[k] > thr) bl[lv[k]] = 1;
-      if (!(m > 0.0) || !(m < INF)) bad = 1;
-      S.mf[j] = m;
+      int lv[6];
+      const int deg = unpack_path(S.path[j], l0, lv);
+      isw += deg;
+      S.mf[j] = share_and_block(lk, lv, deg, st, bad);
     }
     clk.lap(3);
     g.sync();
@@ -650,24 +903,22 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
       int j = 0;
       if (x < nu) {
         j = uin[x];
+        int lv[6];
+        const int deg = unpack_path(S.path[j], l0, lv);
         bool frozen = false;
 #pragma unroll
-        for (int k = 0; k < LDS_DEG; ++k) {
-          const uint16_t u = S.link[j * LDS_DEG + k];
-          if (u != NO_LINK) frozen |= (bl[l0 + (int)u] == 0);
-        }
+        for (int k = 0; k < 6; ++k)
+          if (k < deg) frozen |= !lk.blocked(lv[k], st);
         if (frozen) {
           const double m = S.mf[j];
           P.rate[S.fid[j]] = m;
           const int64_t qv = (int64_t)__builtin_rint(m * P.scale);
 #pragma unroll
-          for (int k = 0; k < LDS_DEG; ++k) {
-            const uint16_t u = S.link[j * LDS_DEG + k];
-            if (u != NO_LINK) {
-              lk.addR(g, l0 + (int)u, -qv);
-              lk.addN(g, l0 + (int)u, (int64_t)-1);
+          for (int k = 0; k < 6; ++k)
+            if (k < deg) {
+              lk.addR(g, lv[k], -qv);
+              lk.addN(g, lv[k], (int64_t)-1);
             }
-          }
         } else {
           keep = true;
         }
@@ -682,41 +933,28 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
         if (keep) uout[b + (int)__popcll(mask & ((1ull << lane) - 1ull))] = (uint16_t)j;
       }
     }
-    if (!one)
-      for (int l = C->l0 + tid; l < C->l1; l += T) bl_next[l] = 0;
     if (bad) g.store(&C->fault_info, bad);
     __syncthreads();
     const int nu_new = S.cnt;
-    if (one) {
-      // clear exactly what this round may have flagged (every read is done)
-      for (int x = threadIdx.x; x < nu; x += blockDim.x) {
-        const int j = uin[x];
-#pragma unroll
-        for (int k = 0; k < LDS_DEG; ++k) {
-          const uint16_t u = S.link[j * LDS_DEG + k];
-          if (u != NO_LINK) bl[l0 + (int)u] = 0;
-        }
-      }
-    }
     if (threadIdx.x == 0 && nu_new > 0) g.add(&C->rem3[r % 3], (int32_t)nu_new);
     clk.lap(5);
     g.sync();
     clk.lap(6);
-    rounds += 1;
-    fsw += total;
-    if (g.aborted()) return ST_BARRIER;
-    if (g.load(&C->fault_info) != 0) return g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE;
-    const int left = g.load(&C->rem3[r % 3]);
-    if (left == 0) {
-      if (!one)
-        for (int l = C->l0 + tid; l < C->l1; l += T) bl[l] = 0;
-      return 0;
+    if (threadIdx.x == 0) {
+      rounds += 1;
+      fsw += total;
     }
-    if (left >= total) return ST_BAD_SHARE;  // a round must freeze something
-    if (++r > P.max_rounds) return ST_ROUNDS;
+    if (g.aborted()) return ST_BARRIER;
+    if (g.load(&C->fault_info) != 0) { rc = g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
+    const int left = g.load(&C->rem3[r % 3]);
+    if (left == 0) break;
+    if (left >= total) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
+    if (++r > P.max_rounds) { rc = ST_ROUNDS; break; }
     total = left;
     nu = nu_new;
   }
+  if (tid == 0) g.store(&C->stamp, st0 + (uint32_t)r);
+  return rc;
 }
 
 // Releases flow h whose last predecessor finished at t (called once per h).
@@ -765,7 +1003,8 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, ScenC
 constexpr double KEEP = 1.0 - 1e-9;  // safety margin below theta
 
 template <class G, class LK>
-__device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const int sc, SolveLds& S) {
+__device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const int sc, SolveLds* S,
+                                           Tally* tl, const FlowCache& fc) {
   ScenCtl* C = &P.ctl[sc];
   const int f0 = C->f0;
   const int cap = C->f1 - C->f0;
@@ -779,14 +1018,16 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   const int tid = g.tid();
   const int b0 = g.block_base();
   const int w0 = tid - lane_id();
-  Clock clk(tid == 0, S.clk);
+  Clock clk(tid == 0, tl->clk);
+  if (threadIdx.x == 0) tl->solves = tl->rounds = tl->fsw = tl->asw = tl->psw = tl->sel = tl->wide = 0;
+  int64_t& rounds = tl->rounds;
+  int64_t& fsw = tl->fsw;
   // links at rest: nothing active; no component has changed yet
   for (int l = C->l0 + tid; l < C->l1; l += T) lk.reset(l, P.R0[l]);
   const uint64_t INF_BITS = (uint64_t)__double_as_longlong(INF);
   for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
   double t = 0.0;
-  int64_t events = 0, solves = 0, rounds = 0, fsw = 0, isw = 0, asw = 0, psw = 0;
-  int64_t sel = 0, wide = 0;
+  int64_t events = 0, isw = 0;
   int nAct = 0;
   int nPend = C->n_pend0;
   int e = 0;  // event index: lists act[e&1], pend[e&1] are this event's input
@@ -821,8 +1062,10 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       const double rl = P.rel[f];
       loc = rl < loc ? rl : loc;
     }
-    asw += nAct;
-    psw += nPend;
+    if (threadIdx.x == 0) {
+      tl->asw += nAct;
+      tl->psw += nPend;
+    }
     const double tn = g.min_all(loc);
     clk.lap(0);
     if (g.aborted()) { status = ST_BARRIER; break; }
@@ -840,76 +1083,68 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     if (tid == 0) g.store(&C->cnt_comp[(q + 1) % 3], 0);
     int err = 0;
     // completions and advance
-    for (int base = b0; base < nAct; base += T) {
-      const int i = base + (int)threadIdx.x;
-      bool done = false, keep = false;
-      int f = -1;
-      if (i < nAct) f = actIn[i];
-      if (i < nAct && !in_range(f, f0, cap)) err = 1;
-      if (i < nAct && in_range(f, f0, cap)) {
-        const double r = P.rate[f];
-        const double dt = P.rem[f] / r;
-        const double tau = t + dt;
-        if (tau <= thr) {
-          done = true;
-          P.finish[f] = tn;
-          g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
-          const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
-          for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
-            const int l = P.plink[k];
-            lk.addNact(g, l, -1);
-            lk.addR(g, l, qv);  // its share returns to the link
-          }
-          if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
-        } else {
-          keep = true;
-          const double moved = r * step;
-          P.rem[f] = P.rem[f] - moved;
-        }
-      }
+    {
       int32_t* const cnts[2] = {compCnt, &C->cnt_act[ob]};
-      const bool pr[2] = {done, keep};
-      int slot[2];
-      block_append<2>(g, cnts, pr, slot);
-      if (done) { if (slot[0] < cap) compOut[slot[0]] = f; else err = 1; }
-      if (keep) { if (slot[1] < cap) actOut[slot[1]] = f; else err = 1; }
-      if (done) g.store(&C->changed[ib], 1);
+      sweep_append<2>(
+          g, nAct, cnts,
+          [&](int i, bool* pr) {
+            const int f = actIn[i];
+            if (!in_range(f, f0, cap)) { err = 1; return; }
+            const double r = P.rate[f];
+            const double dt = P.rem[f] / r;
+            const double tau = t + dt;
+            if (tau <= thr) {
+              pr[0] = true;
+              P.finish[f] = tn;
+              g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
+              const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
+              for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+                const int l = P.plink[k];
+                lk.addNact(g, l, -1);
+                lk.addR(g, l, qv);  // its share returns to the link
+              }
+              if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
+              g.store(&C->changed[ib], 1);
+            } else {
+              pr[1] = true;
+              const double moved = r * step;
+              P.rem[f] = P.rem[f] - moved;
+            }
+          },
+          [&](int k, int slot, int i) {
+            int32_t* out = k == 0 ? compOut : actOut;
+            if (slot < cap) out[slot] = actIn[i]; else err = 1;
+          });
     }
     // releases due now
-    for (int base = b0; base < nPend; base += T) {
-      const int i = base + (int)threadIdx.x;
-      bool zero = false, start = false, keep = false;
-      int f = -1;
-      if (i < nPend) f = pendIn[i];
-      if (i < nPend && !in_range(f, f0, cap)) err = 1;
-      if (i < nPend && in_range(f, f0, cap)) {
-        const double rl = P.rel[f];
-        if (rl <= tn) {
-          if (P.nbytes[f] == 0.0) {
-            zero = true;
-            P.finish[f] = rl;
-            if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
-          } else {
-            start = true;
-            P.rem[f] = P.nbytes[f];
-            P.born[f] = e;
-            for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) lk.addNact(g, P.plink[k], 1);
-          }
-        } else {
-          keep = true;
-        }
-      }
+    {
       int32_t* const cnts[4] = {compCnt, &C->cnt_act[ob], &C->cnt_pend[ob], &C->cnt_arr};
-      const bool pr[4] = {zero, start, keep, start};
-      int slot[4];
-      block_append<4>(g, cnts, pr, slot);
-      if (zero) { if (slot[0] < cap) compOut[slot[0]] = f; else err = 1; }
-      if (start) {
-        if (slot[1] < cap) actOut[slot[1]] = f; else err = 1;
-        if (slot[3] < cap) arrs[slot[3]] = f; else err = 1;
-        g.store(&C->changed[ib], 1);
-      }
-      if (keep) { if (slot[2] < cap) pendOut[slot[2]] = f; else err = 1; }
+      sweep_append<4>(
+          g, nPend, cnts,
+          [&](int i, bool* pr) {
+            const int f = pendIn[i];
+            if (!in_range(f, f0, cap)) { err = 1; return; }
+            const double rl = P.rel[f];
+            if (rl <= tn) {
+              if (P.nbytes[f] == 0.0) {
+                pr[0] = true;
+                P.finish[f] = rl;
+                if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
+              } else {
+                pr[1] = pr[3] = true;
+                P.rem[f] = P.nbytes[f];
+                P.born[f] = e;
+                for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) lk.addNact(g, P.plink[k], 1);
+                g.store(&C->changed[ib], 1);
+              }
+            } else {
+              pr[2] = true;
+            }
+          },
+          [&](int k, int slot, int i) {
+            int32_t* out = k == 0 ? compOut : k == 1 ? actOut : k == 2 ? pendOut : arrs;
+            if (slot < cap) out[slot] = pendIn[i]; else err = 1;
+          });
     }
     if (err) g.store(&C->fault_info, 2);
     g.sync();
@@ -987,74 +1222,73 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       // take back the flows at or above their component's theta (and the new
       // ones) for re-solving
       g.sync();
-      for (int base = b0; base < nNew; base += T) {
-        const int i = base + (int)threadIdx.x;
-        bool upper = false;
-        int f = -1;
-        if (i < nNew) {
-          f = actOut[i];
-          if (in_range(f, f0, cap)) {
-            const bool fresh = P.born[f] == e;
-            const double r = P.rate[f];
-            const double th = __longlong_as_double((long long)g.load(&P.theta[P.comp[f]]));
-            upper = fresh || !(r < th * KEEP);
-            if (upper) {
-              const int64_t qv = fresh ? 0 : (int64_t)__builtin_rint(r * P.scale);
-              for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
-                const int l = P.plink[k];
-                if (!fresh) lk.addR(g, l, qv);
-                lk.addN(g, l, (int64_t)1);
-              }
-            }
-          } else {
-            err = 1;
-          }
-        }
+      {
         int32_t* const cnts[1] = {&C->cnt_sel};
-        const bool pr[1] = {upper};
-        int slot[1];
-        block_append<1>(g, cnts, pr, slot);
-        if (upper) { if (slot[0] < cap) arrs[slot[0]] = f; else err = 1; }
+        sweep_append<1>(
+            g, nNew, cnts,
+            [&](int i, bool* pr) {
+              const int f = actOut[i];
+              if (!in_range(f, f0, cap)) { err = 1; return; }
+              const bool fresh = P.born[f] == e;
+              const double r = P.rate[f];
+              const double th = __longlong_as_double((long long)g.load(&P.theta[P.comp[f]]));
+              if (fresh || !(r < th * KEEP)) {
+                pr[0] = true;
+                const int64_t qv = fresh ? 0 : (int64_t)__builtin_rint(r * P.scale);
+                for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+                  const int l = P.plink[k];
+                  if (!fresh) lk.addR(g, l, qv);
+                  lk.addN(g, l, (int64_t)1);
+                }
+              }
+            },
+            [&](int, int slot, int i) {
+              if (slot < cap) arrs[slot] = actOut[i]; else err = 1;
+            });
       }
       if (err) g.store(&C->fault_info, 2);
       g.sync();
       clk.lap(7);
       for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
       const int nSel = g.load(&C->cnt_sel);
-      if (P.debug) {
-        // blocked flags must be clean between solves
-        for (int l = C->l0 + tid; l < C->l1; l += T)
-          if (lk.flags(0)[l] | lk.flags(1)[l]) {
-            g.store(&C->dbg[0], (int64_t)(e + 1));
-            g.store(&C->dbg[1], (int64_t)l);
-          }
-        g.sync();
-        if (g.load(&C->dbg[0]) != 0 && status == ST_DONE) { status = -8; break; }
-      }
-      sel += nSel;
-      wide += nSel > LDS_FLOWS ? 1 : 0;
+      if (threadIdx.x == 0) tl->sel += nSel;
       int rc = 0;
       if (nSel > 0) {
-        if (P.debug && tid == 0) g.store(&C->dbg[2], (int64_t)(nSel <= LDS_FLOWS ? 1 : nSel <= g.nblocks() * LDS_FLOWS ? 2 : 3));
-        if (C->lds_paths && nSel <= LDS_FLOWS) {
-          if (g.nblocks() == 1) {
-            rc = solve_lds(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
+        if constexpr (!IsGrid<G>::value) {
+          if (C->lds_paths && nSel <= 64 * (int)blockDim.x) {
+            rc = solve_mask(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc);
           } else {
+            if (threadIdx.x == 0) tl->wide += 1;
+            rc = solve(g, P, lk, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
+          }
+        } else {
+          if (C->lds_paths && nSel <= LDS_FLOWS) {
             if (g.block_id() == 0) {
               BlockG b{g.lds, g.ldsi};
-              const int r1 = solve_lds(b, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
+              const int r1 = solve_mask(b, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc);
               if (threadIdx.x == 0) g.store(&C->solve_rc, r1);
             }
             g.sync();
             rc = g.load(&C->solve_rc);
+          } else if (C->lds_paths && nSel <= g.nblocks() * LDS_FLOWS) {
+            rc = solve_lds(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, *S, true);
+          } else {
+            if (threadIdx.x == 0) tl->wide += 1;
+            rc = solve(g, P, lk, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
           }
-        } else if (C->lds_paths && nSel <= g.nblocks() * LDS_FLOWS) {
-          rc = solve_lds(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, S, true);
-        } else {
-          rc = solve(g, P, lk, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
         }
       }
-      solves += 1;  // the active set changed: one rate solve (possibly empty)
+      if (P.debug && rc == 0) {
+        // after a solve every active flow is frozen: no link has an unfrozen flow
+        for (int l = C->l0 + tid; l < C->l1; l += T)
+          if (lk.nfree(l) != 0) {
+            g.store(&C->dbg[0], (int64_t)(e + 1));
+            g.store(&C->dbg[1], (int64_t)l);
+          }
+        g.sync();
+        if (g.load(&C->dbg[0]) != 0) { status = -8; break; }
+      }
+      if (threadIdx.x == 0) tl->solves += 1;  // the active set changed: one rate solve (possibly empty)
       if (rc != 0) { status = rc; break; }
     }
     nAct = nNew;
@@ -1065,61 +1299,82 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   if (tid == 0) {
     C->t = t;
     C->events = events;
-    C->solves = solves;
-    C->rounds = rounds;
-    C->flows_swept = fsw;
-    C->active_swept = asw;
-    C->pending_swept = psw;
-    C->reselected = sel;
-    C->wide_solves = wide;
+    C->solves = tl->solves;
+    C->rounds = tl->rounds;
+    C->flows_swept = tl->fsw;
+    C->active_swept = tl->asw;
+    C->pending_swept = tl->psw;
+    C->reselected = tl->sel;
+    C->wide_solves = tl->wide;
     C->status = status;
-    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)S.clk[k];
+    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)tl->clk[k];
   }
 }
 
 template <class G>
-__device__ __forceinline__ void solve_only(G& g, const Params& P, const int sc, SolveLds& S) {
-  LinksGlobal lk{P.lst, P.nact, P.blocked0, P.blocked1, P.inv_scale};
+__device__ __forceinline__ void solve_only(G& g, const Params& P, const int sc, SolveLds* S,
+                                           Tally* tl, const FlowCache& fc) {
+  LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
   ScenCtl* C = &P.ctl[sc];
   const int f0 = C->f0;
-  int64_t rounds = 0, fsw = 0, isw = 0;
-  Clock clk(g.tid() == 0, S.clk);
+  if (threadIdx.x == 0) tl->rounds = tl->fsw = 0;
+  int64_t& rounds = tl->rounds;
+  int64_t& fsw = tl->fsw;
+  int64_t isw = 0;
+  Clock clk(g.tid() == 0, tl->clk);
   int rc = 0;
-  if (C->n_solve > 0)
-    rc = (C->lds_paths && C->n_solve <= g.nblocks() * LDS_FLOWS)
-             ? solve_lds(g, P, lk, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, S, false)
-             : solve(g, P, lk, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0,
-                     rounds, fsw, isw, clk, false);
+  if (C->n_solve > 0) {
+    if constexpr (IsGrid<G>::value) {
+      if (C->lds_paths && C->n_solve <= g.nblocks() * LDS_FLOWS)
+        rc = solve_lds(g, P, lk, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, *S, false);
+      else
+        rc = solve(g, P, lk, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0,
+                   rounds, fsw, isw, clk, false);
+    } else {
+      if (C->lds_paths && C->n_solve <= 64 * (int)blockDim.x)
+        rc = solve_mask(g, P, lk, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, false, fc);
+      else
+        rc = solve(g, P, lk, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0,
+                   rounds, fsw, isw, clk, false);
+    }
+  }
   g.add(&C->incidences_swept, isw);
   if (g.tid() == 0) {
     C->solves = C->n_solve > 0 ? 1 : 0;
-    C->rounds = rounds;
-    C->flows_swept = fsw;
+    C->rounds = tl->rounds;
+    C->flows_swept = tl->fsw;
     C->status = rc;
-    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)S.clk[k];
+    for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)tl->clk[k];
   }
 }
 
 }  // namespace
 
 // One workgroup per part.  A part whose links fit keeps its link state in
-// shared memory for the whole run.
+// shared memory for the whole run; the rest of the pool caches the path
+// records of the flows being solved.
 __global__ __launch_bounds__(1024) void netsim_block_kernel(Params P) {
   __shared__ double lds[32];
   __shared__ int ldsi[128];
-  __shared__ SolveLds S;
-  __shared__ LinkLds LL;
+  __shared__ Tally tally;
+  __shared__ __align__(16) unsigned char pool[POOL_BYTES];
   BlockG g{lds, ldsi};
   for (int sc = blockIdx.x; sc < P.num_scen; sc += gridDim.x) {
     const ScenCtl* C = &P.ctl[sc];
+    const int nl = C->l1 - C->l0;
+    const bool in_lds = P.mode == 0 && link_pool_bytes(nl) <= POOL_BYTES;
+    const int used = in_lds ? (link_pool_bytes(nl) + 15) & ~15 : 0;
+    const int ncache = (POOL_BYTES - used) / FLOW_LDS_BYTES;
+    const FlowCache fc{reinterpret_cast<uint4*>(pool + used),
+                       reinterpret_cast<int32_t*>(pool + used + 16 * ncache), ncache};
     if (P.mode != 0) {
-      solve_only(g, P, sc, S);
-    } else if (C->l1 - C->l0 <= LDS_LINKS) {
-      LinksShared lk{&LL, C->l0, P.inv_scale};
-      event_loop(g, P, lk, sc, S);
+      solve_only(g, P, sc, nullptr, &tally, fc);
+    } else if (in_lds) {
+      LinksShared lk(pool, C->l0, nl, P.inv_scale);
+      event_loop(g, P, lk, sc, nullptr, &tally, fc);
     } else {
-      LinksGlobal lk{P.lst, P.nact, P.blocked0, P.blocked1, P.inv_scale};
-      event_loop(g, P, lk, sc, S);
+      LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
+      event_loop(g, P, lk, sc, nullptr, &tally, fc);
     }
     __syncthreads();
   }
@@ -1130,12 +1385,14 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   __shared__ int ldsi[128];
   __shared__ int flag;
   __shared__ SolveLds S;
+  __shared__ Tally tally;
   GridG g{lds, ldsi, &flag, P.bar, P.slots, 0u, 0u, false, 0u, 0u, 0u};
   g.init();
-  LinksGlobal lk{P.lst, P.nact, P.blocked0, P.blocked1, P.inv_scale};
+  LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
+  const FlowCache none{nullptr, nullptr, 0};
   for (int sc = 0; sc < P.num_scen; ++sc) {
-    if (P.mode == 0) event_loop(g, P, lk, sc, S);
-    else solve_only(g, P, sc, S);
+    if (P.mode == 0) event_loop(g, P, lk, sc, &S, &tally, none);
+    else solve_only(g, P, sc, &S, &tally, none);
     g.sync();
   }
 }

@@ -363,12 +363,18 @@ netsim_status prepare(netsim_t* h) {
     ndeps[(size_t)d] = (int32_t)(h->d_off[(size_t)id + 1] - h->d_off[(size_t)id]);
   }
   poff[(size_t)F] = (int32_t)e;
-  // shared-memory solve: paths of at most 6 links, local link ids below 0xFFFF
+  // 16-byte path records (six 16-bit part-local link ids, 0xFFFF = none) for
+  // parts whose paths have at most 6 links and whose link ids fit 16 bits
+  std::vector<uint16_t> path16((size_t)std::max<int64_t>(F, 1) * 8, 0xFFFF);
   for (int32_t k = 0; k < NP; ++k) {
     ScenCtl& c = ctl[(size_t)k];
     int32_t deg = 0;
     for (int32_t d = c.f0; d < c.f1; ++d) deg = std::max(deg, poff[(size_t)d + 1] - poff[(size_t)d]);
     c.lds_paths = (deg <= 6 && c.l1 - c.l0 < 0xFFFF) ? 1 : 0;
+    if (!c.lds_paths) continue;
+    for (int32_t d = c.f0; d < c.f1; ++d)
+      for (int32_t j = poff[(size_t)d]; j < poff[(size_t)d + 1]; ++j)
+        path16[(size_t)d * 8 + (size_t)(j - poff[(size_t)d])] = (uint16_t)(plink[(size_t)j] - c.l0);
   }
   // link components per part (union-find over links only): flows of
   // different components never share a link, so a change in one cannot move
@@ -455,8 +461,8 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.arr, sizeof(int32_t) * Fz},
       {(void**)&P.lst, sizeof(int64_t) * 2 * Lz},
       {(void**)&P.nact, sizeof(int32_t) * Lz},
-      {(void**)&P.blocked0, Lz},
-      {(void**)&P.blocked1, Lz},
+      {(void**)&P.fl, sizeof(uint32_t) * Lz},
+      {(void**)&P.path16, 16 * Fz},
       {(void**)&P.act0, sizeof(int32_t) * Fz},
       {(void**)&P.act1, sizeof(int32_t) * Fz},
       {(void**)&P.pend0, sizeof(int32_t) * Fz},
@@ -494,6 +500,7 @@ netsim_status prepare(netsim_t* h) {
       {succ.data(), P.succ, sizeof(int32_t) * succ.size()},
       {R0.data(), P.R0, sizeof(int64_t) * R0.size()},
       {comp_of_dev.data(), P.comp, sizeof(int32_t) * comp_of_dev.size()},
+      {path16.data(), P.path16, sizeof(uint16_t) * path16.size()},
   };
   for (const Up& u : ups) {
     he = hipMemcpy((void*)u.dst, u.src, u.bytes, hipMemcpyHostToDevice);

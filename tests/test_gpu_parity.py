@@ -176,15 +176,18 @@ def test_c4_one_group_full_run():
 @pytest.mark.parametrize("exec_", ["block", "grid"])
 def test_c4_full_size_prefix(exec_):
     """Full 4096-GPU C4 (8 independent parts of 8 expert groups each),
-    simulated up to the time the oracle reaches in its first 60 events; every
-    flow finished by then must agree."""
+    simulated up to the last completion among the oracle's first 150 events
+    (the 64 group arrivals, then the first completions); every flow finished
+    by then must agree and the sets of finished flows must be equal."""
     ns, pr = _gpu()
     _say(f"test_c4_full_size_prefix exec={exec_}")
     program = configs.c4(4)
     fs = oflows.expand(program.scenarios[0])
-    probe = osim.run_flowset(fs, max_events=60)
-    T = float(np.nanmax(probe.finish)) if np.isfinite(probe.finish).any() else 2e-4
+    probe = osim.run_flowset(fs, max_events=150)
+    assert np.isfinite(probe.finish).sum() >= 50
+    T = float(np.nanmax(probe.finish))
     ref = osim.run_flowset(fs, until=T)
+    assert np.isfinite(ref.finish).sum() >= 50
     ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
     fins, stats = pr.run_program(program, ns.make_options(exec=ex, until=T))
     assert stats["complete"] == 0 and stats["parts"] == 8
