@@ -81,7 +81,8 @@ typedef struct {
   double until;              /* do not process events later than this time (s); +inf = none */
   int32_t max_rounds;        /* per-solve round watchdog; 0 = number of flows + 1 */
   int32_t block_threads;     /* threads per workgroup in block mode; 0 = 1024    */
-  int32_t debug;             /* 1: internal consistency checks on the device     */
+  int32_t debug;             /* bit 0: consistency checks on the device; bit 1:
+                                phase timers (netsim_stats.phase_seconds)        */
   int32_t single_clock;      /* 1: one part (one clock) per scenario             */
 } netsim_options;
 
@@ -147,10 +148,11 @@ typedef struct {
   double sim_time;           /* largest simulated time reached over scenarios    */
   double device_seconds;     /* device time of the last netsim_run (HIP events)  */
   double upload_seconds;     /* host->device preparation of the last run          */
-  /* Device time by phase, summed over scenarios, as seen by the first thread
-   * of the group running each scenario: [0] next-event search, [1] settling
-   * completions and releases, [2] solve set-up, [3] share/blocking sweep,
-   * [4] wait after it, [5] freezing sweep, [6] wait after it, [7] unused. */
+  /* Device time by phase, summed over parts, as seen by the first thread of
+   * the group running each part (only with debug bit 1; zero otherwise):
+   * [0] next-event search, [1] settling completions and releases, [2] solve
+   * set-up, [3] share/blocking sweep, [4] wait after it, [5] freezing sweep,
+   * [6] wait after it, [7] choosing the flows to re-solve. */
   double phase_seconds[8];
 } netsim_stats;
 

@@ -7,6 +7,23 @@
 
 namespace netsim_dev {
 
+// Counters of the event loop's work lists and flags of the current event.
+// Kernel scratch, zero when a part starts: in global memory (the part's
+// control block) when the whole grid runs the part, in shared memory when
+// one workgroup does.
+struct Lists {
+  int32_t act[2];          // active flows (input and output lists alternate)
+  int32_t pend[2];         // flows waiting for their release time
+  int32_t comp[3];         // flows finished in the current wave of releases
+  int32_t unf[2];          // unfrozen flows of a solve with global lists
+  int32_t changed[2];      // the active set changed in this event
+  int32_t rem3[3];         // shared-memory solve: unfrozen flows left, rotating
+  int32_t arr;             // flows activated in the current event
+  int32_t sel;             // flows taken back for re-solving in the current event
+  int32_t succ_flag[2];    // a flow finished in this event has dependants
+  int32_t solve_rc;        // status of a solve run by one workgroup
+};
+
 // Control block of one part in device memory.  A part is a set of flows of
 // one scenario that shares no link and no dependency with the rest of the
 // scenario, simulated with its own clock.  The host fills the ranges and the
@@ -29,18 +46,8 @@ struct ScenCtl {
   int32_t fault_info;
   int64_t ticks[8];        // wall-clock ticks per phase (first thread of the group)
   int64_t dbg[4];          // debug checks (options.debug)
-  // list counters (kernel scratch; zero at launch)
-  int32_t cnt_act[2];
-  int32_t cnt_pend[2];
-  int32_t cnt_comp[3];
-  int32_t cnt_unf[2];
-  int32_t changed[2];
-  int32_t rem3[3];         // shared-memory solve: unfrozen flows left, rotating
-  int32_t cnt_arr;         // flows activated in the current event
-  int32_t cnt_sel;         // flows taken back for re-solving in the current event
-  int32_t succ_flag[2];    // a flow finished in this event has dependants
-  int32_t solve_rc;        // status of a solve run by one workgroup
   uint32_t stamp;          // last freezing-round number used by the part's solves
+  Lists k;                 // list counters in global memory (grid layout)
 };
 
 enum : int32_t {

@@ -57,6 +57,8 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 struct BlockG {
   double* lds;
   int* ldsi;
+  Lists* lst;  // list counters in shared memory (zeroed when a part starts)
+  __device__ Lists* lists(ScenCtl*) const { return lst; }
   __device__ int tid() const { return threadIdx.x; }
   __device__ int block_base() const { return 0; }
   __device__ int nblocks() const { return 1; }
@@ -107,6 +109,8 @@ __device__ __forceinline__ unsigned xcc_id() {
 struct GridG {
   double* lds;
   int* ldsi;
+  Lists* blk_lists;  // shared-memory counters for a solve run by one workgroup
+  __device__ Lists* lists(ScenCtl* C) const { return &C->k; }
   int* flag;      // shared: abort state as seen by this block's thread 0
   uint32_t* bar;
   uint64_t* slots;
@@ -303,89 +307,63 @@ __device__ __forceinline__ void block_append(G& g, int32_t* const* counters, con
   __syncthreads();
 }
 
-// One workgroup: the first slot of each thread in each of NL lists, given the
-// items each thread puts there as bit masks.  A wave-level inclusive scan,
-// the wave totals in shared memory, and one fetch-add per list on its
-// counter.  Every thread of the workgroup must call it (NL <= 4).
-template <int NL>
-__device__ __forceinline__ void block_reserve(BlockG& g, const uint64_t* mask, int32_t* const* counters,
-                                              int* first) {
-  int* sh = g.ldsi;  // [k*16 + w] wave totals, then offsets; [96 + k] list bases
-  const int lane = lane_id(), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  int incl[NL];
-#pragma unroll
-  for (int k = 0; k < NL; ++k) {
-    int x = (int)__popcll(mask[k]);
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, 64);
-      if (lane >= o) x += y;
-    }
-    incl[k] = x;
-    if (lane == 63) sh[k * 16 + w] = x;
-  }
-  __syncthreads();
-  if ((int)threadIdx.x < NL) {
-    const int k = threadIdx.x;
-    int total = 0;
-    for (int j = 0; j < nw; ++j) {
-      const int c = sh[k * 16 + j];
-      sh[k * 16 + j] = total;
-      total += c;
-    }
-    sh[96 + k] = total ? g.add(counters[k], (int32_t)total) : 0;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < NL; ++k) first[k] = sh[96 + k] + sh[k * 16 + w] + incl[k] - (int)__popcll(mask[k]);
-  __syncthreads();
-}
-
-// Runs decide(i, pred) for every item i < n of the group (pred[k]: the item
-// goes to list k, counted by counters[k]) and then put(k, slot, i) for every
-// list it goes to.  One workgroup with n <= 64 * blockDim.x keeps the
-// decisions as per-thread bit masks (items t + j*T) and takes all slots from
-// one prefix sum; otherwise chunks of one item per thread are appended with
-// block_append.  Every thread of the group must call it.
-template <int NL, class G, class Decide, class Put>
-__device__ __forceinline__ void sweep_append(G& g, int n, int32_t* const* counters, Decide decide,
-                                             Put put) {
+// For every item i < n of the group: x = fetch(i) (loads only), then
+// decide(i, x, pred) (pred[k]: the item goes to list k, counted by
+// counters[k]), then put(k, slot, x) for every list it goes to.  One
+// workgroup fetches four items of a thread at a time (their loads in flight
+// together) and appends with one ballot and one shared-memory atomic per
+// wave and list, so the sweep needs no workgroup barrier (list order is
+// arbitrary; nothing depends on it).  The grid appends chunks of one item per
+// thread with block_append.  Every thread of the group must call it.
+template <int NL, class G, class Fetch, class Decide, class Put>
+__device__ __forceinline__ void sweep_append(G& g, int n, int32_t* const* counters, Fetch fetch,
+                                             Decide decide, Put put) {
   const int T = g.nthr();
   if constexpr (!IsGrid<G>::value) {
-    if (n <= 64 * T) {
-      uint64_t mask[NL];
+    using Item = decltype(fetch(0));
+    for (int j0 = 0; j0 * T < n; j0 += 4) {
+      Item x[4];
 #pragma unroll
-      for (int k = 0; k < NL; ++k) mask[k] = 0;
-      for (int j = 0; j * T < n; ++j) {
-        const int i = (int)threadIdx.x + j * T;
-        if (i < n) {
-          bool pr[NL] = {};
-          decide(i, pr);
+      for (int u = 0; u < 4; ++u) {
+        const int i = (int)threadIdx.x + (j0 + u) * T;
+        if (i < n) x[u] = fetch(i);
+      }
 #pragma unroll
-          for (int k = 0; k < NL; ++k)
-            if (pr[k]) mask[k] |= 1ull << j;
+      for (int u = 0; u < 4; ++u) {
+        const int i = (int)threadIdx.x + (j0 + u) * T;
+        bool pr[NL] = {};
+        if (i < n) decide(i, x[u], pr);
+#pragma unroll
+        for (int k = 0; k < NL; ++k) {
+          const int slot = wave_append(g, counters[k], pr[k]);
+          if (pr[k]) put(k, slot, x[u]);
         }
       }
-      int first[NL];
-      block_reserve<NL>(g, mask, counters, first);
-#pragma unroll
-      for (int k = 0; k < NL; ++k)
-        for (uint64_t m = mask[k]; m; m &= m - 1)
-          put(k, first[k]++, (int)threadIdx.x + (__ffsll((unsigned long long)m) - 1) * T);
-      return;
     }
+    return;
   }
   for (int base = g.block_base(); base < n; base += T) {
     const int i = base + (int)threadIdx.x;
     bool pr[NL] = {};
-    if (i < n) decide(i, pr);
+    decltype(fetch(0)) x{};
+    if (i < n) {
+      x = fetch(i);
+      decide(i, x, pr);
+    }
     int slot[NL];
     block_append<NL>(g, counters, pr, slot);
 #pragma unroll
     for (int k = 0; k < NL; ++k)
-      if (pr[k]) put(k, slot[k], i);
+      if (pr[k]) put(k, slot[k], x);
   }
 }
+
+// What a sweep loads for one item before deciding about it.
+struct FlowVal {
+  int f = -1;
+  int k = 0;
+  double a = 0.0, b = 0.0;
+};
 
 // Per-phase wall-clock accounting by the group's first thread, kept in
 // shared memory (acc[0..8) and the last reading in acc[8]).
@@ -393,10 +371,9 @@ struct Clock {
   bool on;
   uint64_t* acc;
   __device__ __forceinline__ Clock(bool o, uint64_t* a) : on(o), acc(a) {
-    if (on) {
+    if (threadIdx.x == 0)
       for (int k = 0; k < 8; ++k) acc[k] = 0;
-      acc[8] = wall_clock64();
-    }
+    if (on) acc[8] = wall_clock64();
   }
   __device__ __forceinline__ void lap(int k) {
     if (on) {
@@ -610,13 +587,14 @@ template <class G, class LK>
 __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, const int32_t* list0,
                                      int n0, int32_t* unf_a, int32_t* unf_b, int cap, int64_t& rounds,
                                      int64_t& fsw, int64_t& isw, Clock& clk, bool warm) {
+  Lists* K = g.lists(C);
   const int T = g.nthr();
   const int tid = g.tid();
   const int b0 = g.block_base();
   if (!warm) cold_links(g, P, lk, C);
   if (tid == 0) {
-    g.store(&C->cnt_unf[0], 0);
-    g.store(&C->cnt_unf[1], 0);
+    g.store(&K->unf[0], 0);
+    g.store(&K->unf[1], 0);
   }
   g.sync();
   const uint32_t st0 = first_round(g, P, lk, C);
@@ -629,7 +607,7 @@ __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, 
   for (;;) {
     const uint32_t st = st0 + (uint32_t)r;
     int32_t* out = (r & 1) ? unf_b : unf_a;
-    int32_t* out_cnt = &C->cnt_unf[r & 1];
+    int32_t* out_cnt = &K->unf[r & 1];
     if (tid == 0 && r > 0) g.store(out_cnt, 0);
     round_table(g, lk, C);
     // phase B: smallest share on each path; block links above it
@@ -723,6 +701,33 @@ struct FlowCache {
   int cap;
 };
 
+// Bit k set for every item t + k*T < n of this thread (k < 64).
+__device__ __forceinline__ uint64_t low_items(int n, int T) {
+  const int t = threadIdx.x;
+  const int c = n > t ? (n - t - 1) / T + 1 : 0;
+  return c >= 64 ? ~0ull : (1ull << c) - 1ull;
+}
+
+// Calls body(k, f, rec) for every item k set in `mask` (item i = t + k*T):
+// flow id and path record from the shared-memory cache for the items below
+// nc (bits in cmask), from global memory for the rest.  Two separate loops,
+// so that the two kinds of read are never merged into one access through a
+// generic pointer.
+template <class Body>
+__device__ __forceinline__ void for_items(uint64_t mask, uint64_t cmask, const FlowCache& fc,
+                                          const Params& P, const int32_t* list, int T, Body body) {
+  for (uint64_t m = mask & cmask; m; m &= m - 1) {
+    const int k = __ffsll((unsigned long long)m) - 1;
+    const int i = (int)threadIdx.x + k * T;
+    body(k, fc.fid[i], fc.path[i]);
+  }
+  for (uint64_t m = mask & ~cmask; m; m &= m - 1) {
+    const int k = __ffsll((unsigned long long)m) - 1;
+    const int f = list[(int)threadIdx.x + k * T];
+    body(k, f, P.path16[f]);
+  }
+}
+
 // Thread t of the workgroup owns the flows list[t + k*T], k < 64, and keeps
 // which of them are still unfrozen as a 64-bit mask, so a round needs no list
 // compaction: the workgroup barriers, the path reads (one 16-byte record per
@@ -740,10 +745,10 @@ __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, Sc
   const int f0 = C->f0, cap = C->f1 - C->f0;
   int* cntr = g.ldsi + 112;  // three rotating counters of unfrozen flows
   if (!warm) cold_links(g, P, lk, C);
-  uint64_t alive = 0;
-  for (int k = 0; k < 64; ++k)
-    if ((int)threadIdx.x + k * T < n) alive |= 1ull << k;
+  const uint64_t alive0 = low_items(n, T);
+  uint64_t alive = alive0;
   const int nc = min(n, fc.cap);
+  const uint64_t cmask = low_items(nc, T);  // items served from the cache
   for (int i = threadIdx.x; i < nc; i += T) {
     const int f = list[i];
     fc.fid[i] = f;
@@ -762,55 +767,51 @@ __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, Sc
     if (threadIdx.x == 0) cntr[(r + 1) % 3] = 0;
     round_table(g, lk, C);
     // phase B: smallest share on each path; block links above it
-    for (uint64_t m = alive; m; m &= m - 1) {
-      const int i = (int)threadIdx.x + (__ffsll((unsigned long long)m) - 1) * T;
-      const int f = i < nc ? fc.fid[i] : list[i];
-      if (!in_range(f, f0, cap)) { bad = 2; continue; }
+    for_items(alive, cmask, fc, P, list, T, [&](int, int f, uint4 rec) {
+      if (!in_range(f, f0, cap)) { bad = 2; return; }
       int lv[6];
-      const int deg = unpack_path(i < nc ? fc.path[i] : P.path16[f], l0, lv);
+      const int deg = unpack_path(rec, l0, lv);
       isw += deg;
       const double mv = share_and_block(lk, lv, deg, st, bad);
       if constexpr (!LK::kTable) P.mf[f] = mv;
-    }
+    });
     clk.lap(3);
     __syncthreads();
     clk.lap(4);
     // phase C: freeze flows crossing an unblocked link
-    for (uint64_t m = alive; m; m &= m - 1) {
-      const int k = __ffsll((unsigned long long)m) - 1;
-      const int i = (int)threadIdx.x + k * T;
-      const int f = i < nc ? fc.fid[i] : list[i];
-      if (!in_range(f, f0, cap)) { bad = 2; continue; }
+    uint64_t frozen_mask = 0;
+    for_items(alive, cmask, fc, P, list, T, [&](int k, int f, uint4 rec) {
+      if (!in_range(f, f0, cap)) { bad = 2; return; }
       int lv[6];
-      const int deg = unpack_path(i < nc ? fc.path[i] : P.path16[f], l0, lv);
+      const int deg = unpack_path(rec, l0, lv);
       bool frozen = false;
 #pragma unroll
       for (int j = 0; j < 6; ++j)
         if (j < deg) frozen |= !lk.blocked(lv[j], st);
-      if (frozen) {
-        double mv;
-        if constexpr (LK::kTable) {
-          mv = INF;
-#pragma unroll
-          for (int j = 0; j < 6; ++j)
-            if (j < deg) {
-              const double sv = lk.table(lv[j]);
-              mv = sv < mv ? sv : mv;
-            }
-        } else {
-          mv = P.mf[f];
-        }
-        P.rate[f] = mv;
-        const int64_t qv = (int64_t)__builtin_rint(mv * P.scale);
+      if (!frozen) return;
+      double mv;
+      if constexpr (LK::kTable) {
+        mv = INF;
 #pragma unroll
         for (int j = 0; j < 6; ++j)
           if (j < deg) {
-            lk.addR(g, lv[j], -qv);
-            lk.addN(g, lv[j], (int64_t)-1);
+            const double sv = lk.table(lv[j]);
+            mv = sv < mv ? sv : mv;
           }
-        alive &= ~(1ull << k);
+      } else {
+        mv = P.mf[f];
       }
-    }
+      P.rate[f] = mv;
+      const int64_t qv = (int64_t)__builtin_rint(mv * P.scale);
+#pragma unroll
+      for (int j = 0; j < 6; ++j)
+        if (j < deg) {
+          lk.addR(g, lv[j], -qv);
+          lk.addN(g, lv[j], (int64_t)-1);
+        }
+      frozen_mask |= 1ull << k;
+    });
+    alive &= ~frozen_mask;
     int c = __popcll(alive);
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
@@ -854,6 +855,7 @@ template <class G, class LK>
 __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl* C, const int32_t* list0,
                                          int n0, int64_t& rounds, int64_t& fsw, int64_t& isw, Clock& clk,
                                          SolveLds& S, bool warm) {
+  Lists* K = g.lists(C);
   const int tid = g.tid();
   const int nb = g.nblocks();
   const int per = (n0 + nb - 1) / nb;
@@ -862,7 +864,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
   const int l0 = C->l0;
   if (!warm) cold_links(g, P, lk, C);
   if (tid == 0)
-    for (int k = 0; k < 3; ++k) g.store(&C->rem3[k], 0);
+    for (int k = 0; k < 3; ++k) g.store(&K->rem3[k], 0);
   int bad = 0;
   for (int j = threadIdx.x; j < nl; j += blockDim.x) {
     int f = list0[c0 + j];
@@ -883,7 +885,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     const uint16_t* uin = S.u[r & 1];
     uint16_t* uout = S.u[(r & 1) ^ 1];
     if (threadIdx.x == 0) S.cnt = 0;
-    if (tid == 0) g.store(&C->rem3[(r + 1) % 3], 0);
+    if (tid == 0) g.store(&K->rem3[(r + 1) % 3], 0);
     round_table(g, lk, C);
     // phase B: smallest share on each path; block links above it
     for (int x = threadIdx.x; x < nu; x += blockDim.x) {
@@ -936,7 +938,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     if (bad) g.store(&C->fault_info, bad);
     __syncthreads();
     const int nu_new = S.cnt;
-    if (threadIdx.x == 0 && nu_new > 0) g.add(&C->rem3[r % 3], (int32_t)nu_new);
+    if (threadIdx.x == 0 && nu_new > 0) g.add(&K->rem3[r % 3], (int32_t)nu_new);
     clk.lap(5);
     g.sync();
     clk.lap(6);
@@ -946,7 +948,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     }
     if (g.aborted()) return ST_BARRIER;
     if (g.load(&C->fault_info) != 0) { rc = g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
-    const int left = g.load(&C->rem3[r % 3]);
+    const int left = g.load(&K->rem3[r % 3]);
     if (left == 0) break;
     if (left >= total) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
     if (++r > P.max_rounds) { rc = ST_ROUNDS; break; }
@@ -963,6 +965,7 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, ScenC
                                             int ob, int ib, int ev, int32_t* actOut,
                                             int32_t* pendOut, int32_t* arrOut, int32_t* cout,
                                             int32_t* coutCnt, int cap, int& err) {
+  Lists* K = g.lists(C);
   const double rl = P.start[h] + t;
   if (rl <= t) {
     if (P.nbytes[h] == 0.0) {
@@ -973,15 +976,15 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, ScenC
       P.rem[h] = P.nbytes[h];
       P.born[h] = ev;
       for (int j = P.poff[h]; j < P.poff[h + 1]; ++j) lk.addNact(g, P.plink[j], 1);
-      const int s = g.add(&C->cnt_act[ob], 1);
+      const int s = g.add(&K->act[ob], 1);
       if (s < cap) actOut[s] = h; else err = 1;
-      const int a = g.add(&C->cnt_arr, 1);
+      const int a = g.add(&K->arr, 1);
       if (a < cap) arrOut[a] = h; else err = 1;
-      g.store(&C->changed[ib], 1);
+      g.store(&K->changed[ib], 1);
     }
   } else {
     P.rel[h] = rl;
-    const int s = g.add(&C->cnt_pend[ob], 1);
+    const int s = g.add(&K->pend[ob], 1);
     if (s < cap) pendOut[s] = h; else err = 1;
   }
 }
@@ -1006,11 +1009,14 @@ template <class G, class LK>
 __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const int sc, SolveLds* S,
                                            Tally* tl, const FlowCache& fc) {
   ScenCtl* C = &P.ctl[sc];
+  Lists* K = g.lists(C);
   const int f0 = C->f0;
   const int cap = C->f1 - C->f0;
-  int32_t* act[2] = {P.act0 + f0, P.act1 + f0};
-  int32_t* pend[2] = {P.pend0 + f0, P.pend1 + f0};
-  int32_t* comp[3] = {P.comp0 + f0, P.comp1 + f0, P.comp2 + f0};
+  // alternating work lists, picked with selects (not runtime-indexed arrays,
+  // which would hide that they live in global memory)
+  auto act = [&](int k) { return k ? P.act1 + f0 : P.act0 + f0; };
+  auto pend = [&](int k) { return k ? P.pend1 + f0 : P.pend0 + f0; };
+  auto comp = [&](int k) { return k == 0 ? P.comp0 + f0 : k == 1 ? P.comp1 + f0 : P.comp2 + f0; };
   int32_t* unf_a = P.unf0 + f0;
   int32_t* unf_b = P.unf1 + f0;
   int32_t* arrs = P.arr + f0;
@@ -1018,7 +1024,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   const int tid = g.tid();
   const int b0 = g.block_base();
   const int w0 = tid - lane_id();
-  Clock clk(tid == 0, tl->clk);
+  Clock clk(tid == 0 && (P.debug & 2), tl->clk);
   if (threadIdx.x == 0) tl->solves = tl->rounds = tl->fsw = tl->asw = tl->psw = tl->sel = tl->wide = 0;
   int64_t& rounds = tl->rounds;
   int64_t& fsw = tl->fsw;
@@ -1035,17 +1041,17 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   int status = ST_DONE;
   for (;;) {
     const int ib = e & 1, ob = ib ^ 1;
-    const int32_t* actIn = act[ib];
-    int32_t* actOut = act[ob];
-    const int32_t* pendIn = pend[ib];
-    int32_t* pendOut = pend[ob];
+    const int32_t* actIn = act(ib);
+    int32_t* actOut = act(ob);
+    const int32_t* pendIn = pend(ib);
+    int32_t* pendOut = pend(ob);
     if (tid == 0) {
-      g.store(&C->cnt_act[ob], 0);
-      g.store(&C->cnt_pend[ob], 0);
-      g.store(&C->changed[ib], 0);
-      g.store(&C->succ_flag[ib], 0);
-      g.store(&C->cnt_arr, 0);
-      g.store(&C->cnt_sel, 0);
+      g.store(&K->act[ob], 0);
+      g.store(&K->pend[ob], 0);
+      g.store(&K->changed[ib], 0);
+      g.store(&K->succ_flag[ib], 0);
+      g.store(&K->arr, 0);
+      g.store(&K->sel, 0);
     }
     // next event time: earliest completion or release
     double loc = INF;
@@ -1078,20 +1084,29 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     events += 1;
     const double thr = tn * THR;
     const double step = tn - t;
-    int32_t* compOut = comp[q % 3];
-    int32_t* compCnt = &C->cnt_comp[q % 3];
-    if (tid == 0) g.store(&C->cnt_comp[(q + 1) % 3], 0);
+    int32_t* compOut = comp(q % 3);
+    int32_t* compCnt = &K->comp[q % 3];
+    if (tid == 0) g.store(&K->comp[(q + 1) % 3], 0);
     int err = 0;
     // completions and advance
     {
-      int32_t* const cnts[2] = {compCnt, &C->cnt_act[ob]};
+      int32_t* const cnts[2] = {compCnt, &K->act[ob]};
       sweep_append<2>(
           g, nAct, cnts,
-          [&](int i, bool* pr) {
-            const int f = actIn[i];
+          [&](int i) {
+            FlowVal x;
+            x.f = actIn[i];
+            if (in_range(x.f, f0, cap)) {
+              x.a = P.rate[x.f];
+              x.b = P.rem[x.f];
+            }
+            return x;
+          },
+          [&](int i, const FlowVal& x, bool* pr) {
+            const int f = x.f;
             if (!in_range(f, f0, cap)) { err = 1; return; }
-            const double r = P.rate[f];
-            const double dt = P.rem[f] / r;
+            const double r = x.a;
+            const double dt = x.b / r;
             const double tau = t + dt;
             if (tau <= thr) {
               pr[0] = true;
@@ -1103,47 +1118,53 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
                 lk.addNact(g, l, -1);
                 lk.addR(g, l, qv);  // its share returns to the link
               }
-              if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
-              g.store(&C->changed[ib], 1);
+              if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
+              g.store(&K->changed[ib], 1);
             } else {
               pr[1] = true;
               const double moved = r * step;
-              P.rem[f] = P.rem[f] - moved;
+              P.rem[f] = x.b - moved;
             }
           },
-          [&](int k, int slot, int i) {
+          [&](int k, int slot, const FlowVal& x) {
             int32_t* out = k == 0 ? compOut : actOut;
-            if (slot < cap) out[slot] = actIn[i]; else err = 1;
+            if (slot < cap) out[slot] = x.f; else err = 1;
           });
     }
     // releases due now
     {
-      int32_t* const cnts[4] = {compCnt, &C->cnt_act[ob], &C->cnt_pend[ob], &C->cnt_arr};
+      int32_t* const cnts[4] = {compCnt, &K->act[ob], &K->pend[ob], &K->arr};
       sweep_append<4>(
           g, nPend, cnts,
-          [&](int i, bool* pr) {
-            const int f = pendIn[i];
+          [&](int i) {
+            FlowVal x;
+            x.f = pendIn[i];
+            if (in_range(x.f, f0, cap)) x.a = P.rel[x.f];
+            return x;
+          },
+          [&](int i, const FlowVal& x, bool* pr) {
+            const int f = x.f;
             if (!in_range(f, f0, cap)) { err = 1; return; }
-            const double rl = P.rel[f];
+            const double rl = x.a;
             if (rl <= tn) {
               if (P.nbytes[f] == 0.0) {
                 pr[0] = true;
                 P.finish[f] = rl;
-                if (P.soff[f + 1] > P.soff[f]) g.store(&C->succ_flag[ib], 1);
+                if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
               } else {
                 pr[1] = pr[3] = true;
                 P.rem[f] = P.nbytes[f];
                 P.born[f] = e;
                 for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) lk.addNact(g, P.plink[k], 1);
-                g.store(&C->changed[ib], 1);
+                g.store(&K->changed[ib], 1);
               }
             } else {
               pr[2] = true;
             }
           },
-          [&](int k, int slot, int i) {
+          [&](int k, int slot, const FlowVal& x) {
             int32_t* out = k == 0 ? compOut : k == 1 ? actOut : k == 2 ? pendOut : arrs;
-            if (slot < cap) out[slot] = pendIn[i]; else err = 1;
+            if (slot < cap) out[slot] = x.f; else err = 1;
           });
     }
     if (err) g.store(&C->fault_info, 2);
@@ -1153,12 +1174,12 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     // dependants of finished flows, to a fixpoint through zero-byte flows.
     // A lane releases the successors of its own finished flow when it has a
     // few; long successor lists (a barrier's) are shared by the whole wave.
-    int nc = g.load(&C->succ_flag[ib]) ? g.load(&C->cnt_comp[(q - 1) % 3]) : 0;
+    int nc = g.load(&K->succ_flag[ib]) ? g.load(&K->comp[(q - 1) % 3]) : 0;
     while (nc > 0) {
-      const int32_t* cin = comp[(q - 1) % 3];
-      int32_t* cout = comp[q % 3];
-      int32_t* coutCnt = &C->cnt_comp[q % 3];
-      if (tid == 0) g.store(&C->cnt_comp[(q + 1) % 3], 0);
+      const int32_t* cin = comp((q - 1) % 3);
+      int32_t* cout = comp(q % 3);
+      int32_t* coutCnt = &K->comp[q % 3];
+      if (tid == 0) g.store(&K->comp[(q + 1) % 3], 0);
       for (int i0 = w0; i0 < nc; i0 += T) {
         const int i = i0 + lane_id();
         int k0 = 0, k1 = 0;
@@ -1196,18 +1217,18 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       if (err) g.store(&C->fault_info, 2);
       g.sync();
       q += 1;
-      nc = g.load(&C->cnt_comp[(q - 1) % 3]);
+      nc = g.load(&K->comp[(q - 1) % 3]);
     }
     clk.lap(1);
     if (g.aborted()) { status = ST_BARRIER; break; }
     if (g.load(&C->fault_info) != 0) { status = ST_OVERFLOW; break; }
-    const int nNew = g.load(&C->cnt_act[ob]);
-    const int pNew = g.load(&C->cnt_pend[ob]);
-    if (g.load(&C->changed[ib]) && nNew > 0) {
+    const int nNew = g.load(&K->act[ob]);
+    const int pNew = g.load(&K->pend[ob]);
+    if (g.load(&K->changed[ib]) && nNew > 0) {
       // theta of each component: below it every rate stays as it was.
       // Finished flows have fed it their rates; new flows feed the initial
       // share of their links.
-      const int nArr = g.load(&C->cnt_arr);
+      const int nArr = g.load(&K->arr);
       for (int i = tid; i < nArr; i += T) {
         const int f = arrs[i];
         if (!in_range(f, f0, cap)) continue;
@@ -1223,15 +1244,25 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       // ones) for re-solving
       g.sync();
       {
-        int32_t* const cnts[1] = {&C->cnt_sel};
+        int32_t* const cnts[1] = {&K->sel};
         sweep_append<1>(
             g, nNew, cnts,
-            [&](int i, bool* pr) {
-              const int f = actOut[i];
+            [&](int i) {
+              FlowVal x;
+              x.f = actOut[i];
+              if (in_range(x.f, f0, cap)) {
+                x.k = P.born[x.f];
+                x.a = P.rate[x.f];
+                x.b = __longlong_as_double((long long)g.load(&P.theta[P.comp[x.f]]));
+              }
+              return x;
+            },
+            [&](int i, const FlowVal& x, bool* pr) {
+              const int f = x.f;
               if (!in_range(f, f0, cap)) { err = 1; return; }
-              const bool fresh = P.born[f] == e;
-              const double r = P.rate[f];
-              const double th = __longlong_as_double((long long)g.load(&P.theta[P.comp[f]]));
+              const bool fresh = x.k == e;
+              const double r = x.a;
+              const double th = x.b;
               if (fresh || !(r < th * KEEP)) {
                 pr[0] = true;
                 const int64_t qv = fresh ? 0 : (int64_t)__builtin_rint(r * P.scale);
@@ -1242,15 +1273,15 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
                 }
               }
             },
-            [&](int, int slot, int i) {
-              if (slot < cap) arrs[slot] = actOut[i]; else err = 1;
+            [&](int, int slot, const FlowVal& x) {
+              if (slot < cap) arrs[slot] = x.f; else err = 1;
             });
       }
       if (err) g.store(&C->fault_info, 2);
       g.sync();
       clk.lap(7);
       for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
-      const int nSel = g.load(&C->cnt_sel);
+      const int nSel = g.load(&K->sel);
       if (threadIdx.x == 0) tl->sel += nSel;
       int rc = 0;
       if (nSel > 0) {
@@ -1264,12 +1295,12 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
         } else {
           if (C->lds_paths && nSel <= LDS_FLOWS) {
             if (g.block_id() == 0) {
-              BlockG b{g.lds, g.ldsi};
+              BlockG b{g.lds, g.ldsi, g.blk_lists};
               const int r1 = solve_mask(b, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc);
-              if (threadIdx.x == 0) g.store(&C->solve_rc, r1);
+              if (threadIdx.x == 0) g.store(&K->solve_rc, r1);
             }
             g.sync();
-            rc = g.load(&C->solve_rc);
+            rc = g.load(&K->solve_rc);
           } else if (C->lds_paths && nSel <= g.nblocks() * LDS_FLOWS) {
             rc = solve_lds(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, *S, true);
           } else {
@@ -1278,7 +1309,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
           }
         }
       }
-      if (P.debug && rc == 0) {
+      if ((P.debug & 1) && rc == 0) {
         // after a solve every active flow is frozen: no link has an unfrozen flow
         for (int l = C->l0 + tid; l < C->l1; l += T)
           if (lk.nfree(l) != 0) {
@@ -1321,7 +1352,7 @@ __device__ __forceinline__ void solve_only(G& g, const Params& P, const int sc, 
   int64_t& rounds = tl->rounds;
   int64_t& fsw = tl->fsw;
   int64_t isw = 0;
-  Clock clk(g.tid() == 0, tl->clk);
+  Clock clk(g.tid() == 0 && (P.debug & 2), tl->clk);
   int rc = 0;
   if (C->n_solve > 0) {
     if constexpr (IsGrid<G>::value) {
@@ -1352,15 +1383,20 @@ __device__ __forceinline__ void solve_only(G& g, const Params& P, const int sc, 
 
 // One workgroup per part.  A part whose links fit keeps its link state in
 // shared memory for the whole run; the rest of the pool caches the path
-// records of the flows being solved.
-__global__ __launch_bounds__(1024) void netsim_block_kernel(Params P) {
+// records of the flows being solved.  Built for workgroups of up to 512
+// threads (256 registers per lane) and of up to 1024 (128 per lane).
+template <int NT>
+__global__ __launch_bounds__(NT) void netsim_block_kernel(Params P) {
   __shared__ double lds[32];
   __shared__ int ldsi[128];
   __shared__ Tally tally;
+  __shared__ Lists lists;
   __shared__ __align__(16) unsigned char pool[POOL_BYTES];
-  BlockG g{lds, ldsi};
+  BlockG g{lds, ldsi, &lists};
   for (int sc = blockIdx.x; sc < P.num_scen; sc += gridDim.x) {
     const ScenCtl* C = &P.ctl[sc];
+    if (threadIdx.x == 0) lists = Lists{};
+    __syncthreads();
     const int nl = C->l1 - C->l0;
     const bool in_lds = P.mode == 0 && link_pool_bytes(nl) <= POOL_BYTES;
     const int used = in_lds ? (link_pool_bytes(nl) + 15) & ~15 : 0;
@@ -1386,7 +1422,8 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   __shared__ int flag;
   __shared__ SolveLds S;
   __shared__ Tally tally;
-  GridG g{lds, ldsi, &flag, P.bar, P.slots, 0u, 0u, false, 0u, 0u, 0u};
+  __shared__ Lists blk_lists;
+  GridG g{lds, ldsi, &blk_lists, &flag, P.bar, P.slots, 0u, 0u, false, 0u, 0u, 0u};
   g.init();
   LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
   const FlowCache none{nullptr, nullptr, 0};
@@ -1398,7 +1435,10 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
 }
 
 hipError_t launch_block(const Params& p, int blocks, int threads, hipStream_t s) {
-  hipLaunchKernelGGL(netsim_block_kernel, dim3(blocks), dim3(threads), 0, s, p);
+  if (threads <= 512)
+    hipLaunchKernelGGL(netsim_block_kernel<512>, dim3(blocks), dim3(threads), 0, s, p);
+  else
+    hipLaunchKernelGGL(netsim_block_kernel<1024>, dim3(blocks), dim3(threads), 0, s, p);
   return hipGetLastError();
 }
 

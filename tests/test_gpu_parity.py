@@ -185,9 +185,12 @@ def test_c4_full_size_prefix(exec_):
     fs = oflows.expand(program.scenarios[0])
     probe = osim.run_flowset(fs, max_events=150)
     assert np.isfinite(probe.finish).sum() >= 50
-    T = float(np.nanmax(probe.finish))
+    # the horizon sits 1e-9 relative after the last completion: far above the
+    # ~1e-12 GPU/oracle gap, far below the spacing of events there
+    T = float(np.nanmax(probe.finish)) * (1 + 1e-9)
     ref = osim.run_flowset(fs, until=T)
-    assert np.isfinite(ref.finish).sum() >= 50
+    done = ref.finish[np.isfinite(ref.finish)]
+    assert len(done) >= 50 and np.all(np.abs(done - T) > 1e-10 * T)
     ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
     fins, stats = pr.run_program(program, ns.make_options(exec=ex, until=T))
     assert stats["complete"] == 0 and stats["parts"] == 8
