@@ -44,15 +44,15 @@ def algorithmic_bytes(st: dict) -> float:
 
 
 # The oracle is far too slow for the whole workload (a solve over ~258k
-# flows takes it ~0.1 s), so it is timed on a bounded sample: events 65..128
+# flows takes it ~0.1 s), so it is timed on a bounded sample: events 65..192
 # of the workload on one clock (the first 64 events are the arrivals of the
 # 64 groups; from then on every group is active), by differencing runs to 64
-# and 128 events.
-STEADY = (64, 128)
+# and 192 events.
+STEADY = (64, 192)
 
 
 def cpu_baseline():
-    """The fp64 oracle (single thread, as it stands) on events 65..128 of C4."""
+    """The fp64 oracle (single thread, as it stands) on events 65..192 of C4."""
     from oracle import flows as oflows
     from oracle import sim as osim
     from workloads import configs
