@@ -34,7 +34,7 @@ HBM_PEAK_GBPS = 8000.0
 # visit (the byte model of the event-loop kernel).
 BYTES_PER_FLOW_ROUND = 28      # list entry 4 + path offsets 8 + min-share write 8 + read 8
 BYTES_PER_INCIDENCE_ROUND = 21  # link id 4+4 + residual capacity 8 + count 4 + flag 1
-BYTES_PER_ACTIVE_EVENT = 48    # rem, rate read twice (32) + rem write 8 + list in/out 8
+BYTES_PER_ACTIVE_EVENT = 20    # slot: predicted completion 8 + flow id 4 + rate 8
 BYTES_PER_PENDING_EVENT = 28   # list in 4 + release time 8, twice, + list out 4
 
 

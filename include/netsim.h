@@ -151,8 +151,9 @@ typedef struct {
   /* Device time by phase, summed over parts, as seen by the first thread of
    * the group running each part (only with debug bit 1; zero otherwise):
    * [0] next-event search, [1] settling completions and releases, [2] solve
-   * set-up, [3] share/blocking sweep, [4] wait after it, [5] freezing sweep,
-   * [6] wait after it, [7] choosing the flows to re-solve. */
+   * set-up and the share table of every round, [3] share/blocking sweep, [4]
+   * wait after it, [5] freezing sweep, [6] wait after it, [7] choosing the
+   * flows to re-solve. */
   double phase_seconds[8];
 } netsim_stats;
 

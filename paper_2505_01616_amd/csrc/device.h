@@ -12,7 +12,9 @@ namespace netsim_dev {
 // control block) when the whole grid runs the part, in shared memory when
 // one workgroup does.
 struct Lists {
-  int32_t act[2];          // active flows (input and output lists alternate)
+  int32_t slots;           // slots in use in the current slot buffer
+  int32_t holes;           // slots of finished flows among them
+  int32_t slots2;          // slots filled by a compaction
   int32_t pend[2];         // flows waiting for their release time
   int32_t comp[3];         // flows finished in the current wave of releases
   int32_t unf[2];          // unfrozen flows of a solve with global lists
@@ -22,6 +24,8 @@ struct Lists {
   int32_t sel;             // flows taken back for re-solving in the current event
   int32_t succ_flag[2];    // a flow finished in this event has dependants
   int32_t solve_rc;        // status of a solve run by one workgroup
+  int32_t fault;           // 1: bad fair share, 2: a work list overflowed or held a bad id
+  uint32_t stamp;          // last freezing-round number used by the part's solves
 };
 
 // Control block of one part in device memory.  A part is a set of flows of
@@ -43,10 +47,9 @@ struct ScenCtl {
   int64_t active_swept, pending_swept;
   int64_t reselected, wide_solves;
   int32_t status;          // 0 ran to the end, 1 stopped at a limit, < 0 fault
-  int32_t fault_info;
+  int32_t reserved;
   int64_t ticks[8];        // wall-clock ticks per phase (first thread of the group)
   int64_t dbg[4];          // debug checks (options.debug)
-  uint32_t stamp;          // last freezing-round number used by the part's solves
   Lists k;                 // list counters in global memory (grid layout)
 };
 
@@ -79,13 +82,13 @@ struct Params {
   const uint4* path16;     // [F] path as six 16-bit part-local link ids (0xFFFF =
                            //     none; valid in parts with lds_paths)
   // dynamic flow state
-  double* rem;             // [F] bytes left (active flows)
+  double* rem;             // [F] bytes left at time tref (active flows)
+  double* tref;            // [F] time at which rem was last brought up to date
   double* rate;            // [F] current rate
   double* finish;          // [F] completion time (NaN until finished)
   double* mf;              // [F] smallest fair share on the path (current round)
   double* rel;             // [F] release time (pending flows)
   int32_t* cnt;            // [F] predecessors not yet finished
-  int32_t* born;           // [F] event index at activation (-1 before)
   const int32_t* comp;     // [F] component of the flow (flows of different
                            //     components share no link)
   uint64_t* theta;         // [C] per component: lowest level that may change
@@ -94,8 +97,12 @@ struct Params {
   int64_t* lst;            // [2L] per link: residual capacity (fixed point), unfrozen flows
   int32_t* nact;           // [L] active flows
   uint32_t* fl;            // [L] number of the freezing round that blocked the link
-  // work lists, each [F], used per scenario on [f0, f1)
-  int32_t* act0; int32_t* act1;
+  // slots of the active flows (two buffers) and work lists, each [F], used per
+  // part on [f0, f1)
+  int32_t* act0; int32_t* act1;  // slot: flow id, -1 for a hole
+  double* tau0; double* tau1;    // slot: predicted completion time
+  double* srate0; double* srate1;  // slot: rate
+  int32_t* arrslot;        // slot of each entry of the re-solve list
   int32_t* pend0; int32_t* pend1;
   int32_t* comp0; int32_t* comp1; int32_t* comp2;
   int32_t* unf0; int32_t* unf1;

@@ -57,7 +57,9 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 struct BlockG {
   double* lds;
   int* ldsi;
-  Lists* lst;  // list counters in shared memory (zeroed when a part starts)
+  Lists* lst;  // list counters: shared memory (block kernel, zeroed when a part
+               // starts) or the part's control block (a solve run by one workgroup
+               // of the grid)
   __device__ Lists* lists(ScenCtl*) const { return lst; }
   __device__ int tid() const { return threadIdx.x; }
   __device__ int block_base() const { return 0; }
@@ -109,7 +111,6 @@ __device__ __forceinline__ unsigned xcc_id() {
 struct GridG {
   double* lds;
   int* ldsi;
-  Lists* blk_lists;  // shared-memory counters for a solve run by one workgroup
   __device__ Lists* lists(ScenCtl* C) const { return &C->k; }
   int* flag;      // shared: abort state as seen by this block's thread 0
   uint32_t* bar;
@@ -504,7 +505,8 @@ __host__ __device__ constexpr int link_pool_bytes(int nl) { return LINK_LDS_BYTE
 // restarts, so a stale stamp can never equal a live round number.
 template <class G, class LK>
 __device__ __forceinline__ uint32_t first_round(G& g, const Params& P, LK& lk, ScenCtl* C) {
-  uint32_t base = g.load(&C->stamp);
+  Lists* K = g.lists(C);
+  uint32_t base = g.load(&K->stamp);
   if (base > 0x7FFFFFFFu) {
     for (int l = C->l0 + g.tid(); l < C->l1; l += g.nthr()) lk.clear_flag(l);
     g.sync();
@@ -610,6 +612,7 @@ __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, 
     int32_t* out_cnt = &K->unf[r & 1];
     if (tid == 0 && r > 0) g.store(out_cnt, 0);
     round_table(g, lk, C);
+    clk.lap(2);
     // phase B: smallest share on each path; block links above it
     for (int i = tid; i < n; i += T) {
       const int f = in[i];
@@ -672,7 +675,7 @@ __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, 
         else bad = 2;
       }
     }
-    if (bad) g.store(&C->fault_info, bad);
+    if (bad) g.store(&K->fault, bad);
     clk.lap(5);
     g.sync();
     clk.lap(6);
@@ -682,14 +685,14 @@ __device__ __forceinline__ int solve(G& g, const Params& P, LK& lk, ScenCtl* C, 
     }
     if (g.aborted()) return ST_BARRIER;
     const int nout = g.load(out_cnt);
-    if (g.load(&C->fault_info) != 0) { rc = g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
+    if (g.load(&K->fault) != 0) { rc = g.load(&K->fault) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
     if (nout == 0) break;
     if (nout >= n) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
     if (++r > P.max_rounds) { rc = ST_ROUNDS; break; }
     in = out;
     n = nout;
   }
-  if (tid == 0) g.store(&C->stamp, st0 + (uint32_t)r);
+  if (tid == 0) g.store(&K->stamp, st0 + (uint32_t)r);
   return rc;
 }
 
@@ -740,6 +743,7 @@ template <class LK>
 __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, ScenCtl* C,
                                           const int32_t* list, int n, int64_t& rounds, int64_t& fsw,
                                           int64_t& isw, Clock& clk, bool warm, const FlowCache& fc) {
+  Lists* K = g.lists(C);
   const int T = blockDim.x;
   const int l0 = C->l0;
   const int f0 = C->f0, cap = C->f1 - C->f0;
@@ -766,6 +770,7 @@ __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, Sc
     const uint32_t st = st0 + (uint32_t)r;
     if (threadIdx.x == 0) cntr[(r + 1) % 3] = 0;
     round_table(g, lk, C);
+    clk.lap(2);
     // phase B: smallest share on each path; block links above it
     for_items(alive, cmask, fc, P, list, T, [&](int, int f, uint4 rec) {
       if (!in_range(f, f0, cap)) { bad = 2; return; }
@@ -816,7 +821,7 @@ __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, Sc
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
     if (lane_id() == 0 && c > 0) atomicAdd(&cntr[r % 3], c);
-    if (bad) g.store(&C->fault_info, bad);
+    if (bad) g.store(&K->fault, bad);
     clk.lap(5);
     __syncthreads();
     clk.lap(6);
@@ -824,14 +829,14 @@ __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, Sc
       rounds += 1;
       fsw += total;
     }
-    if (g.load(&C->fault_info) != 0) { rc = g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
+    if (g.load(&K->fault) != 0) { rc = g.load(&K->fault) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
     const int left = cntr[r % 3];
     if (left == 0) break;
     if (left >= total) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
     if (++r > P.max_rounds) { rc = ST_ROUNDS; break; }
     total = left;
   }
-  if (threadIdx.x == 0) g.store(&C->stamp, st0 + (uint32_t)r);
+  if (threadIdx.x == 0) g.store(&K->stamp, st0 + (uint32_t)r);
   return rc;
 }
 
@@ -887,6 +892,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     if (threadIdx.x == 0) S.cnt = 0;
     if (tid == 0) g.store(&K->rem3[(r + 1) % 3], 0);
     round_table(g, lk, C);
+    clk.lap(2);
     // phase B: smallest share on each path; block links above it
     for (int x = threadIdx.x; x < nu; x += blockDim.x) {
       const int j = uin[x];
@@ -935,7 +941,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
         if (keep) uout[b + (int)__popcll(mask & ((1ull << lane) - 1ull))] = (uint16_t)j;
       }
     }
-    if (bad) g.store(&C->fault_info, bad);
+    if (bad) g.store(&K->fault, bad);
     __syncthreads();
     const int nu_new = S.cnt;
     if (threadIdx.x == 0 && nu_new > 0) g.add(&K->rem3[r % 3], (int32_t)nu_new);
@@ -947,7 +953,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
       fsw += total;
     }
     if (g.aborted()) return ST_BARRIER;
-    if (g.load(&C->fault_info) != 0) { rc = g.load(&C->fault_info) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
+    if (g.load(&K->fault) != 0) { rc = g.load(&K->fault) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
     const int left = g.load(&K->rem3[r % 3]);
     if (left == 0) break;
     if (left >= total) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
@@ -955,38 +961,8 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     total = left;
     nu = nu_new;
   }
-  if (tid == 0) g.store(&C->stamp, st0 + (uint32_t)r);
+  if (tid == 0) g.store(&K->stamp, st0 + (uint32_t)r);
   return rc;
-}
-
-// Releases flow h whose last predecessor finished at t (called once per h).
-template <class G, class LK>
-__device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, ScenCtl* C, int h, double t,
-                                            int ob, int ib, int ev, int32_t* actOut,
-                                            int32_t* pendOut, int32_t* arrOut, int32_t* cout,
-                                            int32_t* coutCnt, int cap, int& err) {
-  Lists* K = g.lists(C);
-  const double rl = P.start[h] + t;
-  if (rl <= t) {
-    if (P.nbytes[h] == 0.0) {
-      P.finish[h] = rl;
-      const int s = g.add(coutCnt, 1);
-      if (s < cap) cout[s] = h; else err = 1;
-    } else {
-      P.rem[h] = P.nbytes[h];
-      P.born[h] = ev;
-      for (int j = P.poff[h]; j < P.poff[h + 1]; ++j) lk.addNact(g, P.plink[j], 1);
-      const int s = g.add(&K->act[ob], 1);
-      if (s < cap) actOut[s] = h; else err = 1;
-      const int a = g.add(&K->arr, 1);
-      if (a < cap) arrOut[a] = h; else err = 1;
-      g.store(&K->changed[ib], 1);
-    }
-  } else {
-    P.rel[h] = rl;
-    const int s = g.add(&K->pend[ob], 1);
-    if (s < cap) pendOut[s] = h; else err = 1;
-  }
 }
 
 // ------------------------------------------------------------- event loop
@@ -1001,9 +977,69 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, ScenC
 // whose rate is below theta keeps it; the others (and the new flows) have
 // their contributions taken back and are re-solved from that state.  Rates
 // are identical to a full re-solve in exact arithmetic, and kept flows keep
-// their bits.  Re-solves that fit in one workgroup's shared memory run on
-// workgroup 0 alone, with workgroup barriers.
+// their bits.  theta is kept per link component (flows of different
+// components share no link).
+//
+// Active flows live in slots: per part, the flow id, predicted completion
+// time tau and rate of every active flow, in two buffers used alternately
+// across compactions.  Remaining bytes are kept lazily: rem[f] is the value
+// at time tref[f], brought up to date (rem - rate * elapsed) only when the
+// flow's rate is re-solved, after which tau = t + rem / rate.  So an event
+// reads a kept flow's tau (next-event search) and rate (re-solve selection)
+// and writes nothing for it.  A finished flow leaves a hole (id -1, tau
+// +inf); when holes outnumber live slots, the live ones are compacted into
+// the other buffer.
 constexpr double KEEP = 1.0 - 1e-9;  // safety margin below theta
+
+struct Slots {
+  int32_t* id;
+  double* tau;
+  double* rate;
+};
+
+// Flow f becomes active at time t: remaining bytes, active counts on its
+// links, a new slot (tau set after its first solve) and the arrivals list.
+template <class G, class LK>
+__device__ __forceinline__ void activate(G& g, const Params& P, LK& lk, Lists* K, int f, double t,
+                                         const Slots& sl, int32_t* arrOut, int ib, int cap,
+                                         int& err) {
+  P.rem[f] = P.nbytes[f];
+  P.tref[f] = t;
+  for (int j = P.poff[f]; j < P.poff[f + 1]; ++j) lk.addNact(g, P.plink[j], 1);
+  const int s = g.add(&K->slots, 1);
+  if (s < cap) {
+    sl.id[s] = f;
+    sl.tau[s] = INF;
+    sl.rate[s] = 0.0;
+  } else {
+    err = 1;
+  }
+  const int a = g.add(&K->arr, 1);
+  if (a < cap) arrOut[a] = f; else err = 1;
+  g.store(&K->changed[ib], 1);
+}
+
+// Releases flow h whose last predecessor finished at t (called once per h).
+template <class G, class LK>
+__device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, Lists* K, int h, double t,
+                                            int ob, int ib, const Slots& sl, int32_t* pendOut,
+                                            int32_t* arrOut, int32_t* cout, int32_t* coutCnt, int cap,
+                                            int& err) {
+  const double rl = P.start[h] + t;
+  if (rl <= t) {
+    if (P.nbytes[h] == 0.0) {
+      P.finish[h] = rl;
+      const int s = g.add(coutCnt, 1);
+      if (s < cap) cout[s] = h; else err = 1;
+    } else {
+      activate(g, P, lk, K, h, t, sl, arrOut, ib, cap, err);
+    }
+  } else {
+    P.rel[h] = rl;
+    const int s = g.add(&K->pend[ob], 1);
+    if (s < cap) pendOut[s] = h; else err = 1;
+  }
+}
 
 template <class G, class LK>
 __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const int sc, SolveLds* S,
@@ -1012,17 +1048,19 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   Lists* K = g.lists(C);
   const int f0 = C->f0;
   const int cap = C->f1 - C->f0;
-  // alternating work lists, picked with selects (not runtime-indexed arrays,
+  // alternating arrays, picked with selects (not runtime-indexed arrays,
   // which would hide that they live in global memory)
-  auto act = [&](int k) { return k ? P.act1 + f0 : P.act0 + f0; };
+  auto slots = [&](int b) {
+    return b ? Slots{P.act1 + f0, P.tau1 + f0, P.srate1 + f0} : Slots{P.act0 + f0, P.tau0 + f0, P.srate0 + f0};
+  };
   auto pend = [&](int k) { return k ? P.pend1 + f0 : P.pend0 + f0; };
   auto comp = [&](int k) { return k == 0 ? P.comp0 + f0 : k == 1 ? P.comp1 + f0 : P.comp2 + f0; };
   int32_t* unf_a = P.unf0 + f0;
   int32_t* unf_b = P.unf1 + f0;
   int32_t* arrs = P.arr + f0;
+  int32_t* arrSlot = P.arrslot + f0;
   const int T = g.nthr();
   const int tid = g.tid();
-  const int b0 = g.block_base();
   const int w0 = tid - lane_id();
   Clock clk(tid == 0 && (P.debug & 2), tl->clk);
   if (threadIdx.x == 0) tl->solves = tl->rounds = tl->fsw = tl->asw = tl->psw = tl->sel = tl->wide = 0;
@@ -1034,48 +1072,46 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
   double t = 0.0;
   int64_t events = 0, isw = 0;
-  int nAct = 0;
+  int ab = 0;      // slot buffer in use
+  int nSlots = 0;  // slots in use (flows or holes)
   int nPend = C->n_pend0;
-  int e = 0;  // event index: lists act[e&1], pend[e&1] are this event's input
+  int e = 0;  // event index: pend[e&1] is this event's pending list
   int q = 0;  // completion-list phase index (three rotating lists)
   int status = ST_DONE;
   for (;;) {
     const int ib = e & 1, ob = ib ^ 1;
-    const int32_t* actIn = act(ib);
-    int32_t* actOut = act(ob);
+    const Slots sl = slots(ab);
     const int32_t* pendIn = pend(ib);
     int32_t* pendOut = pend(ob);
     if (tid == 0) {
-      g.store(&K->act[ob], 0);
       g.store(&K->pend[ob], 0);
       g.store(&K->changed[ib], 0);
       g.store(&K->succ_flag[ib], 0);
       g.store(&K->arr, 0);
       g.store(&K->sel, 0);
+      g.store(&K->slots2, 0);
     }
-    // next event time: earliest completion or release
-    double loc = INF;
-    for (int i = tid; i < nAct; i += T) {
-      const int f = actIn[i];
-      if (!in_range(f, f0, cap)) { g.store(&C->fault_info, 2); continue; }
-      const double dt = P.rem[f] / P.rate[f];
-      const double tau = t + dt;
-      loc = tau < loc ? tau : loc;
+    // next event time: earliest predicted completion or release
+    double mine = INF;
+    for (int s = tid; s < nSlots; s += T) {
+      const double v = sl.tau[s];
+      mine = v < mine ? v : mine;
     }
+    double loc = mine;
     for (int i = tid; i < nPend; i += T) {
       const int f = pendIn[i];
-      if (!in_range(f, f0, cap)) { g.store(&C->fault_info, 2); continue; }
+      if (!in_range(f, f0, cap)) { g.store(&K->fault, 2); continue; }
       const double rl = P.rel[f];
       loc = rl < loc ? rl : loc;
     }
     if (threadIdx.x == 0) {
-      tl->asw += nAct;
+      tl->asw += nSlots;
       tl->psw += nPend;
     }
     const double tn = g.min_all(loc);
     clk.lap(0);
     if (g.aborted()) { status = ST_BARRIER; break; }
-    if (g.load(&C->fault_info) != 0) { status = ST_OVERFLOW; break; }
+    if (g.load(&K->fault) != 0) { status = ST_OVERFLOW; break; }
     if (!(tn < INF)) break;
     if ((P.max_events > 0 && events >= P.max_events) || tn > P.until) {
       status = ST_STOPPED;
@@ -1083,58 +1119,39 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     }
     events += 1;
     const double thr = tn * THR;
-    const double step = tn - t;
+    const int slots0 = nSlots;  // slots at or above this one are activated in this event
     int32_t* compOut = comp(q % 3);
     int32_t* compCnt = &K->comp[q % 3];
     if (tid == 0) g.store(&K->comp[(q + 1) % 3], 0);
     int err = 0;
-    // completions and advance
-    {
-      int32_t* const cnts[2] = {compCnt, &K->act[ob]};
-      sweep_append<2>(
-          g, nAct, cnts,
-          [&](int i) {
-            FlowVal x;
-            x.f = actIn[i];
-            if (in_range(x.f, f0, cap)) {
-              x.a = P.rate[x.f];
-              x.b = P.rem[x.f];
-            }
-            return x;
-          },
-          [&](int i, const FlowVal& x, bool* pr) {
-            const int f = x.f;
-            if (!in_range(f, f0, cap)) { err = 1; return; }
-            const double r = x.a;
-            const double dt = x.b / r;
-            const double tau = t + dt;
-            if (tau <= thr) {
-              pr[0] = true;
-              P.finish[f] = tn;
-              g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
-              const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
-              for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
-                const int l = P.plink[k];
-                lk.addNact(g, l, -1);
-                lk.addR(g, l, qv);  // its share returns to the link
-              }
-              if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
-              g.store(&K->changed[ib], 1);
-            } else {
-              pr[1] = true;
-              const double moved = r * step;
-              P.rem[f] = x.b - moved;
-            }
-          },
-          [&](int k, int slot, const FlowVal& x) {
-            int32_t* out = k == 0 ? compOut : actOut;
-            if (slot < cap) out[slot] = x.f; else err = 1;
-          });
+    // completions: only threads holding a slot that is due look again
+    if (mine <= thr) {
+      for (int s = tid; s < nSlots; s += T) {
+        if (!(sl.tau[s] <= thr)) continue;
+        const int f = sl.id[s];
+        if (!in_range(f, f0, cap)) { err = 1; continue; }
+        const double r = sl.rate[s];
+        P.finish[f] = tn;
+        g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
+        const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
+        for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+          const int l = P.plink[k];
+          lk.addNact(g, l, -1);
+          lk.addR(g, l, qv);  // its share returns to the link
+        }
+        if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
+        g.store(&K->changed[ib], 1);
+        sl.id[s] = -1;
+        sl.tau[s] = INF;
+        g.add(&K->holes, 1);
+        const int c = g.add(compCnt, 1);
+        if (c < cap) compOut[c] = f; else err = 1;
+      }
     }
     // releases due now
     {
-      int32_t* const cnts[4] = {compCnt, &K->act[ob], &K->pend[ob], &K->arr};
-      sweep_append<4>(
+      int32_t* const cnts[2] = {compCnt, &K->pend[ob]};
+      sweep_append<2>(
           g, nPend, cnts,
           [&](int i) {
             FlowVal x;
@@ -1152,22 +1169,18 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
                 P.finish[f] = rl;
                 if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
               } else {
-                pr[1] = pr[3] = true;
-                P.rem[f] = P.nbytes[f];
-                P.born[f] = e;
-                for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) lk.addNact(g, P.plink[k], 1);
-                g.store(&K->changed[ib], 1);
+                activate(g, P, lk, K, f, tn, sl, arrs, ib, cap, err);
               }
             } else {
-              pr[2] = true;
+              pr[1] = true;
             }
           },
           [&](int k, int slot, const FlowVal& x) {
-            int32_t* out = k == 0 ? compOut : k == 1 ? actOut : k == 2 ? pendOut : arrs;
+            int32_t* out = k == 0 ? compOut : pendOut;
             if (slot < cap) out[slot] = x.f; else err = 1;
           });
     }
-    if (err) g.store(&C->fault_info, 2);
+    if (err) g.store(&K->fault, 2);
     g.sync();
     t = tn;
     q += 1;
@@ -1197,8 +1210,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
           for (int k = k0; k < k1; ++k) {
             const int h = P.succ[k];
             if (g.add(&P.cnt[h], -1) == 1)
-              release_one(g, P, lk, C, h, t, ob, ib, e, actOut, pendOut, arrs, cout, coutCnt, cap,
-                          err);
+              release_one(g, P, lk, K, h, t, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, err);
           }
         }
         uint64_t mask = __ballot(big);
@@ -1209,22 +1221,22 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
           for (int k = a + lane_id(); k < z; k += 64) {
             const int h = P.succ[k];
             if (g.add(&P.cnt[h], -1) == 1)
-              release_one(g, P, lk, C, h, t, ob, ib, e, actOut, pendOut, arrs, cout, coutCnt, cap,
-                          err);
+              release_one(g, P, lk, K, h, t, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, err);
           }
         }
       }
-      if (err) g.store(&C->fault_info, 2);
+      if (err) g.store(&K->fault, 2);
       g.sync();
       q += 1;
       nc = g.load(&K->comp[(q - 1) % 3]);
     }
     clk.lap(1);
     if (g.aborted()) { status = ST_BARRIER; break; }
-    if (g.load(&C->fault_info) != 0) { status = ST_OVERFLOW; break; }
-    const int nNew = g.load(&K->act[ob]);
+    if (g.load(&K->fault) != 0) { status = ST_OVERFLOW; break; }
+    nSlots = g.load(&K->slots);
     const int pNew = g.load(&K->pend[ob]);
-    if (g.load(&K->changed[ib]) && nNew > 0) {
+    const int live = nSlots - g.load(&K->holes);
+    if (g.load(&K->changed[ib]) && live > 0) {
       // theta of each component: below it every rate stays as it was.
       // Finished flows have fed it their rates; new flows feed the initial
       // share of their links.
@@ -1240,31 +1252,39 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
         }
         g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(lo));
       }
-      // take back the flows at or above their component's theta (and the new
-      // ones) for re-solving
       g.sync();
+      // take back the flows at or above their component's theta (and the new
+      // ones) for re-solving; their remaining bytes are brought up to date.
+      // With a single link component theta is one value for the whole part.
       {
+        const bool one_comp = C->nc == 1;
+        const double theta1 = __longlong_as_double((long long)g.load(&P.theta[C->c0]));
         int32_t* const cnts[1] = {&K->sel};
         sweep_append<1>(
-            g, nNew, cnts,
-            [&](int i) {
+            g, nSlots, cnts,
+            [&](int s) {
               FlowVal x;
-              x.f = actOut[i];
-              if (in_range(x.f, f0, cap)) {
-                x.k = P.born[x.f];
-                x.a = P.rate[x.f];
+              x.k = s;
+              x.f = sl.id[s];
+              x.a = sl.rate[s];
+              x.b = theta1;
+              if (!one_comp && in_range(x.f, f0, cap))
                 x.b = __longlong_as_double((long long)g.load(&P.theta[P.comp[x.f]]));
-              }
               return x;
             },
-            [&](int i, const FlowVal& x, bool* pr) {
+            [&](int s, const FlowVal& x, bool* pr) {
               const int f = x.f;
+              if (f < 0) return;  // a hole
               if (!in_range(f, f0, cap)) { err = 1; return; }
-              const bool fresh = x.k == e;
+              const bool fresh = s >= slots0;
               const double r = x.a;
-              const double th = x.b;
-              if (fresh || !(r < th * KEEP)) {
+              if (fresh || !(r < x.b * KEEP)) {
                 pr[0] = true;
+                if (!fresh) {
+                  const double moved = r * (t - P.tref[f]);
+                  P.rem[f] = P.rem[f] - moved;
+                  P.tref[f] = t;
+                }
                 const int64_t qv = fresh ? 0 : (int64_t)__builtin_rint(r * P.scale);
                 for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
                   const int l = P.plink[k];
@@ -1274,10 +1294,15 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
               }
             },
             [&](int, int slot, const FlowVal& x) {
-              if (slot < cap) arrs[slot] = x.f; else err = 1;
+              if (slot < cap) {
+                arrs[slot] = x.f;
+                arrSlot[slot] = x.k;
+              } else {
+                err = 1;
+              }
             });
       }
-      if (err) g.store(&C->fault_info, 2);
+      if (err) g.store(&K->fault, 2);
       g.sync();
       clk.lap(7);
       for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
@@ -1295,7 +1320,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
         } else {
           if (C->lds_paths && nSel <= LDS_FLOWS) {
             if (g.block_id() == 0) {
-              BlockG b{g.lds, g.ldsi, g.blk_lists};
+              BlockG b{g.lds, g.ldsi, &C->k};  // the grid's counters, in global memory
               const int r1 = solve_mask(b, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc);
               if (threadIdx.x == 0) g.store(&K->solve_rc, r1);
             }
@@ -1308,6 +1333,16 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
             rc = solve(g, P, lk, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
           }
         }
+        // the re-solved flows' slots: new rate and predicted completion
+        for (int j = tid; j < nSel; j += T) {
+          const int f = arrs[j];
+          const int s = arrSlot[j];
+          if (!in_range(f, f0, cap) || (unsigned)s >= (unsigned)cap) continue;
+          const double r = P.rate[f];
+          sl.rate[s] = r;
+          sl.tau[s] = t + P.rem[f] / r;
+        }
+        g.sync();
       }
       if ((P.debug & 1) && rc == 0) {
         // after a solve every active flow is frozen: no link has an unfrozen flow
@@ -1322,7 +1357,41 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       if (threadIdx.x == 0) tl->solves += 1;  // the active set changed: one rate solve (possibly empty)
       if (rc != 0) { status = rc; break; }
     }
-    nAct = nNew;
+    // compaction: when holes outnumber live slots, copy the live ones into
+    // the other buffer
+    const int holes = g.load(&K->holes);
+    if (2 * holes > nSlots) {
+      const Slots nx = slots(ab ^ 1);
+      int32_t* const cnts[1] = {&K->slots2};
+      sweep_append<1>(
+          g, nSlots, cnts,
+          [&](int s) {
+            FlowVal x;
+            x.f = sl.id[s];
+            x.a = sl.tau[s];
+            x.b = sl.rate[s];
+            return x;
+          },
+          [&](int, const FlowVal& x, bool* pr) { pr[0] = x.f >= 0; },
+          [&](int, int slot, const FlowVal& x) {
+            if (slot < cap) {
+              nx.id[slot] = x.f;
+              nx.tau[slot] = x.a;
+              nx.rate[slot] = x.b;
+            } else {
+              err = 1;
+            }
+          });
+      if (err) g.store(&K->fault, 2);
+      g.sync();
+      nSlots = g.load(&K->slots2);
+      ab ^= 1;
+      g.sync();  // every thread has read the counters before they are reset
+      if (tid == 0) {
+        g.store(&K->slots, nSlots);
+        g.store(&K->holes, 0);
+      }
+    }
     nPend = pNew;
     e += 1;
   }
@@ -1422,8 +1491,7 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   __shared__ int flag;
   __shared__ SolveLds S;
   __shared__ Tally tally;
-  __shared__ Lists blk_lists;
-  GridG g{lds, ldsi, &blk_lists, &flag, P.bar, P.slots, 0u, 0u, false, 0u, 0u, 0u};
+  GridG g{lds, ldsi, &flag, P.bar, P.slots, 0u, 0u, false, 0u, 0u, 0u};
   g.init();
   LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
   const FlowCache none{nullptr, nullptr, 0};

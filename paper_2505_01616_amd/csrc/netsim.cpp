@@ -455,7 +455,12 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.mf, sizeof(double) * Fz},
       {(void**)&P.rel, sizeof(double) * Fz},
       {(void**)&P.cnt, sizeof(int32_t) * Fz},
-      {(void**)&P.born, sizeof(int32_t) * Fz},
+      {(void**)&P.tref, sizeof(double) * Fz},
+      {(void**)&P.tau0, sizeof(double) * Fz},
+      {(void**)&P.tau1, sizeof(double) * Fz},
+      {(void**)&P.srate0, sizeof(double) * Fz},
+      {(void**)&P.srate1, sizeof(double) * Fz},
+      {(void**)&P.arrslot, sizeof(int32_t) * Fz},
       {(void**)&P.comp, sizeof(int32_t) * Fz},
       {(void**)&P.theta, sizeof(uint64_t) * (size_t)std::max<int32_t>(ncomp_total, 1)},
       {(void**)&P.arr, sizeof(int32_t) * Fz},
@@ -537,7 +542,6 @@ netsim_status reset_state(netsim_t* h, hipStream_t st) {
     if (he != hipSuccess) return hip_fail(h, he, "hipMemcpyAsync (reset)");
   }
   he = hipMemsetAsync(P.nact, 0, sizeof(int32_t) * Lz, st);
-  if (he == hipSuccess) he = hipMemsetAsync(P.born, 0xFF, sizeof(int32_t) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.rate, 0, sizeof(double) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 1024, st);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemsetAsync (reset)");

@@ -5,8 +5,10 @@ from the repository root:  python tests/golden/make_golden.py [c3] [c5]
 
 c5_makespans.json   per-scenario makespan of all 256 C5 scenarios (fp64 oracle)
 c3_summary.json     C3 (full size): makespan, a seeded sample of per-flow
-                    finish times, and the oracle's own spread under one-ulp
-                    changes of every capacity (C3 is ill-conditioned in fp64)
+                    finish times, and the oracle's own spread under changes
+                    of every capacity by k ulps, k in -5..-1 and 1..6 (C3 is
+                    ill-conditioned in fp64; eleven perturbations, run in
+                    parallel processes)
 """
 
 from __future__ import annotations
@@ -49,11 +51,22 @@ def _perturbed(fs, k):
                           fs.dep_off, fs.dep_ids)
 
 
+C3_ULPS = (-5, -4, -3, -2, -1, 1, 2, 3, 4, 5, 6)
+
+
+def _c3_run(k):
+    fs = oflows.expand(configs.c3(3).scenarios[0])
+    return osim.run_flowset(_perturbed(fs, k) if k else fs)
+
+
 def c3():
+    from multiprocessing import Pool
     t0 = time.time()
     fs = oflows.expand(configs.c3(3).scenarios[0])
-    ref = osim.run_flowset(fs)
-    runs = [osim.run_flowset(_perturbed(fs, k)).finish for k in (-1, 1, 2)]
+    with Pool(min(6, len(C3_ULPS) + 1)) as pool:
+        res = pool.map(_c3_run, (0,) + C3_ULPS)
+    ref = res[0]
+    runs = [r.finish for r in res[1:]]
     dev = np.max([np.abs(r - ref.finish) / ref.finish for r in runs], axis=0)
     order = np.argsort(ref.finish)
     bad = order[dev[order] > 1e-9]
@@ -64,6 +77,7 @@ def c3():
     early_sample = np.sort(rng.choice(early, size=min(2000, len(early)), replace=False))
     data = {
         "config": "c3 seed 3 (full size)", "writer": "tests/golden/make_golden.py",
+        "ulp_perturbations": list(C3_ULPS),
         "flows": int(fs.F), "events": ref.events, "solves": ref.solves,
         "makespan": ref.makespan,
         "ulp_spread_makespan": max(abs(float(np.max(r)) - ref.makespan) for r in runs) / ref.makespan,

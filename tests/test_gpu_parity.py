@@ -133,12 +133,12 @@ def _perturbed(fs, k):
 
 def _check_ill_conditioned(fs, gpu_finish):
     """For trajectories that fp64 does not determine to 1e-6 (the oracle
-    itself moves by more under a one-ulp change of the capacities):
-    per-flow 1e-6 up to the horizon where one-ulp oracle runs still agree
-    to 1e-9, and beyond it the GPU's deviation from the oracle must stay
-    within 4x the spread of the oracle's own one-ulp runs."""
+    itself moves by more when the capacities change by a few ulps):
+    per-flow 1e-6 up to the horizon where the perturbed oracle runs still
+    agree to 1e-9, and beyond it the GPU's deviation from the oracle must
+    stay within 4x the spread of the oracle's own perturbed runs."""
     ref = osim.run_flowset(fs)
-    runs = [osim.run_flowset(_perturbed(fs, k)).finish for k in (-1, 1, 2)]
+    runs = [osim.run_flowset(_perturbed(fs, k)).finish for k in (-3, -2, -1, 1, 2, 3)]
     dev = np.max([np.abs(r - ref.finish) / ref.finish for r in runs], axis=0)
     order = np.argsort(ref.finish)
     bad = order[dev[order] > 1e-9]
@@ -260,8 +260,9 @@ def test_c5_full_batched():
 
 def test_c3_full_size():
     """Full C3 (ill-conditioned in fp64): sampled flows finishing before the
-    oracle's one-ulp horizon agree to 1e-6; the makespan and the spread of a
-    seeded 4000-flow sample stay within 4x the oracle's own one-ulp spread."""
+    horizon of the oracle's perturbed runs agree to 1e-6; the makespan and
+    the spread of a seeded 4000-flow sample stay within 4x the oracle's own
+    spread over eleven runs with every capacity moved by -5..6 ulps."""
     ns, pr = _gpu()
     _say("test_c3_full_size")
     gold = _golden("c3_summary.json")
