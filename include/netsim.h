@@ -240,13 +240,59 @@ netsim_status netsim_set_limits(netsim_t* h, int64_t max_events, double until);
 
 /*
  * Simulates every scenario from t = 0 on the device, in one kernel launch
- * (the event loop and the rate solves stay on the GPU).  hip_stream may be
- * NULL (the default stream) or a hipStream_t, e.g. torch.cuda's current
- * stream.  Blocks until the run is done.  May be called again: every call
- * starts over from t = 0 with the same flows.  No flows can be added after
- * the first run (NETSIM_E_STATE).
+ * (the event loop and the rate solves stay on the GPU), up to the limits of
+ * netsim_options / netsim_set_limits.  hip_stream may be NULL (the default
+ * stream) or a hipStream_t, e.g. torch.cuda's current stream.  Blocks until
+ * the run is done.  May be called again: every call starts over from t = 0
+ * with the same flows and drops the checkpoints of netsim_advance.  No flows
+ * can be added after the first run (NETSIM_E_STATE).
  */
 netsim_status netsim_run(netsim_t* h, void* hip_stream);
+
+/*
+ * Time rollback (Section 4.2, the network simulator with time rollback: an
+ * API that updates an existing flow's start time, an API that advances the
+ * simulation by steps or up to a given time, and garbage collection of the
+ * history that no later update can reach).
+ *
+ * netsim_advance continues every part from where the last netsim_run or
+ * netsim_advance stopped (from t = 0 if the handle has not run, or after
+ * netsim_run was called), processing events with time <= until and at most
+ * max_events more events per part (0 = no limit; a part stops before the
+ * event that would exceed either limit).  Afterwards netsim_get_finish /
+ * netsim_get_stats describe the position reached (statistics accumulate
+ * from t = 0) and the state is kept as a checkpoint in device memory
+ * (best effort: without memory for it, rollbacks go further back).
+ * Advancing in several calls gives bit for bit the finish times of one
+ * call with the same final limit.  Blocks until done; NETSIM_E_INVALID for a
+ * NaN limit or max_events < 0.
+ */
+netsim_status netsim_advance(netsim_t* h, double until, int64_t max_events, void* hip_stream);
+
+/*
+ * Sets flow id's start (its absolute start when it has no dependencies, else
+ * its lag after the last of them) to `start` (finite, >= 0).  If the
+ * simulation of the flow's part has already processed its old or its new
+ * release time, the part is rolled back to the latest checkpoint in which
+ * the flow was not yet released and whose last event precedes the new
+ * release (t = 0 if there is none), and the checkpoints after it no longer
+ * apply to that part; other parts keep their position.  The next
+ * netsim_advance (or netsim_run, from t = 0) re-simulates with the new
+ * start, so completion times that depended on the flow change accordingly
+ * (through the dependency graph).  Valid before the first run as well.
+ */
+netsim_status netsim_update_start(netsim_t* h, int64_t id, double start);
+
+/*
+ * Garbage collection: the caller promises that no later netsim_update_start
+ * moves a release before t_min.  Checkpoints that no rollback to t_min or
+ * later can need are freed (results are unaffected: a rollback never needs
+ * more than the latest checkpoint before its target).
+ */
+netsim_status netsim_gc(netsim_t* h, double t_min);
+
+/* Number of checkpoints held in device memory. */
+netsim_status netsim_num_checkpoints(const netsim_t* h, int64_t* n);
 
 /*
  * finish[num_flows] (host) receives each flow's completion time (NaN for a

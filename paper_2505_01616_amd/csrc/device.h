@@ -41,6 +41,11 @@ struct ScenCtl {
   int32_t n_solve;         // solve-once: active flows listed in act0 + f0
   int32_t scen;            // the scenario the part belongs to
   int32_t lds_paths;       // every path has <= 6 links and the part < 65535 links
+  // event-loop position, saved when a launch stops and read when the next
+  // one continues (Params::resume)
+  int32_t started;         // 1 once a launch has run the part
+  int32_t e, q, ab;        // event index, completion-list phase, slot buffer
+  int32_t nslots, holes, npend;  // slots in use, holes among them, pending flows
   // results
   double t;                // simulated time reached
   int64_t events, solves, rounds, flows_swept, incidences_swept;
@@ -65,6 +70,7 @@ enum : int32_t {
 struct Params {
   int32_t num_scen;
   int32_t mode;            // 0 event loop, 1 one rate solve per scenario
+  int32_t resume;          // 1: continue every started part from its saved position
   int64_t max_events;      // 0 = no limit
   double until;
   int32_t max_rounds;
@@ -87,7 +93,8 @@ struct Params {
   double* rate;            // [F] current rate
   double* finish;          // [F] completion time (NaN until finished)
   double* mf;              // [F] smallest fair share on the path (current round)
-  double* rel;             // [F] release time (pending flows)
+  double* rel;             // [F] release time (set when a flow is released or pending)
+  double* base;            // [F] release base: finish time of the last predecessor
   int32_t* cnt;            // [F] predecessors not yet finished
   const int32_t* comp;     // [F] component of the flow (flows of different
                            //     components share no link)

@@ -424,9 +424,10 @@ struct LinksGlobal {
   __device__ __forceinline__ int64_t nfree(int l) const { return lst[2 * l + 1]; }
   __device__ __forceinline__ int nactv(int l) const { return nact[l]; }
   __device__ __forceinline__ void clear_flag(int l) { fl[l] = 0; }
-  // link at rest: full capacity, no flow (active counts are cleared by the host)
+  // link at rest: full capacity, no flow
   __device__ __forceinline__ void reset(int l, int64_t R) {
     set(l, R, 0);
+    nact[l] = 0;
     fl[l] = 0;
   }
   __device__ __forceinline__ void block(int l, uint32_t st) { fl[l] = st; }
@@ -1026,6 +1027,8 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, Lists
                                             int32_t* arrOut, int32_t* cout, int32_t* coutCnt, int cap,
                                             int& err) {
   const double rl = P.start[h] + t;
+  P.base[h] = t;
+  P.rel[h] = rl;
   if (rl <= t) {
     if (P.nbytes[h] == 0.0) {
       P.finish[h] = rl;
@@ -1035,7 +1038,6 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, Lists
       activate(g, P, lk, K, h, t, sl, arrOut, ib, cap, err);
     }
   } else {
-    P.rel[h] = rl;
     const int s = g.add(&K->pend[ob], 1);
     if (s < cap) pendOut[s] = h; else err = 1;
   }
@@ -1063,21 +1065,52 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   const int tid = g.tid();
   const int w0 = tid - lane_id();
   Clock clk(tid == 0 && (P.debug & 2), tl->clk);
-  if (threadIdx.x == 0) tl->solves = tl->rounds = tl->fsw = tl->asw = tl->psw = tl->sel = tl->wide = 0;
+  const bool resume = P.resume && C->started;
+  if (threadIdx.x == 0) {
+    // statistics accumulate over the launches that continue a part
+    tl->solves = resume ? C->solves : 0;
+    tl->rounds = resume ? C->rounds : 0;
+    tl->fsw = resume ? C->flows_swept : 0;
+    tl->asw = resume ? C->active_swept : 0;
+    tl->psw = resume ? C->pending_swept : 0;
+    tl->sel = resume ? C->reselected : 0;
+    tl->wide = resume ? C->wide_solves : 0;
+  }
   int64_t& rounds = tl->rounds;
   int64_t& fsw = tl->fsw;
   // links at rest: nothing active; no component has changed yet
   for (int l = C->l0 + tid; l < C->l1; l += T) lk.reset(l, P.R0[l]);
   const uint64_t INF_BITS = (uint64_t)__double_as_longlong(INF);
   for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
-  double t = 0.0;
-  int64_t events = 0, isw = 0;
-  int ab = 0;      // slot buffer in use
-  int nSlots = 0;  // slots in use (flows or holes)
-  int nPend = C->n_pend0;
-  int e = 0;  // event index: pend[e&1] is this event's pending list
-  int q = 0;  // completion-list phase index (three rotating lists)
+  double t = resume ? C->t : 0.0;
+  int64_t events = resume ? C->events : 0, isw = 0;
+  const int64_t events0 = events;
+  int ab = resume ? C->ab : 0;          // slot buffer in use
+  int nSlots = resume ? C->nslots : 0;  // slots in use (flows or holes)
+  int nPend = resume ? C->npend : C->n_pend0;
+  int e = resume ? C->e : 0;  // event index: pend[e&1] is this event's pending list
+  int q = resume ? C->q : 0;  // completion-list phase index (three rotating lists)
   int status = ST_DONE;
+  if (resume) {
+    // link state of the active flows, rebuilt exactly (integer sums): every
+    // active flow holds rint(rate * scale) of each of its links; all are frozen
+    g.sync();
+    const Slots s0 = slots(ab);
+    for (int s = tid; s < nSlots; s += T) {
+      const int f = s0.id[s];
+      if (!in_range(f, f0, cap)) continue;
+      const int64_t qv = (int64_t)__builtin_rint(s0.rate[s] * P.scale);
+      for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+        lk.addNact(g, P.plink[k], 1);
+        lk.addR(g, P.plink[k], -qv);
+      }
+    }
+    if (tid == 0) {
+      g.store(&K->slots, nSlots);
+      g.store(&K->holes, C->holes);
+    }
+  }
+  g.sync();
   for (;;) {
     const int ib = e & 1, ob = ib ^ 1;
     const Slots sl = slots(ab);
@@ -1113,7 +1146,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     if (g.aborted()) { status = ST_BARRIER; break; }
     if (g.load(&K->fault) != 0) { status = ST_OVERFLOW; break; }
     if (!(tn < INF)) break;
-    if ((P.max_events > 0 && events >= P.max_events) || tn > P.until) {
+    if ((P.max_events > 0 && events - events0 >= P.max_events) || tn > P.until) {
       status = ST_STOPPED;
       break;
     }
@@ -1395,8 +1428,18 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     nPend = pNew;
     e += 1;
   }
+  if (tid == 0 && !resume) C->incidences_swept = 0;
+  g.sync();
   g.add(&C->incidences_swept, isw);
   if (tid == 0) {
+    // position for a later launch that continues the part
+    C->started = 1;
+    C->e = e;
+    C->q = q;
+    C->ab = ab;
+    C->nslots = nSlots;
+    C->holes = g.load(&K->holes);
+    C->npend = nPend;
     C->t = t;
     C->events = events;
     C->solves = tl->solves;

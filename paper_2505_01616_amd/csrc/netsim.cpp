@@ -61,6 +61,16 @@ struct netsim {
   std::vector<ScenCtl> h_ctl0;
   double scale = 1.0;
   void* d_block = nullptr;            // one allocation holding every device array
+  char* persist = nullptr;            // the persistent dynamic state inside it
+  size_t persist_bytes = 0;
+  bool has_state = false;             // the device holds a simulation position
+  struct Checkpoint {
+    void* dev = nullptr;              // copy of the persistent state
+    std::vector<double> t;            // per part: time of its last processed event
+    std::vector<char> valid;          // per part: still on the current history
+  };
+  std::vector<Checkpoint> checkpoints;
+  std::vector<double> part_t;         // per part: time of its last processed event (-inf: none)
   Params prm{};
   // results
   std::vector<double> finish;         // id order
@@ -449,17 +459,25 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.soff, sizeof(int32_t) * (Fz + 1)},
       {(void**)&P.succ, sizeof(int32_t) * succ.size()},
       {(void**)&P.R0, sizeof(int64_t) * Lz},
+      // persistent dynamic state (contiguous: one copy makes a checkpoint)
       {(void**)&P.rem, sizeof(double) * Fz},
+      {(void**)&P.tref, sizeof(double) * Fz},
       {(void**)&P.rate, sizeof(double) * Fz},
       {(void**)&P.finish, sizeof(double) * Fz},
-      {(void**)&P.mf, sizeof(double) * Fz},
       {(void**)&P.rel, sizeof(double) * Fz},
+      {(void**)&P.base, sizeof(double) * Fz},
       {(void**)&P.cnt, sizeof(int32_t) * Fz},
-      {(void**)&P.tref, sizeof(double) * Fz},
+      {(void**)&P.act0, sizeof(int32_t) * Fz},
+      {(void**)&P.act1, sizeof(int32_t) * Fz},
       {(void**)&P.tau0, sizeof(double) * Fz},
       {(void**)&P.tau1, sizeof(double) * Fz},
       {(void**)&P.srate0, sizeof(double) * Fz},
       {(void**)&P.srate1, sizeof(double) * Fz},
+      {(void**)&P.pend0, sizeof(int32_t) * Fz},
+      {(void**)&P.pend1, sizeof(int32_t) * Fz},
+      {(void**)&P.ctl, sizeof(ScenCtl) * (size_t)std::max<int32_t>(NP, 1)},
+      // scratch
+      {(void**)&P.mf, sizeof(double) * Fz},
       {(void**)&P.arrslot, sizeof(int32_t) * Fz},
       {(void**)&P.comp, sizeof(int32_t) * Fz},
       {(void**)&P.theta, sizeof(uint64_t) * (size_t)std::max<int32_t>(ncomp_total, 1)},
@@ -468,16 +486,11 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.nact, sizeof(int32_t) * Lz},
       {(void**)&P.fl, sizeof(uint32_t) * Lz},
       {(void**)&P.path16, 16 * Fz},
-      {(void**)&P.act0, sizeof(int32_t) * Fz},
-      {(void**)&P.act1, sizeof(int32_t) * Fz},
-      {(void**)&P.pend0, sizeof(int32_t) * Fz},
-      {(void**)&P.pend1, sizeof(int32_t) * Fz},
       {(void**)&P.comp0, sizeof(int32_t) * Fz},
       {(void**)&P.comp1, sizeof(int32_t) * Fz},
       {(void**)&P.comp2, sizeof(int32_t) * Fz},
       {(void**)&P.unf0, sizeof(int32_t) * Fz},
       {(void**)&P.unf1, sizeof(int32_t) * Fz},
-      {(void**)&P.ctl, sizeof(ScenCtl) * (size_t)std::max<int32_t>(NP, 1)},
       {(void**)&P.bar, sizeof(uint32_t) * 1024},
       {(void**)&P.slots, sizeof(uint64_t) * 8},
   };
@@ -495,6 +508,8 @@ netsim_status prepare(netsim_t* h) {
     *p.dst = base;
     base += (p.bytes + 255) & ~size_t(255);
   }
+  h->persist = (char*)P.rem;
+  h->persist_bytes = (size_t)((char*)P.ctl - (char*)P.rem) + sizeof(ScenCtl) * (size_t)std::max<int32_t>(NP, 1);
   struct Up { const void* src; const void* dst; size_t bytes; };
   const Up ups[] = {
       {poff.data(), P.poff, sizeof(int32_t) * (size_t)(F + 1)},
@@ -542,6 +557,7 @@ netsim_status reset_state(netsim_t* h, hipStream_t st) {
     if (he != hipSuccess) return hip_fail(h, he, "hipMemcpyAsync (reset)");
   }
   he = hipMemsetAsync(P.nact, 0, sizeof(int32_t) * Lz, st);
+  if (he == hipSuccess) he = hipMemsetAsync(P.base, 0, sizeof(double) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.rate, 0, sizeof(double) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 1024, st);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemsetAsync (reset)");
@@ -550,19 +566,33 @@ netsim_status reset_state(netsim_t* h, hipStream_t st) {
   return NETSIM_OK;
 }
 
-netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms) {
+// One kernel launch: a rate solve per part (solve_only), or the event loop of
+// every part from t = 0 or, with resume, from where the last launch stopped,
+// processing events up to `until` and at most max_events more per part.
+netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bool resume = false,
+                     int64_t max_events = -1, double until = std::numeric_limits<double>::quiet_NaN()) {
   Params P = h->prm;
   P.mode = solve_only ? 1 : 0;
-  P.max_events = solve_only ? 0 : h->opt.max_events;
-  P.until = std::isnan(h->opt.until) ? std::numeric_limits<double>::infinity() : h->opt.until;
+  P.resume = resume ? 1 : 0;
+  if (max_events < 0) max_events = h->opt.max_events;
+  if (std::isnan(until)) until = h->opt.until;
+  P.max_events = solve_only ? 0 : max_events;
+  P.until = std::isnan(until) ? std::numeric_limits<double>::infinity() : until;
   P.debug = h->opt.debug;
   P.max_rounds = h->opt.max_rounds > 0 ? h->opt.max_rounds
                                        : (int32_t)std::min<int64_t>(h->F + 1, std::numeric_limits<int32_t>::max());
   const int32_t S = h->num_parts;
   int exec = h->opt.exec;
   if (exec == NETSIM_EXEC_AUTO) exec = (S > 1 || h->F < 100000) ? NETSIM_EXEC_BLOCK : NETSIM_EXEC_GRID;
+  // grid-barrier words and min-reduction slots start fresh in every launch
+  // (a launch that continues a run must not see the last launch's counts)
+  uint64_t inf_slots[8];
+  for (auto& x : inf_slots) x = 0x7FF0000000000000ull;
+  hipError_t he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 1024, st);
+  if (he == hipSuccess) he = hipMemcpyAsync(P.slots, inf_slots, sizeof(inf_slots), hipMemcpyHostToDevice, st);
+  if (he != hipSuccess) return hip_fail(h, he, "reset of the grid synchronisation words");
   hipEvent_t e0, e1;
-  hipError_t he = hipEventCreate(&e0);
+  he = hipEventCreate(&e0);
   if (he == hipSuccess) he = hipEventCreate(&e1);
   if (he != hipSuccess) return hip_fail(h, he, "hipEventCreate");
   he = hipEventRecord(e0, st);
@@ -617,6 +647,168 @@ netsim_status collect(netsim_t* h, std::vector<ScenCtl>* ctl_out) {
     }
   }
   return NETSIM_OK;
+}
+
+
+void drop_checkpoints(netsim_t* h) {
+  for (auto& c : h->checkpoints)
+    if (c.dev) (void)hipFree(c.dev);
+  h->checkpoints.clear();
+}
+
+// A fresh run from t = 0 (resume = false) or a continuation of the current
+// position (resume = true; from t = 0 if there is none), then the results.
+netsim_status simulate(netsim_t* h, hipStream_t st, bool resume, int64_t max_events, double until) {
+  const auto t0 = std::chrono::steady_clock::now();
+  netsim_status rc;
+  if (!h->prepared) {
+    rc = prepare(h);
+    if (rc) return rc;
+  }
+  hipError_t he = hipSetDevice(h->opt.device);
+  if (he != hipSuccess) return hip_fail(h, he, "hipSetDevice");
+  if (!resume || !h->has_state) {
+    drop_checkpoints(h);
+    rc = reset_state(h, st);
+    if (rc) return rc;
+  }
+  const auto t1 = std::chrono::steady_clock::now();
+  float ms = 0.0f;
+  if (h->F > 0) {
+    rc = launch(h, st, false, &ms, resume, max_events, until);
+    if (rc) return rc;
+  }
+  h->has_state = true;
+  std::vector<ScenCtl> ctl;
+  rc = h->F > 0 ? collect(h, &ctl) : NETSIM_OK;
+  if (h->F == 0) ctl = h->h_ctl0;
+  // results, even on a device fault (partial), for inspection
+  const int64_t F = h->F;
+  std::vector<double> fin_dev((size_t)std::max<int64_t>(F, 1));
+  if (F > 0) {
+    he = hipMemcpy(fin_dev.data(), h->prm.finish, sizeof(double) * (size_t)F, hipMemcpyDeviceToHost);
+    if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (finish)");
+  }
+  h->finish.assign((size_t)F, 0.0);
+  for (int64_t id = 0; id < F; ++id) h->finish[(size_t)id] = fin_dev[(size_t)h->dev_of_flow[(size_t)id]];
+  h->makespan.assign(h->scen.size(), 0.0);
+  netsim_stats s{};
+  s.complete = 1;
+  s.parts = h->num_parts;
+  const int32_t NP = h->num_parts;
+  h->part_t.assign((size_t)NP, -std::numeric_limits<double>::infinity());
+  for (int32_t k = 0; k < NP; ++k)
+    if (ctl[(size_t)k].started) h->part_t[(size_t)k] = ctl[(size_t)k].t;
+  for (int32_t k = 0; k < NP; ++k) {
+    const ScenCtl& c = ctl[(size_t)k];
+    double& m = h->makespan[(size_t)c.scen];
+    for (int32_t d = c.f0; d < c.f1; ++d)
+      if (!std::isnan(fin_dev[(size_t)d])) {
+        m = std::max(m, fin_dev[(size_t)d]);
+        s.completed_flows += 1;
+      }
+    s.events += c.events;
+    s.solves += c.solves;
+    s.rounds += c.rounds;
+    s.flows_swept += c.flows_swept;
+    s.incidences_swept += c.incidences_swept;
+    s.active_swept += c.active_swept;
+    s.pending_swept += c.pending_swept;
+    s.reselected += c.reselected;
+    s.wide_solves += c.wide_solves;
+    s.sim_time = std::max(s.sim_time, c.t);
+    if (c.status != 0) s.complete = 0;
+  }
+  int khz = 0;
+  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->opt.device) != hipSuccess || khz <= 0)
+    khz = 100000;
+  for (int32_t k = 0; k < NP; ++k)
+    for (int j = 0; j < 8; ++j) s.phase_seconds[j] += (double)ctl[(size_t)k].ticks[j] / (1e3 * khz);
+  s.device_seconds = ms * 1e-3;
+  s.upload_seconds = std::chrono::duration<double>(t1 - t0).count();
+  h->stats = s;
+  h->has_result = true;
+  return rc;
+}
+
+
+// Part of device flow d (parts hold consecutive device flows).
+int32_t part_of_dev(const netsim_t* h, int32_t d) {
+  int32_t lo = 0, hi = h->num_parts - 1;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi) / 2;
+    if (h->h_ctl0[(size_t)mid].f1 <= d) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+// Keeps a copy of the persistent state (best effort: without device memory
+// for it, later rollbacks go back to an older checkpoint or to t = 0).
+netsim_status push_checkpoint(netsim_t* h, hipStream_t st) {
+  netsim_t::Checkpoint c;
+  if (hipMalloc(&c.dev, h->persist_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    return NETSIM_OK;
+  }
+  hipError_t he = hipMemcpyAsync(c.dev, h->persist, h->persist_bytes, hipMemcpyDeviceToDevice, st);
+  if (he == hipSuccess) he = hipStreamSynchronize(st);
+  if (he != hipSuccess) {
+    (void)hipFree(c.dev);
+    return hip_fail(h, he, "checkpoint copy");
+  }
+  c.t = h->part_t;
+  c.valid.assign((size_t)h->num_parts, 1);
+  h->checkpoints.push_back(std::move(c));
+  return NETSIM_OK;
+}
+
+// Restores part p to checkpoint k (k < 0: its state at t = 0) and marks the
+// later checkpoints as off its history.
+netsim_status restore_part(netsim_t* h, int32_t p, int k) {
+  const Params& P = h->prm;
+  const ScenCtl& c0 = h->h_ctl0[(size_t)p];
+  const size_t f0 = (size_t)c0.f0, n = (size_t)(c0.f1 - c0.f0);
+  hipError_t he = hipSuccess;
+  if (k >= 0) {
+    const char* src = (const char*)h->checkpoints[(size_t)k].dev;
+    struct A { void* a; size_t z; };
+    const A arrays[] = {{P.rem, 8}, {P.tref, 8}, {P.rate, 8}, {P.finish, 8}, {P.rel, 8}, {P.base, 8},
+                        {P.cnt, 4}, {P.act0, 4}, {P.act1, 4}, {P.tau0, 8}, {P.tau1, 8},
+                        {P.srate0, 8}, {P.srate1, 8}, {P.pend0, 4}, {P.pend1, 4}};
+    for (const A& a : arrays) {
+      const size_t off = (size_t)((char*)a.a - h->persist) + f0 * a.z;
+      if (he == hipSuccess && n > 0) he = hipMemcpy((char*)a.a + f0 * a.z, src + off, n * a.z, hipMemcpyDeviceToDevice);
+    }
+    const size_t coff = (size_t)((char*)P.ctl - h->persist) + sizeof(ScenCtl) * (size_t)p;
+    if (he == hipSuccess) he = hipMemcpy(P.ctl + p, src + coff, sizeof(ScenCtl), hipMemcpyDeviceToDevice);
+  } else {
+    std::vector<double> nan(n, std::numeric_limits<double>::quiet_NaN()), zero(n, 0.0);
+    if (n > 0) {
+      he = hipMemcpy(P.cnt + f0, h->h_cnt0.data() + f0, 4 * n, hipMemcpyHostToDevice);
+      if (he == hipSuccess) he = hipMemcpy(P.rel + f0, h->h_rel0.data() + f0, 8 * n, hipMemcpyHostToDevice);
+      if (he == hipSuccess) he = hipMemcpy(P.pend0 + f0, h->h_pend0.data() + f0, 4 * n, hipMemcpyHostToDevice);
+      if (he == hipSuccess) he = hipMemcpy(P.finish + f0, nan.data(), 8 * n, hipMemcpyHostToDevice);
+      if (he == hipSuccess) he = hipMemcpy(P.base + f0, zero.data(), 8 * n, hipMemcpyHostToDevice);
+      if (he == hipSuccess) he = hipMemcpy(P.rate + f0, zero.data(), 8 * n, hipMemcpyHostToDevice);
+    }
+    if (he == hipSuccess) he = hipMemcpy(P.ctl + p, &c0, sizeof(ScenCtl), hipMemcpyHostToDevice);
+  }
+  if (he != hipSuccess) return hip_fail(h, he, "rollback copy");
+  for (size_t j = (size_t)std::max(k + 1, 0); j < h->checkpoints.size(); ++j)
+    h->checkpoints[j].valid[(size_t)p] = 0;
+  h->part_t[(size_t)p] = k >= 0 ? h->checkpoints[(size_t)k].t[(size_t)p]
+                                : -std::numeric_limits<double>::infinity();
+  return NETSIM_OK;
+}
+
+// Latest checkpoint on part p's history whose last event precedes `before`
+// (-1: none, i.e. t = 0).
+int latest_checkpoint(const netsim_t* h, int32_t p, double before) {
+  for (int k = (int)h->checkpoints.size() - 1; k >= 0; --k) {
+    const auto& c = h->checkpoints[(size_t)k];
+    if (c.valid[(size_t)p] && c.t[(size_t)p] < before) return k;
+  }
+  return -1;
 }
 
 }  // namespace
@@ -808,70 +1000,91 @@ netsim_status netsim_set_limits(netsim_t* h, int64_t max_events, double until) {
 
 netsim_status netsim_run(netsim_t* h, void* hip_stream) {
   if (!h) return fail(nullptr, NETSIM_E_INVALID, "run: handle is NULL");
+  return simulate(h, (hipStream_t)hip_stream, false, -1, std::numeric_limits<double>::quiet_NaN());
+}
+
+netsim_status netsim_advance(netsim_t* h, double until, int64_t max_events, void* hip_stream) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "advance: handle is NULL");
+  if (std::isnan(until) || max_events < 0) return fail(h, NETSIM_E_INVALID, "advance: bad limit");
   hipStream_t st = (hipStream_t)hip_stream;
-  const auto t0 = std::chrono::steady_clock::now();
-  netsim_status rc;
-  if (!h->prepared) {
-    rc = prepare(h);
-    if (rc) return rc;
-  }
+  netsim_status rc = simulate(h, st, true, max_events, until);
+  if (rc) return rc;
+  return h->F > 0 ? push_checkpoint(h, st) : NETSIM_OK;
+}
+
+netsim_status netsim_update_start(netsim_t* h, int64_t id, double start) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "update_start: handle is NULL");
+  const int64_t F = (int64_t)h->f_bytes.size();
+  if (id < 0 || id >= F) return fail(h, NETSIM_E_INVALID, "update_start: no such flow");
+  if (!finite_nonneg(start)) return fail(h, NETSIM_E_INVALID, "update_start: start must be finite and >= 0");
+  h->f_start[(size_t)id] = start;
+  if (!h->prepared) return NETSIM_OK;  // uploaded by the first run
   hipError_t he = hipSetDevice(h->opt.device);
   if (he != hipSuccess) return hip_fail(h, he, "hipSetDevice");
-  rc = reset_state(h, st);
+  const Params& P = h->prm;
+  const int32_t d = h->dev_of_flow[(size_t)id];
+  he = hipMemcpy(const_cast<double*>(P.start) + d, &start, sizeof(double), hipMemcpyHostToDevice);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (start)");
+  if (!h->has_state) return NETSIM_OK;  // the next run starts from t = 0 with it
+  const int32_t p = part_of_dev(h, d);
+  int32_t cnt = 0;
+  double rel_old = 0.0, base = 0.0;
+  he = hipMemcpy(&cnt, P.cnt + d, sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (he == hipSuccess) he = hipMemcpy(&rel_old, P.rel + d, sizeof(double), hipMemcpyDeviceToHost);
+  if (he == hipSuccess) he = hipMemcpy(&base, P.base + d, sizeof(double), hipMemcpyDeviceToHost);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (flow state)");
+  if (cnt > 0) return NETSIM_OK;  // waiting for predecessors: applies when they finish
+  const double t_part = h->part_t[(size_t)p];
+  const double rel_new = start + base;
+  const bool released = rel_old <= t_part;
+  if (!released && rel_new >= t_part) {
+    // still pending and the new release is not in the part's past
+    he = hipMemcpy(P.rel + d, &rel_new, sizeof(double), hipMemcpyHostToDevice);
+    return he == hipSuccess ? NETSIM_OK : hip_fail(h, he, "hipMemcpy (release)");
+  }
+  // time rollback (Section 4.2): the part goes back to the latest state in
+  // which the flow was not yet released and that precedes its new release
+  const double before = released ? std::min(rel_old, rel_new) : rel_new;
+  netsim_status rc = restore_part(h, p, latest_checkpoint(h, p, before));
   if (rc) return rc;
-  const auto t1 = std::chrono::steady_clock::now();
-  float ms = 0.0f;
-  if (h->F > 0) {
-    rc = launch(h, st, false, &ms);
-    if (rc) return rc;
+  he = hipMemcpy(&cnt, P.cnt + d, sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (flow state)");
+  if (cnt == 0) {
+    he = hipMemcpy(P.rel + d, &rel_new, sizeof(double), hipMemcpyHostToDevice);
+    if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (release)");
   }
-  std::vector<ScenCtl> ctl;
-  rc = h->F > 0 ? collect(h, &ctl) : NETSIM_OK;
-  if (h->F == 0) ctl = h->h_ctl0;
-  // results, even on a device fault (partial), for inspection
-  const int64_t F = h->F;
-  std::vector<double> fin_dev((size_t)std::max<int64_t>(F, 1));
-  if (F > 0) {
-    he = hipMemcpy(fin_dev.data(), h->prm.finish, sizeof(double) * (size_t)F, hipMemcpyDeviceToHost);
-    if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (finish)");
+  return NETSIM_OK;
+}
+
+netsim_status netsim_gc(netsim_t* h, double t_min) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "gc: handle is NULL");
+  if (std::isnan(t_min)) return fail(h, NETSIM_E_INVALID, "gc: bad time");
+  auto& cps = h->checkpoints;
+  std::vector<char> keep(cps.size(), 1);
+  for (size_t k = 0; k < cps.size(); ++k) {
+    bool covered = true;  // every part that may use k has a later checkpoint before t_min
+    for (int32_t p = 0; p < h->num_parts && covered; ++p) {
+      if (!cps[k].valid[(size_t)p]) continue;
+      bool later = false;
+      for (size_t j = k + 1; j < cps.size() && !later; ++j)
+        later = cps[j].valid[(size_t)p] && cps[j].t[(size_t)p] < t_min;
+      covered = later;
+    }
+    if (covered) keep[k] = 0;
   }
-  h->finish.assign((size_t)F, 0.0);
-  for (int64_t id = 0; id < F; ++id) h->finish[(size_t)id] = fin_dev[(size_t)h->dev_of_flow[(size_t)id]];
-  h->makespan.assign(h->scen.size(), 0.0);
-  netsim_stats s{};
-  s.complete = 1;
-  s.parts = h->num_parts;
-  const int32_t NP = h->num_parts;
-  for (int32_t k = 0; k < NP; ++k) {
-    const ScenCtl& c = ctl[(size_t)k];
-    double& m = h->makespan[(size_t)c.scen];
-    for (int32_t d = c.f0; d < c.f1; ++d)
-      if (!std::isnan(fin_dev[(size_t)d])) {
-        m = std::max(m, fin_dev[(size_t)d]);
-        s.completed_flows += 1;
-      }
-    s.events += c.events;
-    s.solves += c.solves;
-    s.rounds += c.rounds;
-    s.flows_swept += c.flows_swept;
-    s.incidences_swept += c.incidences_swept;
-    s.active_swept += c.active_swept;
-    s.pending_swept += c.pending_swept;
-    s.reselected += c.reselected;
-    s.wide_solves += c.wide_solves;
-    s.sim_time = std::max(s.sim_time, c.t);
-    if (c.status != 0) s.complete = 0;
+  std::vector<netsim_t::Checkpoint> out;
+  for (size_t k = 0; k < cps.size(); ++k) {
+    if (keep[k]) out.push_back(std::move(cps[k]));
+    else (void)hipFree(cps[k].dev);
   }
-  int khz = 0;
-  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->opt.device) != hipSuccess || khz <= 0)
-    khz = 100000;
-  for (int32_t k = 0; k < NP; ++k)
-    for (int j = 0; j < 8; ++j) s.phase_seconds[j] += (double)ctl[(size_t)k].ticks[j] / (1e3 * khz);
-  s.device_seconds = ms * 1e-3;
-  s.upload_seconds = std::chrono::duration<double>(t1 - t0).count();
-  h->stats = s;
-  h->has_result = true;
-  return rc;
+  cps = std::move(out);
+  return NETSIM_OK;
+}
+
+netsim_status netsim_num_checkpoints(const netsim_t* h, int64_t* n) {
+  if (!h || !n) return fail(h, NETSIM_E_INVALID, "num_checkpoints: NULL argument");
+  *n = (int64_t)h->checkpoints.size();
+  return NETSIM_OK;
 }
 
 netsim_status netsim_get_finish(const netsim_t* h, double* finish, double* makespan) {
@@ -994,6 +1207,7 @@ void netsim_destroy(netsim_t* h) {
   if (!h) return;
   if (h->d_block) {
     (void)hipSetDevice(h->opt.device);
+    drop_checkpoints(h);
     (void)hipFree(h->d_block);
   }
   delete h;

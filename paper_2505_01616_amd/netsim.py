@@ -97,6 +97,10 @@ _SIGS = {
     "netsim_get_finish_device": (_I32, [_H, _P]),
     "netsim_get_stats": (_I32, [_H, ctypes.POINTER(netsim_stats)]),
     "netsim_solve_once": (_I32, [_H, _I32, _I64, _P, _P]),
+    "netsim_advance": (_I32, [_H, _D, _I64, _P]),
+    "netsim_update_start": (_I32, [_H, _I64, _D]),
+    "netsim_gc": (_I32, [_H, _D]),
+    "netsim_num_checkpoints": (_I32, [_H, ctypes.POINTER(_I64)]),
     "netsim_last_error": (ctypes.c_char_p, [_H]),
     "netsim_destroy": (None, [_H]),
 }
@@ -247,12 +251,16 @@ def netsim_set_limits(h, max_events=0, until=math.inf):
     _check(h, load_library().netsim_set_limits(h, int(max_events), float(until)))
 
 
-def netsim_run(h, stream=None):
-    """stream: None, an int handle, or an object with a ``cuda_stream``
-    attribute (a torch.cuda.Stream)."""
+def _stream(stream):
+    """None, an int handle, or an object with a ``cuda_stream`` attribute
+    (a torch.cuda.Stream)."""
     if stream is not None and not isinstance(stream, int):
         stream = stream.cuda_stream
-    _check(h, load_library().netsim_run(h, stream))
+    return stream
+
+
+def netsim_run(h, stream=None):
+    _check(h, load_library().netsim_run(h, _stream(stream)))
 
 
 def netsim_get_finish(h):
@@ -287,6 +295,24 @@ def netsim_solve_once(h, scen, active_ids):
     rates = np.zeros(max(len(ids), 1))
     _check(h, load_library().netsim_solve_once(h, scen, len(ids), _ptr(ids), _ptr(rates)))
     return rates[: len(ids)]
+
+
+def netsim_advance(h, until=math.inf, max_events=0, stream=None):
+    _check(h, load_library().netsim_advance(h, float(until), int(max_events), _stream(stream)))
+
+
+def netsim_update_start(h, flow_id, start):
+    _check(h, load_library().netsim_update_start(h, int(flow_id), float(start)))
+
+
+def netsim_gc(h, t_min):
+    _check(h, load_library().netsim_gc(h, float(t_min)))
+
+
+def netsim_num_checkpoints(h) -> int:
+    n = _I64()
+    _check(h, load_library().netsim_num_checkpoints(h, ctypes.byref(n)))
+    return n.value
 
 
 def netsim_last_error(h=None) -> str:

@@ -187,3 +187,26 @@ def test_error_device_without_gpu():
         assert _status(ns.netsim_run, h) == ns.E_DEVICE
     finally:
         ns.netsim_destroy(h)
+
+
+def test_update_start_host_side():
+    """Time-rollback entry points without a GPU: argument checks, and a start
+    changed before the first run is what the flows hold (and export)."""
+    h = ns.netsim_create(np.array([0, 2], np.int64), np.array([1.0, 2.0]))
+    try:
+        po = np.array([0, 1, 2], np.int64)
+        ns.netsim_add_flows(h, 0, [4.0, 8.0], [0.0, 0.5], path_off=po,
+                            path_link=np.array([0, 1], np.int32))
+        assert _status(ns.netsim_update_start, h, 2, 1.0) == ns.E_INVALID     # no such flow
+        assert _status(ns.netsim_update_start, h, -1, 1.0) == ns.E_INVALID
+        assert _status(ns.netsim_update_start, h, 0, -1.0) == ns.E_INVALID    # negative start
+        assert _status(ns.netsim_update_start, h, 0, np.nan) == ns.E_INVALID
+        assert _status(ns.netsim_advance, h, np.nan, 0) == ns.E_INVALID
+        assert _status(ns.netsim_advance, h, 1.0, -1) == ns.E_INVALID
+        assert _status(ns.netsim_gc, h, np.nan) == ns.E_INVALID
+        ns.netsim_update_start(h, 1, 0.25)
+        np.testing.assert_array_equal(ns.netsim_export_flows(h)["start"], [0.0, 0.25])
+        assert ns.netsim_num_checkpoints(h) == 0
+        ns.netsim_gc(h, 1.0)
+    finally:
+        ns.netsim_destroy(h)
