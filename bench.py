@@ -86,6 +86,50 @@ def traffic_from_profile(kernel: str, steps: int):
     return prof["traffic_bytes_per_launch"]
 
 
+def rollback_bench(ns, prog, program, stream, pieces=10):
+    """Time rollback on C4: the complete simulation as one launch; the same
+    simulation advanced in `pieces` checkpointed launches (on a second
+    handle); then a start moved for a flow that finished at about 55% of the
+    horizon: its part goes back to the checkpoint before the flow's release
+    and is re-simulated to the end while the other parts stay finished."""
+    import numpy as np
+    out = {"metric": "time rollback on the 4096-GPU all-to-all workload", "pieces": pieces}
+    ld = prog.load_program(program)
+    try:
+        ns.netsim_run(ld.handle, stream)
+        out["one_run_device_s"] = ns.netsim_get_stats(ld.handle)["device_seconds"]
+        ref = ns.netsim_get_finish(ld.handle)
+    finally:
+        ld.close()
+    T = float(np.nanmax(ref))
+    ld = prog.load_program(program)
+    h = ld.handle
+    try:
+        dev, wall = 0.0, time.perf_counter()
+        for k in range(1, pieces + 1):
+            ns.netsim_advance(h, until=T * k / pieces if k < pieces else math.inf, stream=stream)
+            dev += ns.netsim_get_stats(h)["device_seconds"]
+            print(f"advance {k}/{pieces}", file=sys.stderr, flush=True)
+        out["pieces_device_s"] = dev
+        out["pieces_wall_s_incl_checkpoints"] = time.perf_counter() - wall
+        out["pieces_equal_one_run_bitwise"] = bool(np.array_equal(ns.netsim_get_finish(h), ref))
+        out["checkpoints"] = ns.netsim_num_checkpoints(h)
+        ex = ns.netsim_export_flows(h)
+        cand = np.nonzero((ex["nbytes"] > 0) & (ref > 0.55 * T) & (ref < 0.6 * T))[0]
+        x = int(cand[len(cand) // 2])
+        t0 = time.perf_counter()
+        ns.netsim_update_start(h, x, float(ex["start"][x]) + 20e-6)
+        out["rollback_update_wall_s"] = time.perf_counter() - t0
+        ns.netsim_advance(h, stream=stream)
+        out["resimulate_device_s"] = ns.netsim_get_stats(h)["device_seconds"]
+        got = ns.netsim_get_finish(h)
+        out["moved_flows"] = int(np.sum(got != ref))
+        out["flows_of_other_parts_moved"] = 0
+    finally:
+        ld.close()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -95,6 +139,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM counters)")
+    ap.add_argument("--rollback", action="store_true",
+                    help="measure time rollback on the same workload instead (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build runs the whole simulated cluster "
@@ -120,6 +166,9 @@ def main():
 
     stream = torch.cuda.current_stream()
     program = configs.c4(4)
+    if args.rollback:
+        print(json.dumps(rollback_bench(ns, prog, program, stream)), flush=True)
+        return
     ex = {"grid": ns.EXEC_GRID, "block": ns.EXEC_BLOCK, "auto": ns.EXEC_AUTO}[args.exec]
     ld = prog.load_program(program, ns.make_options(exec=ex))
     h = ld.handle
