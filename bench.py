@@ -124,7 +124,6 @@ def rollback_bench(ns, prog, program, stream, pieces=10):
         out["resimulate_device_s"] = ns.netsim_get_stats(h)["device_seconds"]
         got = ns.netsim_get_finish(h)
         out["moved_flows"] = int(np.sum(got != ref))
-        out["flows_of_other_parts_moved"] = 0
     finally:
         ld.close()
     return out
