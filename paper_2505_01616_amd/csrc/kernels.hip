@@ -548,7 +548,7 @@ __device__ __forceinline__ void round_table(G& g, LK& lk, const ScenCtl* C) {
 
 template <class LK>
 __device__ __forceinline__ double share_and_block(LK& lk, const int* lv, int deg, uint32_t st,
-                                                  int& bad) {
+                                                  int& bad, uint32_t* at_min = nullptr) {
   double sv[6];
   double m = INF;
 #pragma unroll
@@ -558,10 +558,15 @@ __device__ __forceinline__ double share_and_block(LK& lk, const int* lv, int deg
       m = sv[k] < m ? sv[k] : m;
     }
   const double thr = m * THR;
+  uint32_t cm = 0;  // links of the path within the tie band of its minimum
 #pragma unroll
   for (int k = 0; k < 6; ++k)
-    if (k < deg && sv[k] > thr) lk.block(lv[k], st);
+    if (k < deg) {
+      if (sv[k] > thr) lk.block(lv[k], st);
+      else cm |= 1u << k;
+    }
   if (!(m > 0.0) || !(m < INF)) bad = 1;
+  if (at_min) *at_min = cm;
   return m;
 }
 
@@ -723,12 +728,13 @@ __device__ __forceinline__ void for_items(uint64_t mask, uint64_t cmask, const F
   for (uint64_t m = mask & cmask; m; m &= m - 1) {
     const int k = __ffsll((unsigned long long)m) - 1;
     const int i = (int)threadIdx.x + k * T;
-    body(k, fc.fid[i], fc.path[i]);
+    body(k, i, true, fc.fid[i], fc.path[i]);
   }
   for (uint64_t m = mask & ~cmask; m; m &= m - 1) {
     const int k = __ffsll((unsigned long long)m) - 1;
-    const int f = list[(int)threadIdx.x + k * T];
-    body(k, f, P.path16[f]);
+    const int i = (int)threadIdx.x + k * T;
+    const int f = list[i];
+    body(k, i, false, f, P.path16[f]);
   }
 }
 
@@ -773,34 +779,41 @@ __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, Sc
     round_table(g, lk, C);
     clk.lap(2);
     // phase B: smallest share on each path; block links above it
-    for_items(alive, cmask, fc, P, list, T, [&](int, int f, uint4 rec) {
+    // (a cached flow keeps, in its record's spare word, which of its links
+    // are at its minimum: the others carry its own stamp, so phase C need
+    // look only at those)
+    for_items(alive, cmask, fc, P, list, T, [&](int, int i, bool cached, int f, uint4 rec) {
       if (!in_range(f, f0, cap)) { bad = 2; return; }
       int lv[6];
       const int deg = unpack_path(rec, l0, lv);
       isw += deg;
-      const double mv = share_and_block(lk, lv, deg, st, bad);
+      uint32_t cm;
+      const double mv = share_and_block(lk, lv, deg, st, bad, &cm);
       if constexpr (!LK::kTable) P.mf[f] = mv;
+      if (cached) fc.path[i].w = cm;
     });
     clk.lap(3);
     __syncthreads();
     clk.lap(4);
     // phase C: freeze flows crossing an unblocked link
     uint64_t frozen_mask = 0;
-    for_items(alive, cmask, fc, P, list, T, [&](int k, int f, uint4 rec) {
+    for_items(alive, cmask, fc, P, list, T, [&](int k, int, bool cached, int f, uint4 rec) {
       if (!in_range(f, f0, cap)) { bad = 2; return; }
       int lv[6];
       const int deg = unpack_path(rec, l0, lv);
+      const uint32_t cm = cached ? rec.w : 0x3Fu;
       bool frozen = false;
 #pragma unroll
       for (int j = 0; j < 6; ++j)
-        if (j < deg) frozen |= !lk.blocked(lv[j], st);
+        if (j < deg && ((cm >> j) & 1u)) frozen |= !lk.blocked(lv[j], st);
       if (!frozen) return;
       double mv;
       if constexpr (LK::kTable) {
+        // the smallest share is at one of the links at the minimum
         mv = INF;
 #pragma unroll
         for (int j = 0; j < 6; ++j)
-          if (j < deg) {
+          if (j < deg && ((cm >> j) & 1u)) {
             const double sv = lk.table(lv[j]);
             mv = sv < mv ? sv : mv;
           }
