@@ -222,6 +222,50 @@ netsim_status netsim_add_all_to_all(netsim_t* h, int32_t scen, int32_t p, const 
                                     const double* nbytes, double lag, int64_t n_after,
                                     const int64_t* after, int64_t* first_id, int64_t* count);
 
+/*
+ * Event-queue front end (Section 4.1: the simulator's event queue emulates
+ * CUDA streams and events -- operations on one stream run in order,
+ * operations on different streams are independent unless linked by an
+ * event; an NCCL collective starts its flows only once every rank of the
+ * communicator has reached it; a stream synchronisation returns the
+ * completion time of the stream's last operation).
+ *
+ * Streams are the caller's int64 ids within a scenario (a stream belongs to
+ * one rank; ids need not be dense).  Every call appends flows and returns
+ * the id of the zero-byte flow that marks the operation's completion on
+ * each participating stream (it becomes that stream's tail).  After a run,
+ * the finish time of a stream's tail is what a synchronisation on the
+ * stream returns; a tail recorded at some point serves as a CUDA event.
+ * A computation of d seconds is a zero-byte flow released d after the
+ * stream's tail and the flows it waits for.  A collective or send first
+ * appends a rendezvous (zero-byte flow after the tails of every
+ * participating stream), then its flows after it (as netsim_add_ring /
+ * netsim_add_all_to_all / one routed flow), then per rank a completion flow
+ * after the flows out of and into that rank that finish last (chained ring:
+ * the last step's; flat ring and all-to-all: all of them; aggregated ring:
+ * its two edges).  Built-in fabrics only for communication.  NETSIM_E_STATE
+ * after the first run; on error nothing is appended.
+ */
+netsim_status netsim_stream_compute(netsim_t* h, int32_t scen, int64_t stream, double duration,
+                                    int64_t n_wait, const int64_t* wait, int64_t* done);
+/* cudaStreamWaitEvent: the stream's next operation also waits for wait[]. */
+netsim_status netsim_stream_wait(netsim_t* h, int32_t scen, int64_t stream, int64_t n_wait,
+                                 const int64_t* wait);
+/* The stream's current tail (-1 for a stream without operations). */
+netsim_status netsim_stream_tail(const netsim_t* h, int32_t scen, int64_t stream, int64_t* flow);
+/* Ring collective of ranks[i] issued on streams[i] (distinct); done[p]. */
+netsim_status netsim_stream_ring(netsim_t* h, int32_t scen, int32_t kind, int32_t mode, int32_t p,
+                                 const int32_t* ranks, const int64_t* streams, double nbytes,
+                                 int64_t* done);
+/* All-to-all of ranks[i] issued on streams[i]; nbytes as netsim_add_all_to_all; done[p]. */
+netsim_status netsim_stream_all_to_all(netsim_t* h, int32_t scen, int32_t p, const int32_t* ranks,
+                                       const int64_t* streams, const double* nbytes, int64_t* done);
+/* Point-to-point send/recv: src on src_stream, dst on dst_stream (distinct);
+ * *done (may be NULL) receives the completion on src_stream (the same flow
+ * as dst_stream's new tail). */
+netsim_status netsim_stream_send(netsim_t* h, int32_t scen, int32_t src, int64_t src_stream,
+                                 int32_t dst, int64_t dst_stream, double nbytes, int64_t* done);
+
 /* Totals over all scenarios: flows, path incidences, dependency entries. */
 netsim_status netsim_counts(const netsim_t* h, int64_t* num_flows, int64_t* num_incidences,
                             int64_t* num_deps);

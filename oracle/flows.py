@@ -65,11 +65,15 @@ def expand(scenario) -> FlowSet:
     dep_lists = []          # per op: (counts array, flat ids array)
     explicit_paths = {}     # flow id -> list of links (explicit topologies)
     exits = []
+    firsts = []
     nflows = 0
     for op in scenario.ops:
-        pred = (np.concatenate([exits[a] for a in op.after]).astype(np.int64)
+        # an entry of `after` names an operation (its exits) or one flow of it
+        pred = (np.concatenate([np.array([firsts[a[0]] + a[1]]) if isinstance(a, tuple) else exits[a]
+                                for a in op.after]).astype(np.int64)
                 if len(op.after) else np.zeros(0, np.int64))
         first = nflows
+        firsts.append(first)
         if isinstance(op, Ring):
             ranks = np.asarray(op.ranks, dtype=np.int64)
             p = len(ranks)

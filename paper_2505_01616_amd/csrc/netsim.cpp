@@ -15,6 +15,7 @@
 #include <cstring>
 #include <limits>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "device.h"
@@ -33,6 +34,7 @@ struct Scen {
   bool has_fabric = false;
   netsim_host::Fabric fab;
   std::vector<int64_t> flows;  // ids of this scenario's flows, ascending
+  std::unordered_map<int64_t, int64_t> tails;  // stream -> completion flow of its last operation
 };
 
 }  // namespace
@@ -962,6 +964,195 @@ netsim_status netsim_add_all_to_all(netsim_t* h, int32_t scen, int32_t p, const 
   if (st) return st;
   if (first_id) *first_id = first;
   if (count) *count = n;
+  return NETSIM_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------- event-queue front end
+// A computation is a zero-byte flow whose release lags its dependencies by
+// its duration; a rendezvous is a zero-byte flow after the tails of every
+// participating stream; an operation's completion on a stream is the flow
+// that becomes the stream's tail.
+
+namespace {
+
+netsim_status check_stream_scen(netsim_t* h, int32_t s) {
+  if (h->prepared) return fail(h, NETSIM_E_STATE, "stream: operations cannot be added after a run");
+  if (s < 0 || s >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "stream: bad scenario");
+  return NETSIM_OK;
+}
+
+int64_t stream_tail(netsim_t* h, int32_t s, int64_t stream) {
+  auto it = h->scen[(size_t)s].tails.find(stream);
+  return it == h->scen[(size_t)s].tails.end() ? -1 : it->second;
+}
+
+// One zero-byte flow after `deps` (negative entries ignored) and `lag`.
+netsim_status zero_flow(netsim_t* h, int32_t s, std::vector<int64_t> deps, double lag, int64_t* id) {
+  deps.erase(std::remove_if(deps.begin(), deps.end(), [](int64_t d) { return d < 0; }), deps.end());
+  std::sort(deps.begin(), deps.end());
+  deps.erase(std::unique(deps.begin(), deps.end()), deps.end());
+  const int64_t poff[2] = {0, 0};
+  const int64_t doff[2] = {0, (int64_t)deps.size()};
+  const double zero = 0.0;
+  const int32_t none = -1;
+  return add_flows_impl(h, s, 1, &none, &none, &zero, &lag, poff, nullptr, doff,
+                        deps.empty() ? nullptr : deps.data(), id);
+}
+
+netsim_status check_streams(netsim_t* h, int32_t p, const int64_t* streams, int64_t* done) {
+  if (!streams || !done) return fail(h, NETSIM_E_INVALID, "stream collective: streams and done are required");
+  std::vector<int64_t> v(streams, streams + p);
+  std::sort(v.begin(), v.end());
+  if (std::adjacent_find(v.begin(), v.end()) != v.end())
+    return fail(h, NETSIM_E_INVALID, "stream collective: a stream appears twice");
+  return NETSIM_OK;
+}
+
+// Rendezvous of the streams, the collective after it (added by `add` with
+// the rendezvous as its only predecessor), and one completion flow per rank
+// after the collective flows that rank i still waits for (deps_of(i)).
+template <class Add, class DepsOf>
+netsim_status stream_collective(netsim_t* h, int32_t s, int32_t p, const int64_t* streams,
+                                int64_t* done, Add add, DepsOf deps_of) {
+  netsim_status st = check_streams(h, p, streams, done);
+  if (st) return st;
+  const size_t mark = h->f_bytes.size();
+  std::vector<int64_t> tails((size_t)p);
+  for (int32_t i = 0; i < p; ++i) tails[(size_t)i] = stream_tail(h, s, streams[i]);
+  int64_t rv = -1;
+  st = zero_flow(h, s, tails, 0.0, &rv);
+  int64_t first = -1;
+  if (!st) st = add(rv, &first);
+  std::vector<int64_t> ids((size_t)p);
+  for (int32_t i = 0; i < p && !st; ++i) st = zero_flow(h, s, deps_of(first, i), 0.0, &ids[(size_t)i]);
+  if (st) {
+    // all or nothing: drop what this call appended
+    while (h->f_bytes.size() > mark) {
+      h->f_scen.pop_back(); h->f_src.pop_back(); h->f_dst.pop_back();
+      h->f_bytes.pop_back(); h->f_start.pop_back();
+      h->p_link.resize((size_t)h->p_off[h->p_off.size() - 2]);
+      h->p_off.pop_back();
+      h->d_ids.resize((size_t)h->d_off[h->d_off.size() - 2]);
+      h->d_off.pop_back();
+      h->scen[(size_t)s].flows.pop_back();
+    }
+    return st;
+  }
+  for (int32_t i = 0; i < p; ++i) {
+    h->scen[(size_t)s].tails[streams[i]] = ids[(size_t)i];
+    done[i] = ids[(size_t)i];
+  }
+  return NETSIM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+netsim_status netsim_stream_compute(netsim_t* h, int32_t scen, int64_t stream, double duration,
+                                    int64_t n_wait, const int64_t* wait, int64_t* done) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "stream_compute: handle is NULL");
+  netsim_status st = check_stream_scen(h, scen);
+  if (st) return st;
+  if (!finite_nonneg(duration)) return fail(h, NETSIM_E_INVALID, "stream_compute: duration must be finite and >= 0");
+  if (n_wait < 0 || (n_wait > 0 && !wait)) return fail(h, NETSIM_E_INVALID, "stream_compute: bad wait list");
+  std::vector<int64_t> deps(wait, wait + n_wait);
+  deps.push_back(stream_tail(h, scen, stream));
+  int64_t id = -1;
+  st = zero_flow(h, scen, deps, duration, &id);
+  if (st) return st;
+  h->scen[(size_t)scen].tails[stream] = id;
+  if (done) *done = id;
+  return NETSIM_OK;
+}
+
+netsim_status netsim_stream_wait(netsim_t* h, int32_t scen, int64_t stream, int64_t n_wait,
+                                 const int64_t* wait) {
+  return netsim_stream_compute(h, scen, stream, 0.0, n_wait, wait, nullptr);
+}
+
+netsim_status netsim_stream_tail(const netsim_t* h, int32_t scen, int64_t stream, int64_t* flow) {
+  if (!h || !flow) return fail(h, NETSIM_E_INVALID, "stream_tail: NULL argument");
+  if (scen < 0 || scen >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "stream_tail: bad scenario");
+  *flow = stream_tail(const_cast<netsim_t*>(h), scen, stream);
+  return NETSIM_OK;
+}
+
+netsim_status netsim_stream_ring(netsim_t* h, int32_t scen, int32_t kind, int32_t mode, int32_t p,
+                                 const int32_t* ranks, const int64_t* streams, double nbytes,
+                                 int64_t* done) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "stream_ring: handle is NULL");
+  netsim_status st = check_stream_scen(h, scen);
+  if (st) return st;
+  if (p < 2) return fail(h, NETSIM_E_INVALID, "stream_ring: need p >= 2");
+  if (mode < NETSIM_MODE_CHAINED || mode > NETSIM_MODE_AGGREGATED) return fail(h, NETSIM_E_INVALID, "stream_ring: bad mode");
+  const int64_t steps = kind == NETSIM_RING_ALLREDUCE ? 2 * (int64_t)(p - 1) : (int64_t)(p - 1);
+  return stream_collective(
+      h, scen, p, streams, done,
+      [&](int64_t rv, int64_t* first) {
+        return netsim_add_ring(h, scen, kind, mode, p, ranks, nbytes, 0.0, 1, &rv, first, nullptr);
+      },
+      [&](int64_t first, int32_t i) {
+        // rank i is done when the flows out of it and into it are
+        const int64_t in = (i + p - 1) % p;
+        std::vector<int64_t> d;
+        if (mode == NETSIM_MODE_AGGREGATED) {
+          d = {first + i, first + in};
+        } else if (mode == NETSIM_MODE_CHAINED) {
+          d = {first + (steps - 1) * p + i, first + (steps - 1) * p + in};
+        } else {
+          for (int64_t k = 0; k < steps; ++k) {
+            d.push_back(first + k * p + i);
+            d.push_back(first + k * p + in);
+          }
+        }
+        return d;
+      });
+}
+
+netsim_status netsim_stream_all_to_all(netsim_t* h, int32_t scen, int32_t p, const int32_t* ranks,
+                                       const int64_t* streams, const double* nbytes, int64_t* done) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "stream_all_to_all: handle is NULL");
+  netsim_status st = check_stream_scen(h, scen);
+  if (st) return st;
+  if (p < 2) return fail(h, NETSIM_E_INVALID, "stream_all_to_all: need p >= 2");
+  return stream_collective(
+      h, scen, p, streams, done,
+      [&](int64_t rv, int64_t* first) {
+        return netsim_add_all_to_all(h, scen, p, ranks, nbytes, 0.0, 1, &rv, first, nullptr);
+      },
+      [&](int64_t first, int32_t i) {
+        std::vector<int64_t> d;
+        auto id = [&](int32_t a, int32_t b) { return first + (int64_t)a * (p - 1) + (b < a ? b : b - 1); };
+        for (int32_t j = 0; j < p; ++j)
+          if (j != i) {
+            d.push_back(id(i, j));
+            d.push_back(id(j, i));
+          }
+        return d;
+      });
+}
+
+netsim_status netsim_stream_send(netsim_t* h, int32_t scen, int32_t src, int64_t src_stream,
+                                 int32_t dst, int64_t dst_stream, double nbytes, int64_t* done) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "stream_send: handle is NULL");
+  netsim_status st = check_stream_scen(h, scen);
+  if (st) return st;
+  if (src_stream == dst_stream) return fail(h, NETSIM_E_INVALID, "stream_send: the two ends need two streams");
+  const int64_t streams[2] = {src_stream, dst_stream};
+  int64_t d2[2];
+  st = stream_collective(
+      h, scen, 2, streams, d2,
+      [&](int64_t rv, int64_t* first) {
+        const int64_t doff[2] = {0, 1};
+        const double lag = 0.0;
+        return add_flows_impl(h, scen, 1, &src, &dst, &nbytes, &lag, nullptr, nullptr, doff, &rv, first);
+      },
+      [&](int64_t first, int32_t) { return std::vector<int64_t>{first}; });
+  if (st) return st;
+  if (done) *done = d2[0];
   return NETSIM_OK;
 }
 

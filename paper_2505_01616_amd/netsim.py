@@ -98,6 +98,12 @@ _SIGS = {
     "netsim_get_stats": (_I32, [_H, ctypes.POINTER(netsim_stats)]),
     "netsim_solve_once": (_I32, [_H, _I32, _I64, _P, _P]),
     "netsim_advance": (_I32, [_H, _D, _I64, _P]),
+    "netsim_stream_compute": (_I32, [_H, _I32, _I64, _D, _I64, _P, ctypes.POINTER(_I64)]),
+    "netsim_stream_wait": (_I32, [_H, _I32, _I64, _I64, _P]),
+    "netsim_stream_tail": (_I32, [_H, _I32, _I64, ctypes.POINTER(_I64)]),
+    "netsim_stream_ring": (_I32, [_H, _I32, _I32, _I32, _I32, _P, _P, _D, _P]),
+    "netsim_stream_all_to_all": (_I32, [_H, _I32, _I32, _P, _P, _P, _P]),
+    "netsim_stream_send": (_I32, [_H, _I32, _I32, _I64, _I32, _I64, _D, ctypes.POINTER(_I64)]),
     "netsim_update_start": (_I32, [_H, _I64, _D]),
     "netsim_gc": (_I32, [_H, _D]),
     "netsim_num_checkpoints": (_I32, [_H, ctypes.POINTER(_I64)]),
@@ -295,6 +301,51 @@ def netsim_solve_once(h, scen, active_ids):
     rates = np.zeros(max(len(ids), 1))
     _check(h, load_library().netsim_solve_once(h, scen, len(ids), _ptr(ids), _ptr(rates)))
     return rates[: len(ids)]
+
+
+def netsim_stream_compute(h, scen, stream, duration, wait=()) -> int:
+    w = _arr(list(wait), np.int64)
+    out = _I64()
+    _check(h, load_library().netsim_stream_compute(h, scen, int(stream), float(duration), len(w),
+                                                   _ptr(w) if len(w) else None, ctypes.byref(out)))
+    return out.value
+
+
+def netsim_stream_wait(h, scen, stream, wait):
+    w = _arr(list(wait), np.int64)
+    _check(h, load_library().netsim_stream_wait(h, scen, int(stream), len(w), _ptr(w) if len(w) else None))
+
+
+def netsim_stream_tail(h, scen, stream) -> int:
+    out = _I64()
+    _check(h, load_library().netsim_stream_tail(h, scen, int(stream), ctypes.byref(out)))
+    return out.value
+
+
+def netsim_stream_ring(h, scen, kind, mode, ranks, streams, nbytes) -> np.ndarray:
+    r = _arr(ranks, np.int32)
+    st = _arr(streams, np.int64)
+    done = np.zeros(len(r), np.int64)
+    _check(h, load_library().netsim_stream_ring(h, scen, kind, mode, len(r), _ptr(r), _ptr(st),
+                                                float(nbytes), _ptr(done)))
+    return done
+
+
+def netsim_stream_all_to_all(h, scen, ranks, streams, nbytes) -> np.ndarray:
+    r = _arr(ranks, np.int32)
+    st = _arr(streams, np.int64)
+    b = _arr(nbytes, np.float64).reshape(-1)
+    done = np.zeros(len(r), np.int64)
+    _check(h, load_library().netsim_stream_all_to_all(h, scen, len(r), _ptr(r), _ptr(st), _ptr(b),
+                                                      _ptr(done)))
+    return done
+
+
+def netsim_stream_send(h, scen, src, src_stream, dst, dst_stream, nbytes) -> int:
+    out = _I64()
+    _check(h, load_library().netsim_stream_send(h, scen, int(src), int(src_stream), int(dst),
+                                                int(dst_stream), float(nbytes), ctypes.byref(out)))
+    return out.value
 
 
 def netsim_advance(h, until=math.inf, max_events=0, stream=None):

@@ -112,12 +112,18 @@ def load_program(program, opt: ns.netsim_options = None) -> Loaded:
             next_id = ns.netsim_counts(h)[0]
             first_flow.append(next_id)
             batch = _Batch(h, s, explicit[0])
-            exits = []
+            exits, firsts = [], []
             for op in sc.ops:
-                after = [x for a in op.after for x in exits[a]]
+                after = []
+                for a in op.after:   # an operation's exits, or one flow (op, j) of it
+                    if isinstance(a, tuple):
+                        after.append(firsts[a[0]] + a[1])
+                    else:
+                        after.extend(exits[a])
                 name = type(op).__name__
                 if name in ("Send", "Barrier", "PathFlow"):
                     fid = next_id + len(batch)
+                    firsts.append(fid)
                     if name == "Send":
                         batch.add(op.src, op.dst, op.nbytes, op.lag, after)
                     elif name == "Barrier":
@@ -132,6 +138,7 @@ def load_program(program, opt: ns.netsim_options = None) -> Loaded:
                     p = len(op.ranks)
                     first, n = ns.netsim_add_ring(h, s, _RING[op.kind], _MODE[op.mode], op.ranks,
                                                   op.nbytes, op.lag, after)
+                    firsts.append(first)
                     if op.mode == "chained":
                         steps = _STEPS[op.kind](p)
                         exits.append(list(range(first + (steps - 1) * p, first + steps * p)))
@@ -139,6 +146,7 @@ def load_program(program, opt: ns.netsim_options = None) -> Loaded:
                         exits.append(list(range(first, first + n)))
                 elif name == "AllToAll":
                     first, n = ns.netsim_add_all_to_all(h, s, op.ranks, op.nbytes, op.lag, after)
+                    firsts.append(first)
                     exits.append(list(range(first, first + n)))
                 else:
                     raise TypeError(f"unknown operation {name}")

@@ -19,10 +19,13 @@ Operations and their dependencies:
 * ``PathFlow``  -- one flow over an explicit list of link ids (only on
                    ``explicit`` topologies).
 
-``after`` lists indices of earlier operations in the same scenario.  The
-first flows of an operation wait for the last flows of every operation in
-``after``; ``lag`` seconds are added after that (with no ``after`` the lag
-is the absolute start time).
+``after`` lists earlier operations of the same scenario: an index names
+an operation (its first flows wait for its last flows), a pair (index, j)
+names flow j of that operation (flows numbered as the operation lays them
+out: a ring step-major, an all-to-all row-major without the diagonal).  The
+first flows of an operation wait for everything in ``after``; ``lag``
+seconds are added after that (with no ``after`` the lag is the absolute
+start time).
 """
 
 from __future__ import annotations
@@ -151,7 +154,8 @@ class Scenario:
 
     def add(self, op: Op) -> int:
         for a in op.after:
-            if not (0 <= a < len(self.ops)):
+            k = a[0] if isinstance(a, tuple) else a
+            if not (0 <= k < len(self.ops)) or (isinstance(a, tuple) and a[1] < 0):
                 raise ValueError("'after' must name an earlier operation")
         self.ops.append(op)
         return len(self.ops) - 1
