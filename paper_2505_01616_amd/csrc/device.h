@@ -93,6 +93,7 @@ struct Params {
   double* rate;            // [F] current rate
   double* finish;          // [F] completion time (NaN until finished)
   double* mf;              // [F] smallest fair share on the path (current round)
+  uint4* stage;            // [F] path records of a solve's items, by item (per part on [f0, f1))
   double* rel;             // [F] release time (set when a flow is released or pending)
   double* base;            // [F] release base: finish time of the last predecessor
   int32_t* cnt;            // [F] predecessors not yet finished

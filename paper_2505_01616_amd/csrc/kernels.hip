@@ -453,10 +453,12 @@ struct LinksShared {
   uint32_t* fl;
   int l0;
   double inv;
-  // Carves the link arrays for nl links out of the pool (16-byte aligned).
+  // Carves the link arrays for nl links and one sentinel entry (link id
+  // first + nl: share +inf, never stamped; what absent path entries point
+  // at, so that path gathers need no guard) out of the pool (16-byte aligned).
   __device__ __forceinline__ LinksShared(unsigned char* pool, int first, int nl, double inv_scale)
       : l0(first), inv(inv_scale) {
-    const int nl2 = (nl + 1) & ~1;
+    const int nl2 = (nl + 2) & ~1;
     R = reinterpret_cast<int64_t*>(pool);
     sh = reinterpret_cast<double*>(pool + 8 * nl2);
     n = reinterpret_cast<int32_t*>(pool + 16 * nl2);
@@ -468,6 +470,15 @@ struct LinksShared {
     return ((double)R[i] / (double)n[i]) * inv;
   }
   __device__ __forceinline__ double table(int l) const { return sh[l - l0]; }
+  __device__ __forceinline__ uint32_t stamp(int l) const { return fl[l - l0]; }
+  // the sentinel after the nl links of the part
+  __device__ __forceinline__ void set_sentinel(int nl) {
+    R[nl] = 0;
+    n[nl] = 0;
+    nact[nl] = 0;
+    fl[nl] = 0;
+    sh[nl] = INF;
+  }
   // link pass of a round: the share of every link with an unfrozen flow
   __device__ __forceinline__ void fill_table(int tid, int T, int nl) {
     for (int i = tid; i < nl; i += T)
@@ -498,8 +509,8 @@ struct LinksShared {
   }
 };
 
-// Bytes of the pool taken by the link arrays of nl links.
-__host__ __device__ constexpr int link_pool_bytes(int nl) { return LINK_LDS_BYTES * ((nl + 1) & ~1); }
+// Bytes of the pool taken by the link arrays of nl links and the sentinel.
+__host__ __device__ constexpr int link_pool_bytes(int nl) { return LINK_LDS_BYTES * ((nl + 2) & ~1); }
 
 // First round number of a solve of part C (read by every thread after a
 // group barrier).  Far from wrapping every stamp is cleared and numbering
@@ -710,6 +721,33 @@ struct FlowCache {
   int cap;
 };
 
+// Active flows live in slots: per part, the flow id, predicted completion
+// time tau and rate of every active flow (see the event loop).
+struct Slots {
+  int32_t* id;
+  double* tau;
+  double* rate;
+};
+
+// An incremental re-solve of the flows list[0..n): item i sits in slot at[i];
+// slots at or above s_new were activated at this event and hold no rate yet.
+// Before solving, each flow's contribution is taken back from its links and
+// its remaining bytes are brought up to time t; after solving, its slot gets
+// the new rate and predicted completion.
+struct Resel {
+  Slots sl;
+  const int32_t* at;
+  int s_new;
+  double t;
+};
+
+// Remaining bytes at t of a flow that had rem at tref and ran at rate r
+// (the same roundings in every solve variant: nothing is contracted).
+__device__ __forceinline__ double rem_at(double rem, double r, double t, double tref) {
+  const double moved = r * (t - tref);
+  return rem - moved;
+}
+
 // Bit k set for every item t + k*T < n of this thread (k < 64).
 __device__ __forceinline__ uint64_t low_items(int n, int T) {
   const int t = threadIdx.x;
@@ -717,110 +755,211 @@ __device__ __forceinline__ uint64_t low_items(int n, int T) {
   return c >= 64 ? ~0ull : (1ull << c) - 1ull;
 }
 
-// Calls body(k, f, rec) for every item k set in `mask` (item i = t + k*T):
-// flow id and path record from the shared-memory cache for the items below
-// nc (bits in cmask), from global memory for the rest.  Two separate loops,
-// so that the two kinds of read are never merged into one access through a
-// generic pointer.
+// Calls body(k, i, cached, rec) for every item k set in `mask` (item
+// i = t + k*T) with its path record: from the shared-memory cache for the
+// items in cmask, from the item-indexed staging buffer for the others.  The
+// records of four items are loaded before the first of them is processed,
+// so their latencies overlap.  Two separate loops, so that the two kinds of
+// read are never merged into one access through a generic pointer.
 template <class Body>
 __device__ __forceinline__ void for_items(uint64_t mask, uint64_t cmask, const FlowCache& fc,
-                                          const Params& P, const int32_t* list, int T, Body body) {
-  for (uint64_t m = mask & cmask; m; m &= m - 1) {
-    const int k = __ffsll((unsigned long long)m) - 1;
-    const int i = (int)threadIdx.x + k * T;
-    body(k, i, true, fc.fid[i], fc.path[i]);
+                                          const uint4* stg, int T, Body body) {
+  for (uint64_t m = mask & cmask; m;) {
+    int k[4];
+    uint4 r[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      k[u] = m ? __ffsll((unsigned long long)m) - 1 : -1;
+      m &= m - 1;
+      if (k[u] >= 0) r[u] = fc.path[(int)threadIdx.x + k[u] * T];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (k[u] >= 0) body(k[u], (int)threadIdx.x + k[u] * T, true, r[u]);
   }
-  for (uint64_t m = mask & ~cmask; m; m &= m - 1) {
-    const int k = __ffsll((unsigned long long)m) - 1;
-    const int i = (int)threadIdx.x + k * T;
-    const int f = list[i];
-    body(k, i, false, f, P.path16[f]);
+  for (uint64_t m = mask & ~cmask; m;) {
+    int k[4];
+    uint4 r[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      k[u] = m ? __ffsll((unsigned long long)m) - 1 : -1;
+      m &= m - 1;
+      if (k[u] >= 0) r[u] = stg[(int)threadIdx.x + k[u] * T];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (k[u] >= 0) body(k[u], (int)threadIdx.x + k[u] * T, false, r[u]);
   }
 }
 
 // Thread t of the workgroup owns the flows list[t + k*T], k < 64, and keeps
 // which of them are still unfrozen as a 64-bit mask, so a round needs no list
 // compaction: the workgroup barriers, the path reads (one 16-byte record per
-// flow, from the shared-memory cache for the first fc.cap flows), the
-// link-state gathers and the freezing atomics.  With a share table the
-// smallest share of a frozen flow is read again from the table in phase C
-// (the table does not change within a round).  Paths must fit the record
-// (<= 6 links, part-local ids below 0xFFFF); n <= 64*T.
+// flow: from the shared-memory cache for the first fc.cap items, from the
+// staging buffer P.stage, indexed by item, for the rest; both filled once per
+// solve), the link-state gathers and the freezing atomics.  With a share
+// table the smallest share of a frozen flow is read again from the table in
+// phase C (the table does not change within a round).  With rs, the
+// re-solve's take-back is done while the records are gathered and the slots
+// are written as flows freeze.  Paths must fit the record (<= 6 links,
+// part-local ids below 0xFFFF); n <= 64*T.
 template <class LK>
 __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, ScenCtl* C,
                                           const int32_t* list, int n, int64_t& rounds, int64_t& fsw,
-                                          int64_t& isw, Clock& clk, bool warm, const FlowCache& fc) {
+                                          int64_t& isw, Clock& clk, bool warm, const FlowCache& fc,
+                                          const Resel* rs) {
   Lists* K = g.lists(C);
   const int T = blockDim.x;
   const int l0 = C->l0;
   const int f0 = C->f0, cap = C->f1 - C->f0;
+  uint4* stg = P.stage + f0;
+  double* mfi = P.mf + f0;  // smallest share per item (link state without a table)
+  const int lsent = C->l1;  // the sentinel's id (link state with a table)
   int* cntr = g.ldsi + 112;  // three rotating counters of unfrozen flows
+  int bad = 0;
   if (!warm) cold_links(g, P, lk, C);
   const uint64_t alive0 = low_items(n, T);
   uint64_t alive = alive0;
   const int nc = min(n, fc.cap);
   const uint64_t cmask = low_items(nc, T);  // items served from the cache
-  for (int i = threadIdx.x; i < nc; i += T) {
-    const int f = list[i];
-    fc.fid[i] = f;
-    fc.path[i] = in_range(f, f0, cap) ? P.path16[f] : make_uint4(~0u, ~0u, ~0u, ~0u);
+  // gather: ids, path records (and, re-solving, the rates and remaining
+  // bytes to take back), four items of a thread in flight at a time
+  for (int j0 = 0; j0 * T < n; j0 += 4) {
+    int fv[4], sv[4];
+    uint4 rv[4];
+    double rr[4], tr[4], rm[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = (int)threadIdx.x + (j0 + u) * T;
+      fv[u] = i < n ? list[i] : f0;
+      sv[u] = (rs && i < n) ? rs->at[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = (int)threadIdx.x + (j0 + u) * T;
+      const bool ok = i < n && in_range(fv[u], f0, cap) && (unsigned)sv[u] < (unsigned)cap;
+      rv[u] = ok ? P.path16[fv[u]] : make_uint4(~0u, ~0u, ~0u, ~0u);
+      if (rs && ok && sv[u] < rs->s_new) {
+        rr[u] = rs->sl.rate[sv[u]];
+        tr[u] = P.tref[fv[u]];
+        rm[u] = P.rem[fv[u]];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = (int)threadIdx.x + (j0 + u) * T;
+      if (i >= n) continue;
+      const int f = fv[u];
+      if (!in_range(f, f0, cap) || (unsigned)sv[u] >= (unsigned)cap) bad = 2;
+      if (i < nc) {
+        fc.fid[i] = f;
+        fc.path[i] = rv[u];
+      } else {
+        stg[i] = rv[u];
+      }
+      if (rs && in_range(f, f0, cap)) {
+        const bool fresh = sv[u] >= rs->s_new;
+        int lv[6];
+        const int deg = unpack_path(rv[u], l0, lv);
+        int64_t qv = 0;
+        if (!fresh) {
+          P.rem[f] = rem_at(rm[u], rr[u], rs->t, tr[u]);
+          P.tref[f] = rs->t;
+          qv = (int64_t)__builtin_rint(rr[u] * P.scale);
+        }
+#pragma unroll
+        for (int j = 0; j < 6; ++j)
+          if (j < deg) {
+            if (!fresh) lk.addR(g, lv[j], qv);
+            lk.addN(g, lv[j], (int64_t)1);
+          }
+      }
+    }
   }
   if (threadIdx.x < 3) cntr[threadIdx.x] = 0;
+  if (bad) g.store(&K->fault, bad);
   __syncthreads();
   const uint32_t st0 = first_round(g, P, lk, C);
   clk.lap(2);
   int total = n;
   int r = 0;
-  int bad = 0;
   int rc = 0;
-  for (;;) {
+  if (g.load(&K->fault) != 0) rc = ST_OVERFLOW;
+  for (; rc == 0;) {
     const uint32_t st = st0 + (uint32_t)r;
     if (threadIdx.x == 0) cntr[(r + 1) % 3] = 0;
     round_table(g, lk, C);
     clk.lap(2);
-    // phase B: smallest share on each path; block links above it
-    // (a cached flow keeps, in its record's spare word, which of its links
-    // are at its minimum: the others carry its own stamp, so phase C need
-    // look only at those)
-    for_items(alive, cmask, fc, P, list, T, [&](int, int i, bool cached, int f, uint4 rec) {
-      if (!in_range(f, f0, cap)) { bad = 2; return; }
+    // phase B: smallest share on each path; block links above it.  The
+    // record's spare word keeps which of the flow's links are at its
+    // minimum: the others carry its own stamp, so phase C looks only at those
+    for_items(alive, cmask, fc, stg, T, [&](int, int i, bool cached, uint4 rec) {
       int lv[6];
       const int deg = unpack_path(rec, l0, lv);
       isw += deg;
-      uint32_t cm;
-      const double mv = share_and_block(lk, lv, deg, st, bad, &cm);
-      if constexpr (!LK::kTable) P.mf[f] = mv;
+      uint32_t cm = 0;
+      if constexpr (LK::kTable) {
+        // six unguarded gathers (absent links read the sentinel's +inf),
+        // all in flight before the first is used
+        double sv[6];
+#pragma unroll
+        for (int k = 0; k < 6; ++k) {
+          lv[k] = min(lv[k], lsent);
+          sv[k] = lk.table(lv[k]);
+        }
+        double m = sv[0];
+#pragma unroll
+        for (int k = 1; k < 6; ++k) m = sv[k] < m ? sv[k] : m;
+        const double thr = m * THR;
+#pragma unroll
+        for (int k = 0; k < 6; ++k) {
+          if (!(sv[k] > thr)) cm |= 1u << k;
+          else if (sv[k] < INF) lk.block(lv[k], st);
+        }
+        if (!(m > 0.0) || !(m < INF)) bad = 1;
+      } else {
+        mfi[i] = share_and_block(lk, lv, deg, st, bad, &cm);
+      }
       if (cached) fc.path[i].w = cm;
+      else reinterpret_cast<uint32_t*>(stg + i)[3] = cm;
     });
     clk.lap(3);
     __syncthreads();
     clk.lap(4);
     // phase C: freeze flows crossing an unblocked link
     uint64_t frozen_mask = 0;
-    for_items(alive, cmask, fc, P, list, T, [&](int k, int, bool cached, int f, uint4 rec) {
-      if (!in_range(f, f0, cap)) { bad = 2; return; }
+    for_items(alive, cmask, fc, stg, T, [&](int k, int i, bool cached, uint4 rec) {
       int lv[6];
       const int deg = unpack_path(rec, l0, lv);
-      const uint32_t cm = cached ? rec.w : 0x3Fu;
+      const uint32_t cm = rec.w;
       bool frozen = false;
-#pragma unroll
-      for (int j = 0; j < 6; ++j)
-        if (j < deg && ((cm >> j) & 1u)) frozen |= !lk.blocked(lv[j], st);
-      if (!frozen) return;
       double mv;
       if constexpr (LK::kTable) {
+        uint32_t sp[6];
+#pragma unroll
+        for (int j = 0; j < 6; ++j) {
+          lv[j] = min(lv[j], lsent);
+          sp[j] = lk.stamp(lv[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < 6; ++j) frozen |= ((cm >> j) & 1u) && sp[j] != st;
+        if (!frozen) return;
         // the smallest share is at one of the links at the minimum
+        double sv[6];
+#pragma unroll
+        for (int j = 0; j < 6; ++j) sv[j] = lk.table(lv[j]);
         mv = INF;
 #pragma unroll
         for (int j = 0; j < 6; ++j)
-          if (j < deg && ((cm >> j) & 1u)) {
-            const double sv = lk.table(lv[j]);
-            mv = sv < mv ? sv : mv;
-          }
+          if ((cm >> j) & 1u) mv = sv[j] < mv ? sv[j] : mv;
       } else {
-        mv = P.mf[f];
+#pragma unroll
+        for (int j = 0; j < 6; ++j)
+          if (j < deg && ((cm >> j) & 1u)) frozen |= !lk.blocked(lv[j], st);
+        if (!frozen) return;
+        mv = mfi[i];
       }
-      P.rate[f] = mv;
+      if constexpr (LK::kTable) mfi[i] = mv;  // the rate, by item (written out after the rounds)
       const int64_t qv = (int64_t)__builtin_rint(mv * P.scale);
 #pragma unroll
       for (int j = 0; j < 6; ++j)
@@ -851,7 +990,64 @@ __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, Sc
     total = left;
   }
   if (threadIdx.x == 0) g.store(&K->stamp, st0 + (uint32_t)r);
+  if (rc == 0) {
+    // rates by flow (and, re-solving, the slots' rates and predicted
+    // completions), four items of a thread in flight at a time
+    for (int j0 = 0; j0 * T < n; j0 += 4) {
+      int fv[4], sv[4];
+      double mv[4], rm[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = (int)threadIdx.x + (j0 + u) * T;
+        if (i < n) {
+          fv[u] = i < nc ? fc.fid[i] : list[i];
+          mv[u] = mfi[i];
+          sv[u] = rs ? rs->at[i] : 0;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = (int)threadIdx.x + (j0 + u) * T;
+        if (i < n && rs) rm[u] = P.rem[fv[u]];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = (int)threadIdx.x + (j0 + u) * T;
+        if (i >= n) continue;
+        P.rate[fv[u]] = mv[u];
+        if (rs) {
+          rs->sl.rate[sv[u]] = mv[u];
+          rs->sl.tau[sv[u]] = rs->t + rm[u] / mv[u];
+        }
+      }
+    }
+  }
   return rc;
+}
+
+// The take-back of an incremental re-solve (see Resel) as a pass of its
+// own, for the solve variants that do not fuse it: any group, any path.
+template <class G, class LK>
+__device__ __forceinline__ void take_back(G& g, const Params& P, LK& lk, const int32_t* list, int n,
+                                          const Resel& rs, int f0, int cap, int& err) {
+  for (int j = g.tid(); j < n; j += g.nthr()) {
+    const int f = list[j];
+    const int s = rs.at[j];
+    if (!in_range(f, f0, cap) || (unsigned)s >= (unsigned)cap) { err = 1; continue; }
+    const bool fresh = s >= rs.s_new;
+    int64_t qv = 0;
+    if (!fresh) {
+      const double r = rs.sl.rate[s];
+      P.rem[f] = rem_at(P.rem[f], r, rs.t, P.tref[f]);
+      P.tref[f] = rs.t;
+      qv = (int64_t)__builtin_rint(r * P.scale);
+    }
+    for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+      const int l = P.plink[k];
+      if (!fresh) lk.addR(g, l, qv);
+      lk.addN(g, l, (int64_t)1);
+    }
+  }
 }
 
 // ---------------------------------------------- shared-memory-resident solve
@@ -1005,12 +1201,6 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
 // the other buffer.
 constexpr double KEEP = 1.0 - 1e-9;  // safety margin below theta
 
-struct Slots {
-  int32_t* id;
-  double* tau;
-  double* rate;
-};
-
 // Flow f becomes active at time t: remaining bytes, active counts on its
 // links, a new slot (tau set after its first solve) and the arrivals list.
 template <class G, class LK>
@@ -1093,6 +1283,9 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   int64_t& fsw = tl->fsw;
   // links at rest: nothing active; no component has changed yet
   for (int l = C->l0 + tid; l < C->l1; l += T) lk.reset(l, P.R0[l]);
+  if constexpr (LK::kTable) {
+    if (tid == 0) lk.set_sentinel(C->l1 - C->l0);
+  }
   const uint64_t INF_BITS = (uint64_t)__double_as_longlong(INF);
   for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
   double t = resume ? C->t : 0.0;
@@ -1322,22 +1515,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
               const int f = x.f;
               if (f < 0) return;  // a hole
               if (!in_range(f, f0, cap)) { err = 1; return; }
-              const bool fresh = s >= slots0;
-              const double r = x.a;
-              if (fresh || !(r < x.b * KEEP)) {
-                pr[0] = true;
-                if (!fresh) {
-                  const double moved = r * (t - P.tref[f]);
-                  P.rem[f] = P.rem[f] - moved;
-                  P.tref[f] = t;
-                }
-                const int64_t qv = fresh ? 0 : (int64_t)__builtin_rint(r * P.scale);
-                for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
-                  const int l = P.plink[k];
-                  if (!fresh) lk.addR(g, l, qv);
-                  lk.addN(g, l, (int64_t)1);
-                }
-              }
+              pr[0] = s >= slots0 || !(x.a < x.b * KEEP);
             },
             [&](int, int slot, const FlowVal& x) {
               if (slot < cap) {
@@ -1356,18 +1534,31 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       if (threadIdx.x == 0) tl->sel += nSel;
       int rc = 0;
       if (nSel > 0) {
+        const Resel rs{sl, arrSlot, slots0, t};
+        bool fused = false;  // take-back and slot writes done inside the solve
         if constexpr (!IsGrid<G>::value) {
           if (C->lds_paths && nSel <= 64 * (int)blockDim.x) {
-            rc = solve_mask(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc);
+            rc = solve_mask(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc, &rs);
+            fused = true;
           } else {
+            take_back(g, P, lk, arrs, nSel, rs, f0, cap, err);
+            if (err) g.store(&K->fault, 2);
+            g.sync();
             if (threadIdx.x == 0) tl->wide += 1;
-            rc = solve(g, P, lk, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
+            rc = g.load(&K->fault) != 0 ? ST_OVERFLOW
+                 : solve(g, P, lk, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
           }
         } else {
-          if (C->lds_paths && nSel <= LDS_FLOWS) {
+          take_back(g, P, lk, arrs, nSel, rs, f0, cap, err);
+          if (err) g.store(&K->fault, 2);
+          g.sync();
+          if (g.load(&K->fault) != 0) {
+            rc = ST_OVERFLOW;
+          } else if (C->lds_paths && nSel <= LDS_FLOWS) {
             if (g.block_id() == 0) {
               BlockG b{g.lds, g.ldsi, &C->k};  // the grid's counters, in global memory
-              const int r1 = solve_mask(b, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc);
+              const int r1 = solve_mask(b, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc,
+                                        nullptr);
               if (threadIdx.x == 0) g.store(&K->solve_rc, r1);
             }
             g.sync();
@@ -1379,14 +1570,16 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
             rc = solve(g, P, lk, C, arrs, nSel, unf_a, unf_b, cap, rounds, fsw, isw, clk, true);
           }
         }
-        // the re-solved flows' slots: new rate and predicted completion
-        for (int j = tid; j < nSel; j += T) {
-          const int f = arrs[j];
-          const int s = arrSlot[j];
-          if (!in_range(f, f0, cap) || (unsigned)s >= (unsigned)cap) continue;
-          const double r = P.rate[f];
-          sl.rate[s] = r;
-          sl.tau[s] = t + P.rem[f] / r;
+        if (!fused) {
+          // the re-solved flows' slots: new rate and predicted completion
+          for (int j = tid; j < nSel; j += T) {
+            const int f = arrs[j];
+            const int s = arrSlot[j];
+            if (!in_range(f, f0, cap) || (unsigned)s >= (unsigned)cap) continue;
+            const double r = P.rate[f];
+            sl.rate[s] = r;
+            sl.tau[s] = t + P.rem[f] / r;
+          }
         }
         g.sync();
       }
@@ -1488,7 +1681,8 @@ __device__ __forceinline__ void solve_only(G& g, const Params& P, const int sc, 
                    rounds, fsw, isw, clk, false);
     } else {
       if (C->lds_paths && C->n_solve <= 64 * (int)blockDim.x)
-        rc = solve_mask(g, P, lk, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, false, fc);
+        rc = solve_mask(g, P, lk, C, P.act0 + f0, C->n_solve, rounds, fsw, isw, clk, false, fc,
+                        nullptr);
       else
         rc = solve(g, P, lk, C, P.act0 + f0, C->n_solve, P.unf0 + f0, P.unf1 + f0, C->f1 - f0,
                    rounds, fsw, isw, clk, false);

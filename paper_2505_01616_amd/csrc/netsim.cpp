@@ -488,6 +488,7 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.nact, sizeof(int32_t) * Lz},
       {(void**)&P.fl, sizeof(uint32_t) * Lz},
       {(void**)&P.path16, 16 * Fz},
+      {(void**)&P.stage, 16 * Fz},
       {(void**)&P.comp0, sizeof(int32_t) * Fz},
       {(void**)&P.comp1, sizeof(int32_t) * Fz},
       {(void**)&P.comp2, sizeof(int32_t) * Fz},
