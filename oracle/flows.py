@@ -20,7 +20,33 @@ Flow numbering inside a ring: step-major, id = first + k*p + i.  An
 all-to-all over p ranks gives flows (i, j), j != i, in row-major order.
 Zero-byte flows get no route.  The last flows of an operation (what a
 later operation's ``after`` waits for) are the last step's p flows for a
-chained ring and all flows otherwise.
+chained ring, the broadcast flows for a tree, the last phase's last step for
+a hierarchical all-reduce, and all flows otherwise.
+
+Double binary tree (the ``Tree`` operation; an NCCL-like alternative to
+the ring, cf. the paper's Section 6 on replacing its ring algorithm): with
+node numbers u = 1..p for positions u - 1, node u of level l (the number of
+trailing zero bits of u) has, for l >= 1, a left child u - 2^(l-1) and a
+right child u + 2^j for the largest j < l with u + 2^j <= p (if any); the
+root is the largest power of two <= p; odd nodes are leaves (a parent's
+level always exceeds its child's).  Tree A puts position u - 1 at node u,
+tree B (its mirror) position p - u.  Per tree and edge (child c, parent q):
+a reduce flow c -> q of half the bytes after the reduce flows into c (a
+leaf: after the operation's predecessors, with its lag), and a broadcast
+flow q -> c after the broadcast flow into q (q the root: after the reduce
+flows into the root).  Reduce flows are laid out by child level, lowest
+first, broadcast flows highest first, each level by child node.
+
+Hierarchical all-reduce (``Hier``, ranks m x g): phase 1, per server, a
+chained ring reduce-scatter of chunks S/g over its g ranks; phase 2, per
+local position j, a chained ring all-reduce of chunks S/(g*m) over the m
+servers; phase 3, per server, a chained ring all-gather of chunks S/g.  The
+first step of a phase out of rank (s, i) waits for that rank's previous
+phase: the previous phase's last-step flows out of and into it.  Phases
+of one rank (g = 1: phases 1 and 3; m = 1: phase 2) are left out.
+
+Latency: a flow's latency is the sum over its path, in path order, of its
+links' latencies.
 """
 
 from __future__ import annotations
@@ -29,12 +55,130 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from workloads.program import AllToAll, Barrier, PathFlow, Ring, Send
+from workloads.program import AllToAll, Barrier, Hier, PathFlow, Ring, Send, Tree
 from .topology import Fabric
 
 _STEPS = {"allreduce": lambda p: 2 * (p - 1),
           "reduce_scatter": lambda p: p - 1,
           "all_gather": lambda p: p - 1}
+
+
+def _level(u: int) -> int:
+    return (u & -u).bit_length() - 1
+
+
+def btree(p: int):
+    """The binary tree over nodes 1..p described above: (root, edges (c, q)
+    ordered by child c, children of each node)."""
+    kids = {u: [] for u in range(1, p + 1)}
+    for u in range(2, p + 1, 2):
+        lvl = (u & -u).bit_length() - 1
+        kids[u].append(u - (1 << (lvl - 1)))
+        for j in range(lvl - 1, -1, -1):
+            if u + (1 << j) <= p:
+                kids[u].append(u + (1 << j))
+                break
+    parent = {c: q for q, cs in kids.items() for c in cs}
+    root = 1 << (p.bit_length() - 1)
+    return root, sorted(parent.items()), kids
+
+
+def _tree_flows(ranks, nbytes, lag, pred, first):
+    """Flows of a double binary tree all-reduce (see the module notes)."""
+    p = len(ranks)
+    root, edges, kids = btree(p)
+    red = sorted(edges, key=lambda e: (_level(e[0]), e[0]))    # leaves first
+    bc = sorted(edges, key=lambda e: (-_level(e[0]), e[0]))    # top first
+    rslot = {c: k for k, (c, _) in enumerate(red)}
+    bslot = {c: k for k, (c, _) in enumerate(bc)}
+    half = float(nbytes) / 2.0
+    s, d, nb, st, deps = [], [], [], [], []
+    exits = []
+    for t in range(2):
+        pos = (lambda u: u - 1) if t == 0 else (lambda u: p - u)
+        red0 = first + t * 2 * (p - 1)
+        bc0 = red0 + (p - 1)
+        for c, q in red:
+            s.append(ranks[pos(c)])
+            d.append(ranks[pos(q)])
+            into = [red0 + rslot[x] for x in kids[c]]
+            deps.append(into if into else list(pred))
+            st.append(0.0 if into else float(lag))
+        for c, q in bc:
+            s.append(ranks[pos(q)])
+            d.append(ranks[pos(c)])
+            deps.append([red0 + rslot[x] for x in kids[root]] if q == root else [bc0 + bslot[q]])
+            st.append(0.0)
+            exits.append(bc0 + bslot[c])
+        nb.extend([half] * (2 * (p - 1)))
+    return s, d, nb, st, deps, exits
+
+
+def _hier_flows(ranks, nbytes, lag, pred, first):
+    """Flows of a hierarchical all-reduce over an m x g rank array."""
+    R = np.asarray(ranks)
+    m, g = R.shape
+    S = float(nbytes)
+    s, d, nb, st, deps = [], [], [], [], []
+    done = {}  # (server, local) -> the previous phase's flows out of and into the rank
+
+    def start_deps(a, i):
+        return done[(a, i)] if (a, i) in done else list(pred)
+
+    def lag_of(a, i):
+        return 0.0 if (a, i) in done else float(lag)
+
+    def server_ring(steps_of, chunk):
+        nonlocal first
+        new_done = {}
+        for a in range(m):
+            base = first
+            for k in range(steps_of):
+                for i in range(g):
+                    s.append(R[a, i])
+                    d.append(R[a, (i + 1) % g])
+                    nb.append(chunk)
+                    if k == 0:
+                        deps.append(start_deps(a, i))
+                        st.append(lag_of(a, i))
+                    else:
+                        deps.append([base + (k - 1) * g + (i - 1) % g])
+                        st.append(0.0)
+            last = base + (steps_of - 1) * g
+            for i in range(g):
+                new_done[(a, i)] = [last + i, last + (i - 1) % g]
+            first += steps_of * g
+        done.clear()
+        done.update(new_done)
+
+    if g > 1:
+        server_ring(g - 1, S / g)                      # reduce-scatter
+    if m > 1:
+        new_done = {}
+        for j in range(g):                               # ring all-reduce per position
+            base = first
+            steps = 2 * (m - 1)
+            for k in range(steps):
+                for a in range(m):
+                    s.append(R[a, j])
+                    d.append(R[(a + 1) % m, j])
+                    nb.append(S / (g * m))
+                    if k == 0:
+                        deps.append(start_deps(a, j))
+                        st.append(lag_of(a, j))
+                    else:
+                        deps.append([base + (k - 1) * m + (a - 1) % m])
+                        st.append(0.0)
+            last = base + (steps - 1) * m
+            for a in range(m):
+                new_done[(a, j)] = [last + a, last + (a - 1) % m]
+            first += steps * m
+        done.clear()
+        done.update(new_done)
+    if g > 1:
+        server_ring(g - 1, S / g)                      # all-gather
+    exits = sorted({x for v in done.values() for x in v})
+    return s, d, nb, st, deps, exits
 
 
 @dataclass
@@ -49,6 +193,7 @@ class FlowSet:
     path_link: np.ndarray  # [nnz] i32
     dep_off: np.ndarray    # [F+1] i64
     dep_ids: np.ndarray    # [ndeps] i64
+    lat: np.ndarray = None  # [F] f64 path latency (None: all zero)
 
     @property
     def F(self):
@@ -122,6 +267,16 @@ def expand(scenario) -> FlowSet:
             cnt = np.full(n, len(pred), np.int64)
             ids = np.tile(pred, n)
             ex = first + np.arange(n, dtype=np.int64)
+        elif isinstance(op, (Tree, Hier)):
+            ranks = np.asarray(op.ranks, dtype=np.int64)
+            mk = _tree_flows if isinstance(op, Tree) else _hier_flows
+            fl = mk(ranks, op.nbytes, op.lag, pred, first)
+            s, d, nb, st, dl, ex = fl
+            n = len(nb)
+            cnt = np.array([len(x) for x in dl], np.int64)
+            ids = (np.concatenate([np.asarray(x, np.int64) for x in dl]) if n
+                   else np.zeros(0, np.int64))
+            ex = np.asarray(ex, np.int64)
         elif isinstance(op, (Send, Barrier, PathFlow)):
             n = 1
             if isinstance(op, Send):
@@ -176,5 +331,13 @@ def expand(scenario) -> FlowSet:
         path_off = np.zeros(nflows + 1, np.int64)
         np.cumsum(lens, out=path_off[1:])
         links = r_link
+    lat = None
+    if np.any(fab.lat != 0.0):
+        # summed in path order: ((0 + l_1) + l_2) + ...
+        lens = np.diff(path_off)
+        lat = np.zeros(nflows)
+        for k in range(int(lens.max()) if nflows else 0):
+            has = lens > k
+            lat[has] = lat[has] + fab.lat[links[path_off[:-1][has] + k]]
     return FlowSet(fab.cap, src, dst, nbytes, start, path_off, links.astype(np.int32),
-                   dep_off, dep_ids)
+                   dep_off, dep_ids, lat)

@@ -22,7 +22,8 @@
  *     k_l = number of such flows on l;  R_l = R_l - k_l*s*;  n_l -= k_l
  * Event loop, starting at t = 0:
  *   t_next = min(earliest pending release, min over active f of t + rem_f/r_f)
- *   flows with t + rem_f/r_f <= t_next*THR finish at t_next; the others
+ *   flows with t + rem_f/r_f <= t_next*THR send their last byte at t_next and
+ *   finish their path latency lat_f later (lat = NULL: zero); the others
  *   lose r_f*(t_next - t) bytes; t = t_next; a flow whose predecessors have
  *   all finished is released at start_f + (latest predecessor finish);
  *   released flows with release <= t arrive (zero-byte flows finish at once
@@ -237,7 +238,7 @@ static pitem pheap_pop(pheap* h) {
  * snap_rates[F] (0 for flows not active) and its time into *snap_time.
  */
 int oracle_run(int64_t L, const double* cap, int64_t F, const double* nbytes,
-               const double* start, const int64_t* poff, const int32_t* plink,
+               const double* start, const double* lat, const int64_t* poff, const int32_t* plink,
                const int64_t* doff, const int64_t* dids, int64_t max_events,
                double until, int64_t snap_solve, double* snap_rates, double* snap_time,
                double* finish, int64_t* counts) {
@@ -248,6 +249,7 @@ int oracle_run(int64_t L, const double* cap, int64_t F, const double* nbytes,
     for (int64_t f = 0; f < F; f++) {
         if (!(nbytes[f] >= 0.0) || !isfinite(nbytes[f])) return OR_INVALID;
         if (!(start[f] >= 0.0) || !isfinite(start[f])) return OR_INVALID;
+        if (lat && (!(lat[f] >= 0.0) || !isfinite(lat[f]))) return OR_INVALID;
         if (nbytes[f] > 0.0 && poff[f + 1] == poff[f]) return OR_INVALID;
         for (int64_t e = poff[f]; e < poff[f + 1]; e++)
             if (plink[e] < 0 || plink[e] >= L) return OR_INVALID;
@@ -349,7 +351,8 @@ int oracle_run(int64_t L, const double* cap, int64_t F, const double* nbytes,
             for (int64_t q = 0; q < na; q++) {
                 int64_t f = act[q];
                 if (tau[f] <= thr) {
-                    finish[f] = t_next;
+                    /* the last byte leaves at t_next; it arrives lat[f] later */
+                    finish[f] = lat ? t_next + lat[f] : t_next;
                     S.state[f] = DONE;
                     queue[nq++] = f;
                 } else {

@@ -75,6 +75,8 @@ def simulate(fs, exact: bool = True):
     caps = [num(float(c)) for c in fs.cap]
     nbytes = [num(float(b)) for b in fs.nbytes]
     start = [num(float(s)) for s in fs.start]
+    lat = ([num(float(x)) for x in fs.lat] if getattr(fs, "lat", None) is not None
+           else [num(0)] * F)
     deps = [list(map(int, fs.dep_ids[fs.dep_off[f]:fs.dep_off[f + 1]])) for f in range(F)]
     succ = [[] for _ in range(F)]
     for g in range(F):
@@ -102,7 +104,7 @@ def simulate(fs, exact: bool = True):
         step = t_next - t
         for f in list(active):
             if f in done:
-                finish[f] = t_next
+                finish[f] = t_next + lat[f]  # last byte sent at t_next, arrives lat later
                 del active[f]
             else:
                 active[f] = active[f] - rate[f] * step

@@ -27,7 +27,7 @@ def _load():
             build()
         lib = ctypes.CDLL(LIB)
         lib.oracle_run.restype = ctypes.c_int
-        lib.oracle_run.argtypes = [_I64, _P, _I64, _P, _P, _P, _P, _P, _P, _I64,
+        lib.oracle_run.argtypes = [_I64, _P, _I64, _P, _P, _P, _P, _P, _P, _P, _I64,
                                    ctypes.c_double, _I64, _P, _P, _P, _P]
         lib.oracle_solve.restype = ctypes.c_int
         lib.oracle_solve.argtypes = [_I64, _P, _I64, _P, _P, _I64, _P, _P, _P]
@@ -82,7 +82,10 @@ def run_flowset(fs: FlowSet, max_events: int = 0, snap_solve: int = 0,
     counts = np.zeros(5, np.int64)
     snap = np.zeros(max(F, 1)) if snap_solve else None
     stime = np.zeros(1)
-    rc = lib.oracle_run(fs.L, _ptr(cap), F, _ptr(nb), _ptr(st), _ptr(poff), _ptr(plink),
+    lat = (np.ascontiguousarray(fs.lat, np.float64)
+           if getattr(fs, "lat", None) is not None and F > 0 else None)
+    rc = lib.oracle_run(fs.L, _ptr(cap), F, _ptr(nb), _ptr(st),
+                        _ptr(lat) if lat is not None else None, _ptr(poff), _ptr(plink),
                         _ptr(doff), _ptr(dids), int(max_events), float(until),
                         int(snap_solve),
                         _ptr(snap) if snap is not None else None, _ptr(stime),

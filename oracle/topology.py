@@ -65,6 +65,9 @@ class Fabric:
         if self.kind == "explicit":
             self.cap = np.asarray(topo.capacities, dtype=np.float64).copy()
             self.L = len(self.cap)
+            lat = getattr(topo, "latencies", None)
+            self.lat = (np.zeros(self.L) if lat is None
+                        else np.asarray(lat, dtype=np.float64).copy())
             return
         G, S = topo.gpus_per_server, topo.servers
         self.G, self.S, self.N = G, S, G * S
@@ -91,6 +94,10 @@ class Fabric:
         cap[self.NV::2] = cab
         cap[self.NV + 1::2] = cab
         self.cap = cap
+        # link latency: NVLink links, then every cable direction
+        self.lat = np.empty(self.L, dtype=np.float64)
+        self.lat[: self.NV] = getattr(topo, "nvlink_latency_s", 0.0)
+        self.lat[self.NV:] = getattr(topo, "fabric_latency_s", 0.0)
 
     # ---- link end nodes (for checking routes) -----------------------------
     def link_ends(self):

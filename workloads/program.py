@@ -13,6 +13,13 @@ Operations and their dependencies:
                    decomposition modes ("chained", "flat", "aggregated").
 * ``AllToAll``  -- one flow per ordered pair of distinct ranks, sizes from a
                    p x p matrix (row = sender).
+* ``Tree``      -- a double binary tree all-reduce of ``nbytes`` over ``ranks``:
+                   two binary trees over the rank positions, each carrying
+                   half the bytes, reduced up and broadcast down.
+* ``Hier``      -- a hierarchical all-reduce over ``ranks`` given as an m x g
+                   array (row = server, g ranks each): reduce-scatter inside
+                   every server, a ring all-reduce across the servers for
+                   each local position, all-gather inside every server.
 * ``Send``      -- one point-to-point flow.
 * ``Barrier``   -- a zero-byte flow with no route; completes as soon as it
                    is released.
@@ -22,7 +29,9 @@ Operations and their dependencies:
 ``after`` lists earlier operations of the same scenario: an index names
 an operation (its first flows wait for its last flows), a pair (index, j)
 names flow j of that operation (flows numbered as the operation lays them
-out: a ring step-major, an all-to-all row-major without the diagonal).  The
+out: a ring step-major, an all-to-all row-major without the diagonal, a
+tree as tree A reduce, tree A broadcast, tree B reduce, tree B broadcast, a
+hierarchical all-reduce as its three phases in order).  The
 first flows of an operation wait for everything in ``after``; ``lag``
 seconds are added after that (with no ``after`` the lag is the absolute
 start time).
@@ -66,6 +75,10 @@ class Topology:
     ``fabric_Bps`` is the rate of every switch-to-switch cable.
     ``degraded`` lists cable indices (canonical cable order) whose two
     directions run at ``degraded_Bps``.
+    Latency: every NVLink link takes ``nvlink_latency_s``, every other link
+    ``fabric_latency_s`` (explicit topologies: ``latencies`` per link, or
+    none); a flow finishes its path's summed latency after its last byte
+    leaves.
     """
 
     kind: str
@@ -84,6 +97,9 @@ class Topology:
     degraded: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))
     degraded_Bps: float = 0.0
     capacities: Optional[np.ndarray] = None
+    fabric_latency_s: float = 0.0
+    nvlink_latency_s: float = 0.0
+    latencies: Optional[np.ndarray] = None
 
     @property
     def endpoints(self) -> int:
@@ -122,6 +138,22 @@ class AllToAll:
 
 
 @dataclass
+class Tree:
+    ranks: np.ndarray
+    nbytes: float
+    lag: float = 0.0
+    after: Sequence[int] = ()
+
+
+@dataclass
+class Hier:
+    ranks: np.ndarray    # m x g: row s holds the g ranks of server s
+    nbytes: float
+    lag: float = 0.0
+    after: Sequence[int] = ()
+
+
+@dataclass
 class Send:
     src: int
     dst: int
@@ -144,7 +176,7 @@ class PathFlow:
     after: Sequence[int] = ()
 
 
-Op = Union[Ring, AllToAll, Send, Barrier, PathFlow]
+Op = Union[Ring, AllToAll, Tree, Hier, Send, Barrier, PathFlow]
 
 
 @dataclass
