@@ -111,6 +111,11 @@ typedef struct {
  *   function.
  * degraded_cables (num_degraded entries, may be NULL when 0): cable ids whose
  * two links run at degraded_Bps.  Copied by netsim_create_topology.
+ * Latency (the flow model's bandwidth sharing is instantaneous; this adds
+ * propagation): every intra-server link takes nvlink_latency_s seconds, every
+ * cable direction fabric_latency_s (finite, >= 0; 0 = none).  A flow arrives
+ * the sum of its path's latencies after its last byte leaves; see
+ * netsim_set_link_latency.
  */
 typedef struct {
   int32_t kind;
@@ -130,6 +135,8 @@ typedef struct {
   int64_t num_degraded;
   const int64_t* degraded_cables;
   double degraded_Bps;
+  double fabric_latency_s;
+  double nvlink_latency_s;
 } netsim_topology;
 
 typedef struct {
@@ -223,6 +230,53 @@ netsim_status netsim_add_all_to_all(netsim_t* h, int32_t scen, int32_t p, const 
                                     const int64_t* after, int64_t* first_id, int64_t* count);
 
 /*
+ * Richer collectives (Section 6 names replacing the plain ring algorithm by
+ * NCCL-like ones as a route to accuracy).  Same conventions as
+ * netsim_add_ring (ranks distinct endpoints of the scenario's built-in
+ * fabric, bytes and lag finite >= 0, `after` flows of the same scenario;
+ * *first_id / *count may be NULL; NETSIM_E_STATE after the first run).
+ *
+ * netsim_add_tree_allreduce: double binary tree over ranks[0..p) (p >= 2).
+ * Node numbers u = 1..p; node u of level l = (trailing zero bits of u) >= 1
+ * has children u - 2^(l-1) and u + 2^j for the largest j < l with
+ * u + 2^j <= p (if any); the root is the largest power of two <= p.  Tree A
+ * puts ranks[u-1] at node u, tree B (the mirror) ranks[p-u].  Per tree and
+ * edge (child c, parent q): a reduce flow c -> q of nbytes/2 after the reduce
+ * flows into c (leaves: after `after`, released `lag` later), and a
+ * broadcast flow q -> c after the broadcast flow into q (q the root: after
+ * every reduce flow into the root).  Layout: tree A reduce (children by
+ * level, lowest first, then node), tree A broadcast (by level, highest
+ * first, then node), tree B reduce, tree B broadcast: 4(p-1) flows.
+ *
+ * netsim_add_hier_allreduce: ranks is an m x g array, row-major (row s: the
+ * g ranks of server s), m*g >= 2.  Phase 1 (g > 1): per server, a chained
+ * ring reduce-scatter over its row, chunks nbytes/g, step-major per server;
+ * phase 2 (m > 1): per column j, a chained ring all-reduce over the m rows,
+ * chunks nbytes/(g*m), 2(m-1) steps, step-major per column; phase 3 (g > 1):
+ * per server a chained ring all-gather like phase 1.  A rank's first step of
+ * a phase waits for its previous phase's last-step flows out of and into
+ * it (the first phase: for `after`, released `lag` later).
+ */
+netsim_status netsim_add_tree_allreduce(netsim_t* h, int32_t scen, int32_t p, const int32_t* ranks,
+                                        double nbytes, double lag, int64_t n_after,
+                                        const int64_t* after, int64_t* first_id, int64_t* count);
+netsim_status netsim_add_hier_allreduce(netsim_t* h, int32_t scen, int32_t m, int32_t g,
+                                        const int32_t* ranks, double nbytes, double lag,
+                                        int64_t n_after, const int64_t* after, int64_t* first_id,
+                                        int64_t* count);
+
+/*
+ * Per-link latency of scenario `scen` (num_links = its link count, values
+ * finite >= 0, copied), replacing what its built-in fabric set.  A flow
+ * sends at its max-min rate as before and frees its links when its last byte
+ * leaves; it finishes (its finish time, and the release base of its
+ * dependants) the sum of its path's latencies later, summed in path order.
+ * NETSIM_E_STATE after the first run.
+ */
+netsim_status netsim_set_link_latency(netsim_t* h, int32_t scen, int64_t num_links,
+                                      const double* latency_s);
+
+/*
  * Event-queue front end (Section 4.1: the simulator's event queue emulates
  * CUDA streams and events -- operations on one stream run in order,
  * operations on different streams are independent unless linked by an
@@ -260,6 +314,16 @@ netsim_status netsim_stream_ring(netsim_t* h, int32_t scen, int32_t kind, int32_
 /* All-to-all of ranks[i] issued on streams[i]; nbytes as netsim_add_all_to_all; done[p]. */
 netsim_status netsim_stream_all_to_all(netsim_t* h, int32_t scen, int32_t p, const int32_t* ranks,
                                        const int64_t* streams, const double* nbytes, int64_t* done);
+/* Tree / hierarchical all-reduce of ranks[i] issued on streams[i] (p = m*g
+ * for the latter, row-major); a rank's completion follows its broadcasts in
+ * and out (tree) or its last phase's last-step flows in and out
+ * (hierarchical); done[p]. */
+netsim_status netsim_stream_tree_allreduce(netsim_t* h, int32_t scen, int32_t p,
+                                           const int32_t* ranks, const int64_t* streams,
+                                           double nbytes, int64_t* done);
+netsim_status netsim_stream_hier_allreduce(netsim_t* h, int32_t scen, int32_t m, int32_t g,
+                                           const int32_t* ranks, const int64_t* streams,
+                                           double nbytes, int64_t* done);
 /* Point-to-point send/recv: src on src_stream, dst on dst_stream (distinct);
  * *done (may be NULL) receives the completion on src_stream (the same flow
  * as dst_stream's new tail). */

@@ -23,8 +23,9 @@ This module writes those rules out as a ``workloads.program.Scenario``:
   rendezvous, then one barrier per rank after the flows that leave or
   enter that rank and finish last -- a chained ring's last step, every step
   of a flat ring, both edges of an aggregated ring, the whole row and column
-  of an all-to-all, the single flow of a send -- which becomes the rank's
-  stream completion.
+  of an all-to-all, the broadcasts into and out of it in both trees of a
+  tree all-reduce, its last phase's last step in a hierarchical all-reduce,
+  the single flow of a send -- which becomes the rank's stream completion.
 
 The scenario then goes through ``oracle.flows.expand`` (decomposition and
 routing) and ``oracle.sim`` (the event loop); nothing here computes a time.
@@ -37,7 +38,7 @@ from typing import Dict, List
 
 import numpy as np
 
-from workloads.program import AllToAll, Barrier, Ring, Scenario, Send
+from workloads.program import AllToAll, Barrier, Hier, Ring, Scenario, Send, Tree
 from workloads.trace import Collective, Compute, SendRecv, StreamWait, Trace
 
 from . import flows as oflows
@@ -72,6 +73,18 @@ def _rank_flows(op: Collective, i: int) -> List[int]:
     raise ValueError(op.mode)
 
 
+def _last_flows_of(op: Collective, positions):
+    """Tree / hierarchical all-reduce: per rank position (row-major), the
+    collective's flows (numbered within it) among its last ones that leave
+    or enter the rank."""
+    ranks = np.asarray(op.ranks)
+    mk = oflows._tree_flows if op.kind == "tree_allreduce" else oflows._hier_flows
+    s, d, _, _, _, exits = mk(ranks.reshape(-1) if op.kind == "tree_allreduce" else ranks,
+                              float(op.nbytes), 0.0, [], 0)
+    flat = ranks.reshape(-1)
+    return [[j for j in exits if s[j] == flat[i] or d[j] == flat[i]] for i in range(positions)]
+
+
 def build(trace: Trace) -> Timeline:
     sc = Scenario(trace.topo)
     tail: Dict[int, int] = {}
@@ -88,7 +101,16 @@ def build(trace: Trace) -> Timeline:
             tail[op.stream] = k
             done.append([k])
             continue
-        if isinstance(op, Collective):
+        if isinstance(op, Collective) and op.kind in ("tree_allreduce", "hier_allreduce"):
+            streams = [int(x) for x in np.ravel(op.streams)]
+            rv = sc.add(Barrier(after=tuple(tail[s] for s in streams if s in tail)))
+            kind = Tree if op.kind == "tree_allreduce" else Hier
+            ranks = np.asarray(op.ranks)
+            c = sc.add(kind(ranks.reshape(-1) if kind is Tree else ranks, float(op.nbytes),
+                            after=(rv,)))
+            per_rank = [tuple((c, j) for j in js)
+                        for js in _last_flows_of(op, len(streams))]
+        elif isinstance(op, Collective):
             streams = [int(x) for x in op.streams]
             rv = sc.add(Barrier(after=tuple(tail[s] for s in streams if s in tail)))
             if op.kind == "all_to_all":
@@ -138,6 +160,11 @@ def _first_flows(sc: Scenario) -> np.ndarray:
         if isinstance(op, Ring):
             p = len(op.ranks)
             counts.append(p if op.mode == "aggregated" else _RING_STEPS[op.kind](p) * p)
+        elif isinstance(op, Tree):
+            counts.append(4 * (len(op.ranks) - 1))
+        elif isinstance(op, Hier):
+            m, g = np.asarray(op.ranks).shape
+            counts.append(2 * m * g * (g - 1) + g * 2 * (m - 1) * m)
         elif isinstance(op, AllToAll):
             p = len(op.ranks)
             counts.append(p * (p - 1))

@@ -85,6 +85,7 @@ struct Params {
   const int32_t* soff;     // [F+1] successor offsets
   const int32_t* succ;     // [nsucc]
   const int64_t* R0;       // [L] capacity in fixed point
+  const double* lat;       // [F] path latency (the sum over its links), or NULL: none
   const uint4* path16;     // [F] path as six 16-bit part-local link ids (0xFFFF =
                            //     none; valid in parts with lds_paths)
   // dynamic flow state

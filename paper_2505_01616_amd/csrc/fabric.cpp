@@ -66,8 +66,20 @@ bool Fabric::init(const netsim_topology& t, std::string* err) {
       return false;
     }
   deg_bps_ = t.degraded_Bps;
+  if (!(t.fabric_latency_s >= 0.0) || !std::isfinite(t.fabric_latency_s) ||
+      !(t.nvlink_latency_s >= 0.0) || !std::isfinite(t.nvlink_latency_s)) {
+    *err = "topology: latencies must be finite and >= 0";
+    return false;
+  }
+  nv_lat_ = t.nvlink_latency_s;
+  fab_lat_ = t.fabric_latency_s;
   key_ = splitmix64(t.ecmp_seed);
   return true;
+}
+
+void Fabric::latencies(std::vector<double>* lat) const {
+  lat->assign((size_t)L_, fab_lat_);
+  for (int64_t l = 0; l < NV_; ++l) (*lat)[(size_t)l] = nv_lat_;
 }
 
 void Fabric::capacities(std::vector<double>* cap) const {

@@ -30,6 +30,8 @@ class Fabric {
   int64_t endpoints() const { return N_; }
   int64_t num_cables() const { return ncab_; }
   void capacities(std::vector<double>* cap) const;
+  // Per link: nvlink latency for intra-server links, fabric latency for cables.
+  void latencies(std::vector<double>* lat) const;
   // Writes the route of src -> dst (src != dst, both in [0, N)) into out[0..6)
   // and returns its length.
   int route(int64_t src, int64_t dst, int32_t* out) const;
@@ -43,6 +45,7 @@ class Fabric {
   int64_t P_ = 0, E_ = 0, A_ = 0, U_ = 0, groups_ = 0, leaves_ = 0, ncab_ = 0, L_ = 0;
   uint64_t key_ = 0;
   double nv_bps_ = 0, nic_bps_ = 0, fab_bps_ = 0, deg_bps_ = 0;
+  double nv_lat_ = 0, fab_lat_ = 0;
   std::vector<int64_t> degraded_;
 };
 

@@ -39,7 +39,6 @@ namespace {
 
 constexpr double THR = 1.000000000001;
 constexpr double INF = __builtin_huge_val();
-constexpr int FAST_DEG = 6;
 constexpr uint64_t BARRIER_TIMEOUT_TICKS = 1000000000ull;  // 10 s at 100 MHz
 
 __device__ __forceinline__ double wave_min(double v) {
@@ -96,13 +95,15 @@ struct BlockG {
   __device__ void amin(uint64_t* p, uint64_t v) {
     __hip_atomic_fetch_min(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   }
+  __device__ void amax(uint64_t* p, uint64_t v) {
+    __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
 };
 
 // Barrier words (uint32 indices into Params::bar, 64-byte lines apart):
 constexpr int BAR_COUNT = 0, BAR_GEN = 1, BAR_ABORT = 16, BAR_REG = 32, BAR_REG_GEN = 33;
 constexpr int BAR_XCD = 64;        // XCD x: arrivals at 64 + 32x, generation at 64 + 32x + 16
-constexpr int BAR_XCD_BLOCKS = 640;  // blocks resident on XCD x
-constexpr int BAR_WORDS = 1024;
+constexpr int BAR_XCD_BLOCKS = 640;  // blocks resident on XCD x (of 1024 words)
 
 __device__ __forceinline__ unsigned xcc_id() {
   return __builtin_amdgcn_s_getreg(6164) & 15u;  // hwreg(HW_REG_XCC_ID, 0, 4)
@@ -252,6 +253,9 @@ struct GridG {
   }
   __device__ void amin(uint64_t* p, uint64_t v) {
     __hip_atomic_fetch_min(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __device__ void amax(uint64_t* p, uint64_t v) {
+    __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 };
 
@@ -1223,14 +1227,15 @@ __device__ __forceinline__ void activate(G& g, const Params& P, LK& lk, Lists* K
   g.store(&K->changed[ib], 1);
 }
 
-// Releases flow h whose last predecessor finished at t (called once per h).
+// Releases flow h at event time t, once its predecessors have all finished,
+// the latest of them at `base` (>= t) (called once per h).
 template <class G, class LK>
 __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, Lists* K, int h, double t,
-                                            int ob, int ib, const Slots& sl, int32_t* pendOut,
-                                            int32_t* arrOut, int32_t* cout, int32_t* coutCnt, int cap,
-                                            int& err) {
-  const double rl = P.start[h] + t;
-  P.base[h] = t;
+                                            double base, int ob, int ib, const Slots& sl,
+                                            int32_t* pendOut, int32_t* arrOut, int32_t* cout,
+                                            int32_t* coutCnt, int cap, int& err) {
+  const double rl = P.start[h] + base;
+  P.base[h] = base;
   P.rel[h] = rl;
   if (rl <= t) {
     if (P.nbytes[h] == 0.0) {
@@ -1370,7 +1375,8 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
         const int f = sl.id[s];
         if (!in_range(f, f0, cap)) { err = 1; continue; }
         const double r = sl.rate[s];
-        P.finish[f] = tn;
+        // the last byte leaves now; it arrives the path latency later
+        P.finish[f] = P.lat ? tn + P.lat[f] : tn;
         g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
         const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
         for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
@@ -1432,37 +1438,54 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       int32_t* cout = comp(q % 3);
       int32_t* coutCnt = &K->comp[q % 3];
       if (tid == 0) g.store(&K->comp[(q + 1) % 3], 0);
-      for (int i0 = w0; i0 < nc; i0 += T) {
-        const int i = i0 + lane_id();
-        int k0 = 0, k1 = 0;
-        if (i < nc) {
-          const int f = cin[i];
-          if (in_range(f, f0, cap)) {
-            k0 = P.soff[f];
-            k1 = P.soff[f + 1];
-          } else {
-            err = 1;
+      // body(f, h) for every (finished flow, successor) pair, once
+      auto for_succ = [&](auto body) {
+        for (int i0 = w0; i0 < nc; i0 += T) {
+          const int i = i0 + lane_id();
+          int f = -1, k0 = 0, k1 = 0;
+          if (i < nc) {
+            f = cin[i];
+            if (in_range(f, f0, cap)) {
+              k0 = P.soff[f];
+              k1 = P.soff[f + 1];
+            } else {
+              err = 1;
+            }
+          }
+          const bool big = k1 - k0 > 8;
+          if (!big)
+            for (int k = k0; k < k1; ++k) body(f, P.succ[k]);
+          uint64_t mask = __ballot(big);
+          while (mask) {
+            const int j = __ffsll((unsigned long long)mask) - 1;
+            mask &= mask - 1;
+            const int a = __shfl(k0, j, 64), z = __shfl(k1, j, 64), fj = __shfl(f, j, 64);
+            for (int k = a + lane_id(); k < z; k += 64) body(fj, P.succ[k]);
           }
         }
-        const bool big = k1 - k0 > 8;
-        if (!big) {
-          for (int k = k0; k < k1; ++k) {
-            const int h = P.succ[k];
-            if (g.add(&P.cnt[h], -1) == 1)
-              release_one(g, P, lk, K, h, t, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, err);
+      };
+      if (P.lat) {
+        // with latency, a dependant starts after the latest arrival among its
+        // predecessors, which need not be the last one to send its last
+        // byte: first every finished flow raises its dependants' base to its
+        // finish, then (after a barrier) the counts drop and releases read it
+        for_succ([&](int f, int h) {
+          g.amax(reinterpret_cast<uint64_t*>(&P.base[h]), (uint64_t)__double_as_longlong(P.finish[f]));
+        });
+        g.sync();
+        for_succ([&](int, int h) {
+          if (g.add(&P.cnt[h], -1) == 1) {
+            const double b = __longlong_as_double((long long)__hip_atomic_load(
+                reinterpret_cast<uint64_t*>(&P.base[h]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+            release_one(g, P, lk, K, h, t, b, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, err);
           }
-        }
-        uint64_t mask = __ballot(big);
-        while (mask) {
-          const int j = __ffsll((unsigned long long)mask) - 1;
-          mask &= mask - 1;
-          const int a = __shfl(k0, j, 64), z = __shfl(k1, j, 64);
-          for (int k = a + lane_id(); k < z; k += 64) {
-            const int h = P.succ[k];
-            if (g.add(&P.cnt[h], -1) == 1)
-              release_one(g, P, lk, K, h, t, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, err);
-          }
-        }
+        });
+      } else {
+        // arrival = last byte: the last predecessor to finish is the latest
+        for_succ([&](int, int h) {
+          if (g.add(&P.cnt[h], -1) == 1)
+            release_one(g, P, lk, K, h, t, t, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, err);
+        });
       }
       if (err) g.store(&K->fault, 2);
       g.sync();

@@ -31,6 +31,7 @@ thread_local std::string g_thread_err;
 
 struct Scen {
   std::vector<double> cap;
+  std::vector<double> lat;     // per link latency in seconds (empty: none)
   bool has_fabric = false;
   netsim_host::Fabric fab;
   std::vector<int64_t> flows;  // ids of this scenario's flows, ascending
@@ -363,13 +364,23 @@ netsim_status prepare(netsim_t* h) {
   std::vector<int32_t> plink((size_t)std::max<int64_t>(h->nnz, 1));
   std::vector<double> nbytes((size_t)std::max<int64_t>(F, 1)), start((size_t)std::max<int64_t>(F, 1));
   std::vector<int32_t> ndeps((size_t)std::max<int64_t>(F, 1), 0);
+  // path latency per flow: the sum of its links' latencies in path order
+  std::vector<double> lat((size_t)std::max<int64_t>(F, 1), 0.0);
+  bool any_lat = false;
   int64_t e = 0;
   for (int64_t d = 0; d < F; ++d) {
     const int64_t id = flow_of_dev[(size_t)d];
     const int32_t s = h->f_scen[(size_t)id];
+    const std::vector<double>& llat = h->scen[(size_t)s].lat;
     poff[(size_t)d] = (int32_t)e;
-    for (int64_t k = h->p_off[(size_t)id]; k < h->p_off[(size_t)id + 1]; ++k)
-      plink[(size_t)e++] = h->dev_link[(size_t)s][(size_t)h->p_link[(size_t)k]];
+    double acc = 0.0;
+    for (int64_t k = h->p_off[(size_t)id]; k < h->p_off[(size_t)id + 1]; ++k) {
+      const int32_t l = h->p_link[(size_t)k];
+      plink[(size_t)e++] = h->dev_link[(size_t)s][(size_t)l];
+      if (!llat.empty()) acc = acc + llat[(size_t)l];
+    }
+    lat[(size_t)d] = acc;
+    any_lat = any_lat || acc != 0.0;
     nbytes[(size_t)d] = h->f_bytes[(size_t)id];
     start[(size_t)d] = h->f_start[(size_t)id];
     ndeps[(size_t)d] = (int32_t)(h->d_off[(size_t)id + 1] - h->d_off[(size_t)id]);
@@ -489,6 +500,7 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.fl, sizeof(uint32_t) * Lz},
       {(void**)&P.path16, 16 * Fz},
       {(void**)&P.stage, 16 * Fz},
+      {(void**)&P.lat, sizeof(double) * Fz},
       {(void**)&P.comp0, sizeof(int32_t) * Fz},
       {(void**)&P.comp1, sizeof(int32_t) * Fz},
       {(void**)&P.comp2, sizeof(int32_t) * Fz},
@@ -524,11 +536,14 @@ netsim_status prepare(netsim_t* h) {
       {R0.data(), P.R0, sizeof(int64_t) * R0.size()},
       {comp_of_dev.data(), P.comp, sizeof(int32_t) * comp_of_dev.size()},
       {path16.data(), P.path16, sizeof(uint16_t) * path16.size()},
+      {lat.data(), P.lat, any_lat ? sizeof(double) * lat.size() : 0},
   };
   for (const Up& u : ups) {
+    if (u.bytes == 0) continue;
     he = hipMemcpy((void*)u.dst, u.src, u.bytes, hipMemcpyHostToDevice);
     if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (upload)");
   }
+  if (!any_lat) P.lat = nullptr;  // no latency anywhere: arrival = last byte
   P.num_scen = NP;
   P.scale = h->scale;
   P.inv_scale = 1.0 / h->scale;
@@ -867,6 +882,7 @@ netsim_status netsim_create_topology(netsim_t** out, int32_t num_scenarios,
     }
     sc.has_fabric = true;
     sc.fab.capacities(&sc.cap);
+    sc.fab.latencies(&sc.lat);
   }
   *out = h;
   return NETSIM_OK;
@@ -966,6 +982,242 @@ netsim_status netsim_add_all_to_all(netsim_t* h, int32_t scen, int32_t p, const 
   if (first_id) *first_id = first;
   if (count) *count = n;
   return NETSIM_OK;
+}
+
+
+netsim_status netsim_set_link_latency(netsim_t* h, int32_t scen, int64_t num_links,
+                                      const double* latency_s) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "set_link_latency: handle is NULL");
+  if (h->prepared) return fail(h, NETSIM_E_STATE, "set_link_latency: latencies cannot change after a run");
+  if (scen < 0 || scen >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "set_link_latency: bad scenario");
+  Scen& sc = h->scen[(size_t)scen];
+  if (num_links != (int64_t)sc.cap.size()) return fail(h, NETSIM_E_INVALID, "set_link_latency: need one value per link");
+  if (num_links > 0 && !latency_s) return fail(h, NETSIM_E_INVALID, "set_link_latency: latency_s is NULL");
+  for (int64_t l = 0; l < num_links; ++l)
+    if (!finite_nonneg(latency_s[l])) return fail(h, NETSIM_E_INVALID, "set_link_latency: latencies must be finite and >= 0");
+  sc.lat.assign(latency_s, latency_s + num_links);
+  return NETSIM_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// In-order binary tree over nodes 1..p: node u of level l = ctz(u) >= 1 has
+// children u - 2^(l-1) and u + 2^j for the largest j < l with u + 2^j <= p.
+int32_t tree_level(int32_t u) { return __builtin_ctz((unsigned)u); }
+
+struct TreeShape {
+  int32_t root = 0;
+  std::vector<int32_t> parent;                  // [p+1], 0 for the root
+  std::vector<std::vector<int32_t>> kids;       // [p+1]
+  std::vector<int32_t> up, down;                // children ordered for reduce / broadcast
+};
+
+TreeShape tree_shape(int32_t p) {
+  TreeShape t;
+  t.parent.assign((size_t)p + 1, 0);
+  t.kids.assign((size_t)p + 1, {});
+  for (int32_t u = 2; u <= p; u += 2) {
+    const int32_t l = tree_level(u);
+    t.kids[(size_t)u].push_back(u - (1 << (l - 1)));
+    for (int32_t j = l - 1; j >= 0; --j)
+      if (u + (1 << j) <= p) {
+        t.kids[(size_t)u].push_back(u + (1 << j));
+        break;
+      }
+  }
+  for (int32_t u = 1; u <= p; ++u)
+    for (int32_t c : t.kids[(size_t)u]) t.parent[(size_t)c] = u;
+  t.root = 1;
+  while (t.root * 2 <= p) t.root *= 2;
+  for (int32_t u = 1; u <= p; ++u)
+    if (u != t.root) t.up.push_back(u);
+  t.down = t.up;
+  // reduce: children before parents (lower level first); broadcast: the reverse
+  std::stable_sort(t.up.begin(), t.up.end(), [](int32_t a, int32_t b) {
+    return tree_level(a) != tree_level(b) ? tree_level(a) < tree_level(b) : a < b;
+  });
+  std::stable_sort(t.down.begin(), t.down.end(), [](int32_t a, int32_t b) {
+    return tree_level(a) != tree_level(b) ? tree_level(a) > tree_level(b) : a < b;
+  });
+  return t;
+}
+
+// Flows of a rank set laid out as appended rows (src, dst, bytes, lag, deps).
+struct FlowRows {
+  std::vector<int32_t> src, dst;
+  std::vector<double> b, t0;
+  std::vector<int64_t> doff{0}, dids;
+  void add(int32_t s, int32_t d, double bytes, double lag, const int64_t* deps, size_t nd) {
+    src.push_back(s);
+    dst.push_back(d);
+    b.push_back(bytes);
+    t0.push_back(lag);
+    dids.insert(dids.end(), deps, deps + nd);
+    doff.push_back((int64_t)dids.size());
+  }
+  int64_t size() const { return (int64_t)b.size(); }
+};
+
+netsim_status commit_rows(netsim_t* h, int32_t scen, const FlowRows& r, int64_t first,
+                          int64_t* first_id, int64_t* count) {
+  netsim_status st = add_flows_impl(h, scen, r.size(), r.src.data(), r.dst.data(), r.b.data(),
+                                    r.t0.data(), nullptr, nullptr, r.doff.data(),
+                                    r.dids.empty() ? nullptr : r.dids.data(), nullptr);
+  if (st) return st;
+  if (first_id) *first_id = first;
+  if (count) *count = r.size();
+  return NETSIM_OK;
+}
+
+// Per tree (A: position u-1 at node u; B: position p-u), reduce flows then
+// broadcast flows; rank i's completion flows (the broadcasts into and out
+// of it in both trees) go to done_of[i] when given.
+void tree_rows(int32_t p, const int32_t* ranks, double nbytes, double lag, int64_t n_after,
+               const int64_t* after, int64_t first, FlowRows* r,
+               std::vector<std::vector<int64_t>>* done_of) {
+  const TreeShape t = tree_shape(p);
+  std::vector<int64_t> rslot((size_t)p + 1), bslot((size_t)p + 1);
+  for (size_t k = 0; k < t.up.size(); ++k) rslot[(size_t)t.up[k]] = (int64_t)k;
+  for (size_t k = 0; k < t.down.size(); ++k) bslot[(size_t)t.down[k]] = (int64_t)k;
+  const double half = nbytes / 2.0;
+  for (int32_t tr = 0; tr < 2; ++tr) {
+    auto pos = [&](int32_t u) { return tr == 0 ? u - 1 : p - u; };
+    const int64_t red0 = first + (int64_t)tr * 2 * (p - 1);
+    const int64_t bc0 = red0 + (p - 1);
+    for (int32_t c : t.up) {
+      std::vector<int64_t> into;
+      for (int32_t x : t.kids[(size_t)c]) into.push_back(red0 + rslot[(size_t)x]);
+      if (into.empty())
+        r->add(ranks[pos(c)], ranks[pos(t.parent[(size_t)c])], half, lag, after, (size_t)n_after);
+      else
+        r->add(ranks[pos(c)], ranks[pos(t.parent[(size_t)c])], half, 0.0, into.data(), into.size());
+    }
+    for (int32_t c : t.down) {
+      const int32_t q = t.parent[(size_t)c];
+      std::vector<int64_t> dep;
+      if (q == t.root)
+        for (int32_t x : t.kids[(size_t)q]) dep.push_back(red0 + rslot[(size_t)x]);
+      else
+        dep.push_back(bc0 + bslot[(size_t)q]);
+      r->add(ranks[pos(q)], ranks[pos(c)], half, 0.0, dep.data(), dep.size());
+      if (done_of) {
+        const int64_t f = bc0 + bslot[(size_t)c];
+        (*done_of)[(size_t)pos(q)].push_back(f);
+        (*done_of)[(size_t)pos(c)].push_back(f);
+      }
+    }
+  }
+}
+
+// Hierarchical all-reduce over an m x g rank array (row = server): per
+// server a chained ring reduce-scatter (chunks S/g), per local position a
+// chained ring all-reduce across the servers (chunks S/(g m)), per server a
+// chained ring all-gather (chunks S/g); a rank's first step of a phase waits
+// for its previous phase's last-step flows out of and into it.  done_of
+// (row-major rank index) receives each rank's last-phase flows.
+void hier_rows(int32_t m, int32_t g, const int32_t* R, double nbytes, double lag, int64_t n_after,
+               const int64_t* after, int64_t first, FlowRows* r,
+               std::vector<std::vector<int64_t>>* done_of) {
+  std::vector<std::vector<int64_t>> done((size_t)m * g);  // previous phase, per rank
+  bool started = false;
+  auto rk = [&](int32_t a, int32_t i) { return R[(size_t)a * g + i]; };
+  auto entry = [&](int32_t a, int32_t i, double bytes, int32_t s, int32_t d) {
+    if (started)
+      r->add(s, d, bytes, 0.0, done[(size_t)a * g + i].data(), done[(size_t)a * g + i].size());
+    else
+      r->add(s, d, bytes, lag, after, (size_t)n_after);
+  };
+  int64_t next = first;
+  auto server_rings = [&]() {
+    std::vector<std::vector<int64_t>> nd((size_t)m * g);
+    for (int32_t a = 0; a < m; ++a) {
+      const int64_t base = next;
+      for (int32_t k = 0; k < g - 1; ++k)
+        for (int32_t i = 0; i < g; ++i) {
+          if (k == 0) {
+            entry(a, i, nbytes / (double)g, rk(a, i), rk(a, (i + 1) % g));
+          } else {
+            const int64_t prev = base + (int64_t)(k - 1) * g + (i + g - 1) % g;
+            r->add(rk(a, i), rk(a, (i + 1) % g), nbytes / (double)g, 0.0, &prev, 1);
+          }
+        }
+      const int64_t last = base + (int64_t)(g - 2) * g;
+      for (int32_t i = 0; i < g; ++i) nd[(size_t)a * g + i] = {last + i, last + (i + g - 1) % g};
+      next += (int64_t)(g - 1) * g;
+    }
+    done.swap(nd);
+    started = true;
+  };
+  if (g > 1) server_rings();
+  if (m > 1) {
+    std::vector<std::vector<int64_t>> nd((size_t)m * g);
+    const int32_t steps = 2 * (m - 1);
+    const double chunk = nbytes / ((double)g * (double)m);
+    for (int32_t j = 0; j < g; ++j) {
+      const int64_t base = next;
+      for (int32_t k = 0; k < steps; ++k)
+        for (int32_t a = 0; a < m; ++a) {
+          if (k == 0) {
+            entry(a, j, chunk, rk(a, j), rk((a + 1) % m, j));
+          } else {
+            const int64_t prev = base + (int64_t)(k - 1) * m + (a + m - 1) % m;
+            r->add(rk(a, j), rk((a + 1) % m, j), chunk, 0.0, &prev, 1);
+          }
+        }
+      const int64_t last = base + (int64_t)(steps - 1) * m;
+      for (int32_t a = 0; a < m; ++a) nd[(size_t)a * g + j] = {last + a, last + (a + m - 1) % m};
+      next += (int64_t)steps * m;
+    }
+    done.swap(nd);
+    started = true;
+  }
+  if (g > 1) server_rings();
+  if (done_of) *done_of = done;
+}
+
+netsim_status check_tree_args(netsim_t* h, const char* what, int32_t scen, int32_t p,
+                              const int32_t* ranks, double nbytes, double lag, int64_t n_after,
+                              const int64_t* after) {
+  if (h->prepared) return fail(h, NETSIM_E_STATE, std::string(what) + ": flows cannot be added after a run");
+  if (p < 2) return fail(h, NETSIM_E_INVALID, std::string(what) + ": need at least 2 ranks");
+  if (!finite_nonneg(nbytes) || !finite_nonneg(lag))
+    return fail(h, NETSIM_E_INVALID, std::string(what) + ": bytes and lag must be finite and >= 0");
+  netsim_status st = check_ranks(h, scen, p, ranks);
+  if (st) return st;
+  return check_after(h, scen, n_after, after);
+}
+
+}  // namespace
+
+extern "C" {
+
+netsim_status netsim_add_tree_allreduce(netsim_t* h, int32_t scen, int32_t p, const int32_t* ranks,
+                                        double nbytes, double lag, int64_t n_after,
+                                        const int64_t* after, int64_t* first_id, int64_t* count) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "add_tree_allreduce: handle is NULL");
+  netsim_status st = check_tree_args(h, "add_tree_allreduce", scen, p, ranks, nbytes, lag, n_after, after);
+  if (st) return st;
+  const int64_t first = (int64_t)h->f_bytes.size();
+  FlowRows r;
+  tree_rows(p, ranks, nbytes, lag, n_after, after, first, &r, nullptr);
+  return commit_rows(h, scen, r, first, first_id, count);
+}
+
+netsim_status netsim_add_hier_allreduce(netsim_t* h, int32_t scen, int32_t m, int32_t g,
+                                        const int32_t* ranks, double nbytes, double lag,
+                                        int64_t n_after, const int64_t* after, int64_t* first_id,
+                                        int64_t* count) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "add_hier_allreduce: handle is NULL");
+  if (m < 1 || g < 1 || (int64_t)m * g > std::numeric_limits<int32_t>::max())
+    return fail(h, NETSIM_E_INVALID, "add_hier_allreduce: bad m x g");
+  netsim_status st = check_tree_args(h, "add_hier_allreduce", scen, m * g, ranks, nbytes, lag, n_after, after);
+  if (st) return st;
+  const int64_t first = (int64_t)h->f_bytes.size();
+  FlowRows r;
+  hier_rows(m, g, ranks, nbytes, lag, n_after, after, first, &r, nullptr);
+  return commit_rows(h, scen, r, first, first_id, count);
 }
 
 }  // extern "C"
@@ -1155,6 +1407,48 @@ netsim_status netsim_stream_send(netsim_t* h, int32_t scen, int32_t src, int64_t
   if (st) return st;
   if (done) *done = d2[0];
   return NETSIM_OK;
+}
+
+netsim_status netsim_stream_tree_allreduce(netsim_t* h, int32_t scen, int32_t p,
+                                           const int32_t* ranks, const int64_t* streams,
+                                           double nbytes, int64_t* done) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "stream_tree_allreduce: handle is NULL");
+  netsim_status st = check_stream_scen(h, scen);
+  if (st) return st;
+  if (p < 2) return fail(h, NETSIM_E_INVALID, "stream_tree_allreduce: need p >= 2");
+  std::vector<std::vector<int64_t>> per_rank;
+  return stream_collective(
+      h, scen, p, streams, done,
+      [&](int64_t rv, int64_t* first) {
+        netsim_status s2 = netsim_add_tree_allreduce(h, scen, p, ranks, nbytes, 0.0, 1, &rv, first, nullptr);
+        if (s2) return s2;
+        FlowRows scratch;
+        per_rank.assign((size_t)p, {});
+        tree_rows(p, ranks, nbytes, 0.0, 1, &rv, *first, &scratch, &per_rank);
+        return (netsim_status)NETSIM_OK;
+      },
+      [&](int64_t, int32_t i) { return per_rank[(size_t)i]; });
+}
+
+netsim_status netsim_stream_hier_allreduce(netsim_t* h, int32_t scen, int32_t m, int32_t g,
+                                           const int32_t* ranks, const int64_t* streams,
+                                           double nbytes, int64_t* done) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "stream_hier_allreduce: handle is NULL");
+  netsim_status st = check_stream_scen(h, scen);
+  if (st) return st;
+  if (m < 1 || g < 1 || (int64_t)m * g < 2 || (int64_t)m * g > std::numeric_limits<int32_t>::max())
+    return fail(h, NETSIM_E_INVALID, "stream_hier_allreduce: bad m x g");
+  std::vector<std::vector<int64_t>> per_rank;
+  return stream_collective(
+      h, scen, m * g, streams, done,
+      [&](int64_t rv, int64_t* first) {
+        netsim_status s2 = netsim_add_hier_allreduce(h, scen, m, g, ranks, nbytes, 0.0, 1, &rv, first, nullptr);
+        if (s2) return s2;
+        FlowRows scratch;
+        hier_rows(m, g, ranks, nbytes, 0.0, 1, &rv, *first, &scratch, &per_rank);
+        return (netsim_status)NETSIM_OK;
+      },
+      [&](int64_t, int32_t i) { return per_rank[(size_t)i]; });
 }
 
 netsim_status netsim_counts(const netsim_t* h, int64_t* num_flows, int64_t* num_incidences,

@@ -47,7 +47,8 @@ class netsim_topology(ctypes.Structure):
                 ("fabric_Bps", ctypes.c_double), ("ecmp_seed", ctypes.c_uint64),
                 ("num_degraded", ctypes.c_int64),
                 ("degraded_cables", ctypes.POINTER(ctypes.c_int64)),
-                ("degraded_Bps", ctypes.c_double)]
+                ("degraded_Bps", ctypes.c_double),
+                ("fabric_latency_s", ctypes.c_double), ("nvlink_latency_s", ctypes.c_double)]
 
 
 class netsim_stats(ctypes.Structure):
@@ -89,6 +90,13 @@ _SIGS = {
                                ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
     "netsim_add_all_to_all": (_I32, [_H, _I32, _I32, _P, _P, _D, _I64, _P,
                                      ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
+    "netsim_add_tree_allreduce": (_I32, [_H, _I32, _I32, _P, _D, _D, _I64, _P,
+                                         ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
+    "netsim_add_hier_allreduce": (_I32, [_H, _I32, _I32, _I32, _P, _D, _D, _I64, _P,
+                                         ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
+    "netsim_set_link_latency": (_I32, [_H, _I32, _I64, _P]),
+    "netsim_stream_tree_allreduce": (_I32, [_H, _I32, _I32, _P, _P, _D, _P]),
+    "netsim_stream_hier_allreduce": (_I32, [_H, _I32, _I32, _I32, _P, _P, _D, _P]),
     "netsim_counts": (_I32, [_H, ctypes.POINTER(_I64), ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
     "netsim_export_flows": (_I32, [_H, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "netsim_set_limits": (_I32, [_H, _I64, _D]),
@@ -218,6 +226,36 @@ def netsim_add_ring(h, scen, kind, mode, ranks, nbytes, lag=0.0, after=()):
     return first.value, count.value
 
 
+def netsim_add_tree_allreduce(h, scen, ranks, nbytes, lag=0.0, after=()):
+    lib = load_library()
+    r = _arr(ranks, np.int32)
+    a = _arr(np.asarray(after, dtype=np.int64), np.int64)
+    first, count = _I64(-1), _I64(0)
+    _check(h, lib.netsim_add_tree_allreduce(h, scen, len(r), _ptr(r), float(nbytes), float(lag),
+                                            len(a), _ptr(a) if len(a) else None,
+                                            ctypes.byref(first), ctypes.byref(count)))
+    return first.value, count.value
+
+
+def netsim_add_hier_allreduce(h, scen, ranks, nbytes, lag=0.0, after=()):
+    """ranks: an m x g array (row = server)."""
+    lib = load_library()
+    r2 = np.asarray(ranks)
+    m, g = r2.shape
+    r = _arr(r2.reshape(-1), np.int32)
+    a = _arr(np.asarray(after, dtype=np.int64), np.int64)
+    first, count = _I64(-1), _I64(0)
+    _check(h, lib.netsim_add_hier_allreduce(h, scen, m, g, _ptr(r), float(nbytes), float(lag),
+                                            len(a), _ptr(a) if len(a) else None,
+                                            ctypes.byref(first), ctypes.byref(count)))
+    return first.value, count.value
+
+
+def netsim_set_link_latency(h, scen, latency_s):
+    lat = _arr(latency_s, np.float64)
+    _check(h, load_library().netsim_set_link_latency(h, scen, len(lat), _ptr(lat) if len(lat) else None))
+
+
 def netsim_add_all_to_all(h, scen, ranks, nbytes, lag=0.0, after=()):
     lib = load_library()
     r = _arr(ranks, np.int32)
@@ -338,6 +376,27 @@ def netsim_stream_all_to_all(h, scen, ranks, streams, nbytes) -> np.ndarray:
     done = np.zeros(len(r), np.int64)
     _check(h, load_library().netsim_stream_all_to_all(h, scen, len(r), _ptr(r), _ptr(st), _ptr(b),
                                                       _ptr(done)))
+    return done
+
+
+def netsim_stream_tree_allreduce(h, scen, ranks, streams, nbytes) -> np.ndarray:
+    r = _arr(ranks, np.int32)
+    st = _arr(streams, np.int64)
+    done = np.zeros(len(r), np.int64)
+    _check(h, load_library().netsim_stream_tree_allreduce(h, scen, len(r), _ptr(r), _ptr(st),
+                                                          float(nbytes), _ptr(done)))
+    return done
+
+
+def netsim_stream_hier_allreduce(h, scen, ranks, streams, nbytes) -> np.ndarray:
+    """ranks: m x g (row = server); streams in the same row-major order."""
+    r2 = np.asarray(ranks)
+    m, g = r2.shape
+    r = _arr(r2.reshape(-1), np.int32)
+    st = _arr(np.asarray(streams).reshape(-1), np.int64)
+    done = np.zeros(len(r), np.int64)
+    _check(h, load_library().netsim_stream_hier_allreduce(h, scen, m, g, _ptr(r), _ptr(st),
+                                                          float(nbytes), _ptr(done)))
     return done
 
 

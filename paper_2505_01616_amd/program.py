@@ -1,8 +1,10 @@
 """Feeds a workload description into a libnetsim handle.
 
 Marshalling only: topology parameters become ``netsim_topology`` structs,
-ring and all-to-all operations become ``netsim_add_ring`` /
-``netsim_add_all_to_all`` calls (the library decomposes and routes them),
+ring, all-to-all, tree and hierarchical all-reduce operations become
+``netsim_add_ring`` / ``netsim_add_all_to_all`` / ``netsim_add_tree_allreduce``
+/ ``netsim_add_hier_allreduce`` calls (the library decomposes and routes
+them), link latencies ``netsim_topology`` fields or ``netsim_set_link_latency``,
 and point-to-point sends, barriers and explicit-path flows are batched into
 ``netsim_add_flows`` calls.  The description objects are duck-typed (any
 object with the attributes of ``workloads.program``).
@@ -40,6 +42,8 @@ def topology_struct(t, keep: list) -> ns.netsim_topology:
     if len(deg):
         d.degraded_cables = deg.ctypes.data_as(ns.ctypes.POINTER(ns.ctypes.c_int64))
     d.degraded_Bps = t.degraded_Bps
+    d.fabric_latency_s = float(getattr(t, "fabric_latency_s", 0.0))
+    d.nvlink_latency_s = float(getattr(t, "nvlink_latency_s", 0.0))
     return d
 
 
@@ -104,6 +108,9 @@ def load_program(program, opt: ns.netsim_options = None) -> Loaded:
         off = np.zeros(len(scs) + 1, np.int64)
         np.cumsum([len(c) for c in caps], out=off[1:])
         h = ns.netsim_create(off, np.concatenate(caps), opt)
+        for s, sc in enumerate(scs):
+            if getattr(sc.topo, "latencies", None) is not None:
+                ns.netsim_set_link_latency(h, s, sc.topo.latencies)
     else:
         h = ns.netsim_create_topology([topology_struct(sc.topo, keep) for sc in scs], opt)
     first_flow, nflows = [], []
@@ -148,6 +155,24 @@ def load_program(program, opt: ns.netsim_options = None) -> Loaded:
                     first, n = ns.netsim_add_all_to_all(h, s, op.ranks, op.nbytes, op.lag, after)
                     firsts.append(first)
                     exits.append(list(range(first, first + n)))
+                elif name == "Tree":
+                    p = len(op.ranks)
+                    first, n = ns.netsim_add_tree_allreduce(h, s, op.ranks, op.nbytes, op.lag, after)
+                    firsts.append(first)
+                    exits.append(list(range(first + (p - 1), first + 2 * (p - 1)))
+                                 + list(range(first + 3 * (p - 1), first + n)))
+                elif name == "Hier":
+                    m, g = np.asarray(op.ranks).shape
+                    first, n = ns.netsim_add_hier_allreduce(h, s, op.ranks, op.nbytes, op.lag, after)
+                    firsts.append(first)
+                    # the last step of the last phase: per server (the all-gather),
+                    # or, with one rank per server, the cross-server ring's
+                    if g > 1:
+                        p3 = first + n - m * (g - 1) * g
+                        exits.append([p3 + a * (g - 1) * g + (g - 2) * g + i
+                                      for a in range(m) for i in range(g)])
+                    else:
+                        exits.append(list(range(first + n - m, first + n)))
                 else:
                     raise TypeError(f"unknown operation {name}")
                 next_id = first + n

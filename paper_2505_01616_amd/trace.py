@@ -48,6 +48,12 @@ def load_trace(trace, opt: ns.netsim_options = None) -> LoadedTrace:
                 ns.netsim_stream_wait(h, 0, op.stream, wait)
                 done.append(np.array([ns.netsim_stream_tail(h, 0, op.stream)]))
                 seen.add(int(op.stream))
+            elif name == "Collective" and op.kind == "tree_allreduce":
+                done.append(ns.netsim_stream_tree_allreduce(h, 0, op.ranks, op.streams, op.nbytes))
+                seen.update(int(s) for s in op.streams)
+            elif name == "Collective" and op.kind == "hier_allreduce":
+                done.append(ns.netsim_stream_hier_allreduce(h, 0, op.ranks, op.streams, op.nbytes))
+                seen.update(int(s) for s in np.ravel(op.streams))
             elif name == "Collective":
                 if op.kind == "all_to_all":
                     d = ns.netsim_stream_all_to_all(h, 0, op.ranks, op.streams, op.nbytes)

@@ -43,11 +43,14 @@ class StreamWait:
 
 @dataclass
 class Collective:
-    kind: str                       # "allreduce" | "reduce_scatter" | "all_gather" | "all_to_all"
+    # "allreduce" | "reduce_scatter" | "all_gather" (rings), "all_to_all",
+    # "tree_allreduce" (double binary tree), "hier_allreduce" (ranks and
+    # streams m x g, row = server)
+    kind: str
     ranks: np.ndarray
-    streams: np.ndarray             # the stream each rank issues it on
-    nbytes: Union[float, np.ndarray]  # total bytes (rings); p x p matrix (all_to_all)
-    mode: str = "chained"
+    streams: np.ndarray             # the stream each rank issues it on (same shape)
+    nbytes: Union[float, np.ndarray]  # total bytes; p x p matrix for all_to_all
+    mode: str = "chained"           # rings only
 
 
 @dataclass
@@ -73,8 +76,9 @@ class Trace:
             if not (0 <= k < len(self.ops)) or not (0 <= j < positions(self.ops[k])):
                 raise ValueError("a wait must name an earlier operation and one of its streams")
         if isinstance(op, Collective):
-            if len(op.ranks) < 2 or len(op.streams) != len(op.ranks) \
-                    or len(set(int(x) for x in op.streams)) != len(op.streams):
+            n = np.size(op.ranks)
+            if n < 2 or np.shape(op.streams) != np.shape(op.ranks) \
+                    or len(set(int(x) for x in np.ravel(op.streams))) != n:
                 raise ValueError("a collective needs p >= 2 ranks on p distinct streams")
         if isinstance(op, SendRecv) and (op.src == op.dst or op.src_stream == op.dst_stream):
             raise ValueError("a send/recv joins two ranks on two streams")
@@ -85,7 +89,7 @@ class Trace:
 def positions(op: TraceOp) -> int:
     """Number of streams an operation completes on."""
     if isinstance(op, Collective):
-        return len(op.ranks)
+        return int(np.size(op.ranks))
     return 2 if isinstance(op, SendRecv) else 1
 
 
@@ -93,7 +97,8 @@ def training_step(seed: int = 6, tp: int = 8, pp: int = 4, dp: int = 4, microbat
                   layers: int = 4, fwd_s: float = 1.2e-3, bwd_s: float = 2.4e-3,
                   tp_bytes: float = 16 * MiB, act_bytes: float = 32 * MiB,
                   grad_bytes: float = 512 * MiB, optim_s: float = 0.5e-3,
-                  jitter: float = 0.1) -> Trace:
+                  jitter: float = 0.1, allreduce: str = "ring", fabric_latency_s: float = 0.0,
+                  nvlink_latency_s: float = 0.0) -> Trace:
     """One 3D-parallel (TP x PP x DP) training step with a GPipe schedule.
 
     Rank ``t + tp*(d + dp*s)`` is tensor position t of data-parallel replica
@@ -114,13 +119,17 @@ def training_step(seed: int = 6, tp: int = 8, pp: int = 4, dp: int = 4, microbat
     backward, and an optimizer computation on the compute stream after it.
     Computation times are the per-layer times with a seeded multiplicative
     jitter uniform in [1 - jitter, 1 + jitter].  Fabric: rail-optimised,
-    one leaf per rail, 400 Gb/s NICs and switch cables, eight spines.
+    one leaf per rail, 400 Gb/s NICs and switch cables, eight spines, with
+    the given link latencies.  ``allreduce`` picks the algorithm of every
+    all-reduce: "ring" (chained) or "tree" (double binary tree).
     """
     nranks = tp * pp * dp
     servers = max(1, -(-nranks // 8))
     topo = Topology(kind="rail", servers=servers, gpus_per_server=8, servers_per_leaf=servers,
                     spines=8, nvlink_Bps=900e9, nic_Bps=gbit(400), fabric_Bps=gbit(400),
-                    ecmp_seed=int(Stream(seed, "trace-ecmp").u64(1)[0]))
+                    ecmp_seed=int(Stream(seed, "trace-ecmp").u64(1)[0]),
+                    fabric_latency_s=fabric_latency_s, nvlink_latency_s=nvlink_latency_s)
+    ar = "allreduce" if allreduce == "ring" else "tree_allreduce"
     tr = Trace(f"training step tp{tp} pp{pp} dp{dp} mb{microbatches}", topo)
     draws = Stream(seed, "trace-jitter")
     nd = [0]
@@ -150,8 +159,7 @@ def training_step(seed: int = 6, tp: int = 8, pp: int = 4, dp: int = 4, microbat
             for r in ranks:
                 last[int(r)] = (tr.add(Compute(comp(r), jittered(per_layer))), 0)
             if tp > 1:
-                k = tr.add(Collective("allreduce", ranks, np.array([comp(r) for r in ranks]),
-                                      tp_bytes))
+                k = tr.add(Collective(ar, ranks, np.array([comp(r) for r in ranks]), tp_bytes))
                 for t, r in enumerate(ranks):
                     last[int(r)] = (k, t)
         return ranks
@@ -183,8 +191,7 @@ def training_step(seed: int = 6, tp: int = 8, pp: int = 4, dp: int = 4, microbat
             if dp > 1:
                 for r in ranks:
                     tr.add(StreamWait(comm(r), [last[int(r)]]))
-                k = tr.add(Collective("allreduce", ranks, np.array([comm(r) for r in ranks]),
-                                      grad_bytes))
+                k = tr.add(Collective(ar, ranks, np.array([comm(r) for r in ranks]), grad_bytes))
                 for i, r in enumerate(ranks):
                     last[int(r)] = (tr.add(Compute(comp(r), jittered(optim_s), wait=[(k, i)])), 0)
             else:
