@@ -939,23 +939,18 @@ __device__ __forceinline__ int solve_mask(BlockG& g, const Params& P, LK& lk, Sc
       bool frozen = false;
       double mv;
       if constexpr (LK::kTable) {
-        uint32_t sp[6];
-#pragma unroll
-        for (int j = 0; j < 6; ++j) {
-          lv[j] = min(lv[j], lsent);
-          sp[j] = lk.stamp(lv[j]);
-        }
-#pragma unroll
-        for (int j = 0; j < 6; ++j) frozen |= ((cm >> j) & 1u) && sp[j] != st;
-        if (!frozen) return;
-        // the smallest share is at one of the links at the minimum
-        double sv[6];
-#pragma unroll
-        for (int j = 0; j < 6; ++j) sv[j] = lk.table(lv[j]);
+        // only the links at the flow's minimum (usually one): a stamp tells
+        // whether it is blocked, the table the share it freezes at
         mv = INF;
-#pragma unroll
-        for (int j = 0; j < 6; ++j)
-          if ((cm >> j) & 1u) mv = sv[j] < mv ? sv[j] : mv;
+        for (uint32_t rest = cm; rest; rest &= rest - 1) {
+          const int j = __ffs(rest) - 1;
+          const int l = j == 0 ? lv[0] : j == 1 ? lv[1] : j == 2 ? lv[2]
+                      : j == 3 ? lv[3] : j == 4 ? lv[4] : lv[5];
+          frozen |= lk.stamp(l) != st;
+          const double sv = lk.table(l);
+          mv = sv < mv ? sv : mv;
+        }
+        if (!frozen) return;
       } else {
 #pragma unroll
         for (int j = 0; j < 6; ++j)
