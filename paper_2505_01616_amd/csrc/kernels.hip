@@ -1330,11 +1330,18 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       g.store(&K->sel, 0);
       g.store(&K->slots2, 0);
     }
-    // next event time: earliest predicted completion or release
+    // next event time: earliest predicted completion or release (four
+    // slots of a thread in flight at a time)
     double mine = INF;
-    for (int s = tid; s < nSlots; s += T) {
-      const double v = sl.tau[s];
-      mine = v < mine ? v : mine;
+    for (int s0 = tid; s0 < nSlots; s0 += 4 * T) {
+      double v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int s = s0 + u * T;
+        v[u] = s < nSlots ? sl.tau[s] : INF;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) mine = v[u] < mine ? v[u] : mine;
     }
     double loc = mine;
     for (int i = tid; i < nPend; i += T) {
@@ -1365,27 +1372,38 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     int err = 0;
     // completions: only threads holding a slot that is due look again
     if (mine <= thr) {
-      for (int s = tid; s < nSlots; s += T) {
-        if (!(sl.tau[s] <= thr)) continue;
-        const int f = sl.id[s];
-        if (!in_range(f, f0, cap)) { err = 1; continue; }
-        const double r = sl.rate[s];
-        // the last byte leaves now; it arrives the path latency later
-        P.finish[f] = P.lat ? tn + P.lat[f] : tn;
-        g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
-        const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
-        for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
-          const int l = P.plink[k];
-          lk.addNact(g, l, -1);
-          lk.addR(g, l, qv);  // its share returns to the link
+      // only threads holding a due slot look again, four slots in flight
+      for (int s0 = tid; s0 < nSlots; s0 += 4 * T) {
+        double v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int s = s0 + u * T;
+          v[u] = s < nSlots ? sl.tau[s] : INF;
         }
-        if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
-        g.store(&K->changed[ib], 1);
-        sl.id[s] = -1;
-        sl.tau[s] = INF;
-        g.add(&K->holes, 1);
-        const int c = g.add(compCnt, 1);
-        if (c < cap) compOut[c] = f; else err = 1;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int s = s0 + u * T;
+          if (!(v[u] <= thr)) continue;
+          const int f = sl.id[s];
+          if (!in_range(f, f0, cap)) { err = 1; continue; }
+          const double r = sl.rate[s];
+          // the last byte leaves now; it arrives the path latency later
+          P.finish[f] = P.lat ? tn + P.lat[f] : tn;
+          g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
+          const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
+          for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+            const int l = P.plink[k];
+            lk.addNact(g, l, -1);
+            lk.addR(g, l, qv);  // its share returns to the link
+          }
+          if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
+          g.store(&K->changed[ib], 1);
+          sl.id[s] = -1;
+          sl.tau[s] = INF;
+          g.add(&K->holes, 1);
+          const int c = g.add(compCnt, 1);
+          if (c < cap) compOut[c] = f; else err = 1;
+        }
       }
     }
     // releases due now
