@@ -25,8 +25,8 @@
 // scale), so the per-link sums are order independent and every run is
 // deterministic.
 //
-// The same code runs over a "group" of threads: one workgroup per scenario
-// (BlockG, workgroup barriers) or the whole grid on one scenario at a time
+// The same code runs over a "group" of threads: one workgroup per part of a
+// scenario (BlockG, workgroup barriers) or the whole grid on one part at a time
 // (GridG, an atomic grid barrier with a time-out).  Every loop exit depends
 // only on values read after a group barrier, so all waves leave together.
 #include "device.h"
