@@ -59,7 +59,7 @@ enum { NETSIM_RING_ALLREDUCE = 0, NETSIM_RING_REDUCE_SCATTER = 1, NETSIM_RING_AL
 enum { NETSIM_MODE_CHAINED = 0, NETSIM_MODE_FLAT = 1, NETSIM_MODE_AGGREGATED = 2 };
 /* Execution layout (netsim_options.exec). */
 enum {
-  NETSIM_EXEC_AUTO = 0,  /* block per part when there are several or it is small, else grid */
+  NETSIM_EXEC_AUTO = 0,  /* grid for a single part with > 65536 flows without predecessors, else block */
   NETSIM_EXEC_GRID = 1,  /* whole GPU on one part at a time (grid barriers)      */
   NETSIM_EXEC_BLOCK = 2  /* one workgroup per part (workgroup barriers)          */
 };
@@ -80,7 +80,9 @@ typedef struct {
   int64_t max_events;        /* stop each part after this many events; 0 = no limit */
   double until;              /* do not process events later than this time (s); +inf = none */
   int32_t max_rounds;        /* per-solve round watchdog; 0 = number of flows + 1 */
-  int32_t block_threads;     /* threads per workgroup in block mode; 0 = 1024    */
+  int32_t block_threads;     /* threads per workgroup in block mode; 0 = 1024 if
+                                a part has > 16384 flows without predecessors,
+                                else 512                                        */
   int32_t debug;             /* bit 0: consistency checks on the device; bit 1:
                                 phase timers (netsim_stats.phase_seconds)        */
   int32_t single_clock;      /* 1: one part (one clock) per scenario             */

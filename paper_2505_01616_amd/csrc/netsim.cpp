@@ -601,7 +601,16 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
                                        : (int32_t)std::min<int64_t>(h->F + 1, std::numeric_limits<int32_t>::max());
   const int32_t S = h->num_parts;
   int exec = h->opt.exec;
-  if (exec == NETSIM_EXEC_AUTO) exec = (S > 1 || h->F < 100000) ? NETSIM_EXEC_BLOCK : NETSIM_EXEC_GRID;
+  if (exec == NETSIM_EXEC_AUTO) {
+    // the whole GPU on one part only when its first solve alone exceeds
+    // what one workgroup solves in shared memory: more than 64 x 1024 flows
+    // without predecessors (a part whose flows chain through dependencies
+    // keeps few of them active at once, however many it has)
+    int64_t roots = 0;
+    if (S == 1)
+      for (int32_t c : h->h_cnt0) roots += c == 0;
+    exec = (S == 1 && roots > 65536) ? NETSIM_EXEC_GRID : NETSIM_EXEC_BLOCK;
+  }
   // grid-barrier words and min-reduction slots start fresh in every launch
   // (a launch that continues a run must not see the last launch's counts)
   uint64_t inf_slots[8];
@@ -627,7 +636,17 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
         he = netsim_dev::launch_grid(P, blocks, threads, st);
       }
     } else {
-      int threads = h->opt.block_threads > 0 ? h->opt.block_threads : 1024;
+      // 1024 threads when some part starts with more than 16384 flows
+      // without predecessors (its solves may need more than the 64 x 512
+      // items one 512-thread workgroup solves in shared memory); otherwise
+      // 512, which spills no registers and has cheaper barriers
+      int64_t widest = 0;
+      for (const ScenCtl& c : h->h_ctl0) {
+        int64_t roots = 0;
+        for (int32_t d = c.f0; d < c.f1; ++d) roots += h->h_cnt0[(size_t)d] == 0;
+        widest = std::max(widest, roots);
+      }
+      int threads = h->opt.block_threads > 0 ? h->opt.block_threads : widest > 16384 ? 1024 : 512;
       threads = std::max(64, std::min(1024, threads / 64 * 64));
       const int blocks = std::max(1, std::min<int32_t>(S, 1 << 20));
       he = netsim_dev::launch_block(P, blocks, threads, st);
