@@ -142,7 +142,7 @@ def main():
                     help="measure time rollback on the same workload instead (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build runs the whole simulated cluster "
+        print("bench.py measures one GPU only: the simulator runs the whole simulated cluster "
               "on a single MI355X (no multi-GPU path); use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
