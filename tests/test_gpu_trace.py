@@ -104,3 +104,39 @@ def test_stream_calls_after_a_run_are_refused():
         assert e.value.status == ns.E_STATE
     finally:
         ld.close()
+
+
+@pytest.mark.parametrize("exec_", ["block", "grid"])
+def test_compute_duration_change_rolls_back(exec_):
+    """A computation found longer than assumed after the simulation passed it
+    (the situation time rollback exists for): its flow's start (the
+    duration) is updated, the simulation goes back and continues; the result
+    equals, bit for bit, a run of the trace with the right duration from the
+    start, and the oracle's timeline of that trace."""
+    import copy
+    ns, ptr = _gpu()
+    _say(f"test_compute_duration_change_rolls_back exec={exec_}")
+    tr = training_step(seed=8, tp=4, pp=2, dp=2, microbatches=3, layers=2)
+    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
+    computes = [k for k, op in enumerate(tr.ops) if type(op).__name__ == "Compute"]
+    k = computes[len(computes) // 3]
+    new_d = tr.ops[k].duration + 4e-4
+    ld = ptr.load_trace(tr, ns.make_options(exec=ex))
+    try:
+        h = ld.handle
+        ns.netsim_advance(h)
+        before = ns.netsim_get_finish(h)
+        x = int(ld.done[k][0])
+        assert np.isfinite(before[x])
+        ns.netsim_update_start(h, x, new_d)
+        ns.netsim_advance(h)
+        got = ns.netsim_get_finish(h)
+    finally:
+        ld.close()
+    tr2 = copy.deepcopy(tr)
+    tr2.ops[k].duration = new_d
+    fin2, _, _, _ = ptr.run_trace(tr2, ns.make_options(exec=ex))
+    assert np.array_equal(got, fin2)
+    assert np.sum(got != before) > 0
+    ref = otl.simulate(tr2)
+    assert _rel(got, ref.finish) < TOL
