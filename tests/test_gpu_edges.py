@@ -152,3 +152,24 @@ def test_round_watchdog_reports_limit():
     assert e.value.status == ns.E_LIMIT
     fins, st = pr.run_program(Program("watchdog", [sc]))
     assert _rel(fins[0], osim.run_scenario(sc).finish) < TOL
+
+
+def test_more_groups_than_parts():
+    """3,000 independent flows (each on a link of its own): more groups than
+    the 1,024 parts a scenario is split into, so groups share parts; every
+    flow still ends at start + bytes / capacity."""
+    ns, pr = _gpu()
+    _say("test_more_groups_than_parts")
+    rng = np.random.default_rng(5)
+    n = 3000
+    caps = rng.choice([1e9, 2e9, 4e9], size=n)
+    size = rng.choice([1e5, 2e5, 3e5], size=n)
+    lag = rng.choice([0.0, 1e-4], size=n)
+    sc = Scenario(_explicit(caps))
+    for k in range(n):
+        sc.add(PathFlow([k], float(size[k]), lag=float(lag[k])))
+    fins, st = pr.run_program(Program("groups", [sc]))
+    assert st["parts"] == 1024
+    want = lag + size / caps
+    assert _rel(fins[0], want) < 1e-12
+    assert _rel(fins[0], osim.run_scenario(sc).finish) < TOL
