@@ -61,7 +61,13 @@ enum { NETSIM_MODE_CHAINED = 0, NETSIM_MODE_FLAT = 1, NETSIM_MODE_AGGREGATED = 2
 enum {
   NETSIM_EXEC_AUTO = 0,  /* grid for a single part with > 65536 flows without predecessors, else block */
   NETSIM_EXEC_GRID = 1,  /* whole GPU on one part at a time (grid barriers)      */
-  NETSIM_EXEC_BLOCK = 2  /* one workgroup per part (workgroup barriers)          */
+  NETSIM_EXEC_BLOCK = 2,  /* one workgroup per part (workgroup barriers)         */
+  NETSIM_EXEC_CLUSTER = 3 /* one leader workgroup per XCD runs parts as in block
+                             mode and hands re-solves of at least
+                             assist_min_flows flows to the other workgroups of its
+                             XCD (one per CU, cooperative launch); results equal
+                             block mode's bit for bit.  Rate solves without an
+                             event loop (netsim_solve_rates) run as in block mode */
 };
 
 /*
@@ -86,6 +92,8 @@ typedef struct {
   int32_t debug;             /* bit 0: consistency checks on the device; bit 1:
                                 phase timers (netsim_stats.phase_seconds)        */
   int32_t single_clock;      /* 1: one part (one clock) per scenario             */
+  int32_t assist_min_flows;  /* NETSIM_EXEC_CLUSTER: smallest re-solve handed to the
+                                helper workgroups; 0 = 4096                      */
 } netsim_options;
 
 /*
@@ -164,6 +172,8 @@ typedef struct {
    * wait after it, [5] freezing sweep, [6] wait after it, [7] choosing the
    * flows to re-solve. */
   double phase_seconds[8];
+  int64_t assisted_solves;   /* NETSIM_EXEC_CLUSTER: re-solves run by the helper
+                                workgroups (counted in solves and rounds too)    */
 } netsim_stats;
 
 /* Fills *opt with the defaults (device 0, auto layout, no limits). */

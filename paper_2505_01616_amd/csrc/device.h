@@ -51,6 +51,7 @@ struct ScenCtl {
   int64_t events, solves, rounds, flows_swept, incidences_swept;
   int64_t active_swept, pending_swept;
   int64_t reselected, wide_solves;
+  int64_t assisted;        // re-solves run by helper workgroups (cluster kernel)
   int32_t status;          // 0 ran to the end, 1 stopped at a limit, < 0 fault
   int32_t reserved;
   int64_t ticks[8];        // wall-clock ticks per phase (first thread of the group)
@@ -75,6 +76,7 @@ struct Params {
   double until;
   int32_t max_rounds;
   int32_t debug;           // run internal consistency checks
+  int32_t assist_min;      // cluster kernel: smallest re-solve handed to helper workgroups
   double scale;            // fixed-point units per B/s (a power of two)
   double inv_scale;
   // static flow / link data (device order)
@@ -117,13 +119,21 @@ struct Params {
   int32_t* unf0; int32_t* unf1;
   int32_t* arr;            // flows activated in the current event
   ScenCtl* ctl;            // [num_scen]
-  uint32_t* bar;           // grid barrier words [1024] (layout in kernels.hip)
+  uint32_t* bar;           // synchronisation words [BAR_WORDS] (layout in kernels.hip)
   uint64_t* slots;         // grid min-reduction slots [4]
 };
+
+// Words of Params::bar, cleared before every launch.
+constexpr int BAR_WORDS = 3072;
 
 hipError_t launch_block(const Params& p, int blocks, int threads, hipStream_t s);
 hipError_t launch_grid(const Params& p, int blocks, int threads, hipStream_t s);
 // Largest co-resident grid for launch_grid at `threads` per block.
 hipError_t grid_capacity(int device, int threads, int* blocks);
+// One leader workgroup per XCD running the event loops of the parts, the
+// other workgroups of its XCD solving its large re-solves (cooperative
+// launch, 1024 threads per workgroup; blocks from cluster_capacity).
+hipError_t launch_cluster(const Params& p, int blocks, hipStream_t s);
+hipError_t cluster_capacity(int device, int* blocks);
 
 }  // namespace netsim_dev

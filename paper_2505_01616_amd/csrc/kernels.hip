@@ -259,6 +259,123 @@ struct GridG {
   }
 };
 
+// Cluster kernel words: XCD x owns CL_STRIDE words from CL_BASE + CL_STRIDE*x
+// (offsets below, 64-byte lines apart where several writers meet).
+constexpr int BAR_NEXT = 48;  // next part to be claimed by a leader
+constexpr int CL_BASE = 1024, CL_STRIDE = 128;
+constexpr int CL_REG = 0;                 // workgroups registered on the XCD
+constexpr int CL_MB = 16;                 // jobs posted so far, or CL_CLOSED
+constexpr int CL_SC = 17, CL_N = 18;      // posted job: part, number of flows,
+constexpr int CL_AB = 19, CL_SNEW = 20;   //   slot buffer, first slot activated at this event,
+constexpr int CL_T = 22;                  //   event time (double)
+constexpr int CL_DONE = 32;               // jobs finished, summed over the helpers
+constexpr int CL_RC = 33;                 // job status (first helper)
+constexpr int CL_ROUNDS = 34, CL_FSW = 36;  // job rounds and flows swept (int64, first helper)
+constexpr int CL_ISW = 48;                // incidences swept (int64, summed over the helpers)
+constexpr int CL_CNT = 64;               // barrier among the helpers (arrivals, growing)
+constexpr uint32_t CL_CLOSED = 0xFFFFFFFFu;
+constexpr int NOT_TAKEN = 2;              // the helpers have left: solve locally
+// A helper with no job for this long leaves (its leader then solves alone).
+constexpr uint64_t IDLE_TICKS = 6000000000ull;  // 60 s at 100 MHz
+static_assert(CL_BASE + 16 * CL_STRIDE <= BAR_WORDS, "cluster words");
+
+// Waits (one thread) until *p != v, giving up when the abort word is set or
+// after `ticks` (then raising it).  Returns false if it gave up.
+__device__ __forceinline__ bool wait_ne(uint32_t* bar, uint32_t* p, uint32_t v, uint64_t ticks) {
+  const uint64_t t0 = wall_clock64();
+  while (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == v) {
+    __builtin_amdgcn_s_sleep(1);
+    if (__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return false;
+    if (wall_clock64() - t0 > ticks) {
+      __hip_atomic_store(&bar[BAR_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return false;
+    }
+  }
+  return true;
+}
+
+// Waits for this wave's outstanding memory operations (stores and atomics
+// included), so that a later release by another wave of the workgroup
+// covers them.
+__device__ __forceinline__ void drain() { __builtin_amdgcn_s_waitcnt(0); }
+
+// The helper workgroups of one XCD (all but its leader), solving one job at a
+// time with a barrier of their own.
+//
+// Everything the helpers and their leader share lives in device memory and
+// is exchanged inside one XCD, whose L2 they all use.  So a release needs no
+// L2 write-back (what the agent-scope release adds, for other XCDs): each
+// wave drains its stores and atomics (they are then in that L2, or performed
+// at agent scope) before its workgroup signals.  An acquire stays
+// agent-scope: it drops this CU's L1 and the L2's clean copies, which the
+// agent-scope atomics on link state may have left stale (measured: dropping
+// only the L1 reads stale link state).
+//
+// Barrier: workgroups add one to a counter that only grows and wait until it
+// reaches (barriers passed) x (helpers), so no arrival has to reset it.  A
+// wait longer than BARRIER_TIMEOUT_TICKS raises the launch's abort word.
+struct ClusterG {
+  double* lds;
+  int* ldsi;
+  int* flag;      // shared: abort state as seen by this block's thread 0
+  uint32_t* bar;  // launch words (abort flag)
+  uint32_t* cw;   // this XCD's cluster words
+  uint32_t gen;
+  int rank, nh;   // rank among the helpers, number of helpers
+  bool ab;
+  __device__ Lists* lists(ScenCtl* C) const { return &C->k; }
+  __device__ int tid() const { return rank * blockDim.x + threadIdx.x; }
+  __device__ int block_base() const { return rank * blockDim.x; }
+  __device__ int nblocks() const { return nh; }
+  __device__ int block_id() const { return rank; }
+  __device__ int nthr() const { return nh * blockDim.x; }
+  __device__ bool aborted() const { return ab; }
+  __device__ __forceinline__ void sync() {
+    drain();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (a == 0) {
+        const uint32_t target = (gen + 1) * (uint32_t)nh;
+        const uint32_t prev =
+            __hip_atomic_fetch_add(&cw[CL_CNT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (prev + 1 != target) wait_reach(&cw[CL_CNT], target);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      *flag = (int)a;
+    }
+    gen += 1;
+    __syncthreads();
+    ab = *flag != 0;
+  }
+  // Waits until the counter reaches target (counted modulo 2^32), giving up
+  // on the abort word or after BARRIER_TIMEOUT_TICKS (then raising it).
+  __device__ __forceinline__ void wait_reach(uint32_t* p, uint32_t target) {
+    const uint64_t t0 = wall_clock64();
+    while ((int32_t)(__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+      __builtin_amdgcn_s_sleep(1);
+      if (__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return;
+      if (wall_clock64() - t0 > BARRIER_TIMEOUT_TICKS) {
+        __hip_atomic_store(&bar[BAR_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+      }
+    }
+  }
+  template <class T>
+  __device__ T add(T* p, T v) {
+    return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  template <class T>
+  __device__ T load(const T* p) {
+    return __hip_atomic_load(const_cast<T*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  template <class T>
+  __device__ void store(T* p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+};
+
 template <class G> struct IsGrid { static constexpr bool value = false; };
 template <> struct IsGrid<GridG> { static constexpr bool value = true; };
 
@@ -393,7 +510,7 @@ struct Clock {
 // first thread only (they are the same for every thread of the group).
 struct Tally {
   uint64_t clk[9];
-  int64_t solves, rounds, fsw, asw, psw, sel, wide;
+  int64_t solves, rounds, fsw, asw, psw, sel, wide, asst;
 };
 
 // A flow id read from a work list must lie in the scenario's range.
@@ -1068,7 +1185,7 @@ struct SolveLds {
 template <class G, class LK>
 __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl* C, const int32_t* list0,
                                          int n0, int64_t& rounds, int64_t& fsw, int64_t& isw, Clock& clk,
-                                         SolveLds& S, bool warm) {
+                                         SolveLds& S, bool warm, const Resel* rs = nullptr) {
   Lists* K = g.lists(C);
   const int tid = g.tid();
   const int nb = g.nblocks();
@@ -1076,18 +1193,46 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
   const int c0 = min(n0, g.block_id() * per);
   const int nl = min(n0, c0 + per) - c0;
   const int l0 = C->l0;
+  const int cap = C->f1 - C->f0;
+  int* bc = g.ldsi + 120;  // counters read by thread 0 after a barrier, for the block
   if (!warm) cold_links(g, P, lk, C);
   if (tid == 0)
     for (int k = 0; k < 3; ++k) g.store(&K->rem3[k], 0);
   int bad = 0;
+  // ids and path records into shared memory; re-solving (rs), each flow's
+  // take-back too: remaining bytes brought up to rs->t, its rate and one
+  // unfrozen flow returned to its links
   for (int j = threadIdx.x; j < nl; j += blockDim.x) {
     int f = list0[c0 + j];
-    if (!in_range(f, C->f0, C->f1 - C->f0)) { bad = 2; f = C->f0; }
+    const bool ok = in_range(f, C->f0, cap);
+    if (!ok) { bad = 2; f = C->f0; }
+    const uint4 rec = P.path16[f];
     S.fid[j] = f;
-    S.path[j] = P.path16[f];
+    S.path[j] = rec;
     S.u[0][j] = (uint16_t)j;
+    if (rs && ok) {
+      const int sl = rs->at[c0 + j];
+      if ((unsigned)sl >= (unsigned)cap) { bad = 2; continue; }
+      const bool fresh = sl >= rs->s_new;
+      int64_t qv = 0;
+      if (!fresh) {
+        const double rt = rs->sl.rate[sl];
+        P.rem[f] = rem_at(P.rem[f], rt, rs->t, P.tref[f]);
+        P.tref[f] = rs->t;
+        qv = (int64_t)__builtin_rint(rt * P.scale);
+      }
+      int lv[6];
+      const int deg = unpack_path(rec, l0, lv);
+#pragma unroll
+      for (int k = 0; k < 6; ++k)
+        if (k < deg) {
+          if (!fresh) lk.addR(g, lv[k], qv);
+          lk.addN(g, lv[k], (int64_t)1);
+        }
+    }
   }
   int nu = nl;
+  if (bad) g.store(&K->fault, bad);
   g.sync();
   const uint32_t st0 = first_round(g, P, lk, C);
   clk.lap(2);
@@ -1162,8 +1307,14 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
       fsw += total;
     }
     if (g.aborted()) return ST_BARRIER;
-    if (g.load(&K->fault) != 0) { rc = g.load(&K->fault) == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
-    const int left = g.load(&K->rem3[r % 3]);
+    // one read of the two counters per workgroup, shared through shared memory
+    if (threadIdx.x == 0) {
+      bc[0] = g.load(&K->fault);
+      bc[1] = g.load(&K->rem3[r % 3]);
+    }
+    __syncthreads();
+    const int ft = bc[0], left = bc[1];
+    if (ft != 0) { rc = ft == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
     if (left == 0) break;
     if (left >= total) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
     if (++r > P.max_rounds) { rc = ST_ROUNDS; break; }
@@ -1171,7 +1322,207 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     nu = nu_new;
   }
   if (tid == 0) g.store(&K->stamp, st0 + (uint32_t)r);
+  if (rs && rc == 0) {
+    // each re-solved flow's slot: its rate (the share it froze at) and
+    // predicted completion, by the thread that took it back
+    for (int j = threadIdx.x; j < nl; j += blockDim.x) {
+      const int f = S.fid[j];
+      const int sl = rs->at[c0 + j];
+      if ((unsigned)sl >= (unsigned)cap) continue;
+      const double m = S.mf[j];
+      rs->sl.rate[sl] = m;
+      rs->sl.tau[sl] = rs->t + P.rem[f] / m;
+    }
+  }
   return rc;
+}
+
+// ------------------------------------------------- helper workgroups (cluster kernel)
+// A leader without helpers.
+struct NoAssist {
+  static constexpr bool kOn = false;
+};
+
+// A leader's side of its XCD's helpers: a large re-solve is posted as a job;
+// the helpers take the flows back, run solve_lds over link state in global
+// memory and write the rates by flow and the slots (rate, predicted
+// completion), as the fused block solve does.  A leader whose link
+// state lives in shared memory copies residual capacities and unfrozen
+// counts out before and back after (their stamps are a separate sequence
+// in global memory: C->k.stamp over Params::fl); one whose state is global
+// hands over its stamp counter instead, so both sides number rounds in one
+// sequence over the one stamp array.  Only thread 0 touches the mailbox.
+struct Assist {
+  static constexpr bool kOn = true;
+  uint32_t* bar;
+  uint32_t* cw;   // this XCD's cluster words
+  int nh;         // helper workgroups
+  int min_n;      // smallest solve handed over
+  uint32_t seq;   // jobs posted so far (every thread keeps the same value)
+  int* box;       // shared memory [2]: result broadcast
+  __device__ bool takes(int n) const { return nh > 0 && n >= min_n && n <= nh * LDS_FLOWS; }
+
+  // Re-solve of the part's list of n flows (the event loop's re-solve list
+  // and the slot of each in slot buffer ab; slots from s_new on were
+  // activated at time t): the job's status, or NOT_TAKEN if the helpers
+  // have left (nothing changed then).
+  template <class LK>
+  __device__ __forceinline__ int solve(BlockG& g, const Params& P, LK& lk, ScenCtl* C, int sc, int n,
+                                       int ab, int s_new, double t, int64_t& rounds, int64_t& fsw,
+                                       int64_t& isw) {
+    const int T = blockDim.x;
+    const int l0 = C->l0, nl = C->l1 - C->l0;
+    if constexpr (LK::kTable) {
+      for (int i = threadIdx.x; i < nl; i += T) {
+        P.lst[2 * (l0 + i)] = lk.R[i];
+        P.lst[2 * (l0 + i) + 1] = (int64_t)lk.n[i];
+      }
+    }
+    drain();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int res = NOT_TAKEN, posted = 0;
+      if constexpr (!LK::kTable)
+        __hip_atomic_store(&C->k.stamp, g.lst->stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&cw[CL_SC], (uint32_t)sc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&cw[CL_N], (uint32_t)n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&cw[CL_AB], (uint32_t)ab, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&cw[CL_SNEW], (uint32_t)s_new, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(reinterpret_cast<uint64_t*>(cw + CL_T), (uint64_t)__double_as_longlong(t),
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      drain();  // the job and the link state reach the XCD's L2 before the post
+      uint32_t expect = seq;
+      if (__hip_atomic_compare_exchange_strong(&cw[CL_MB], &expect, seq + 1, __ATOMIC_RELAXED,
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+        posted = 1;
+        const uint32_t want = (seq + 1) * (uint32_t)nh;
+        const uint64_t t0 = wall_clock64();
+        bool ok = true;
+        while (__hip_atomic_load(&cw[CL_DONE], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != want) {
+          __builtin_amdgcn_s_sleep(2);
+          if (__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
+              wall_clock64() - t0 > IDLE_TICKS) {
+            __hip_atomic_store(&bar[BAR_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ok = false;
+            break;
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        if (ok) {
+          res = (int)__hip_atomic_load(&cw[CL_RC], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          auto w64 = [&](int k) { return reinterpret_cast<uint64_t*>(cw + k); };
+          rounds += (int64_t)__hip_atomic_load(w64(CL_ROUNDS), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          fsw += (int64_t)__hip_atomic_load(w64(CL_FSW), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          isw += (int64_t)__hip_atomic_load(w64(CL_ISW), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(w64(CL_ISW), (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if constexpr (!LK::kTable)
+            g.lst->stamp = __hip_atomic_load(&C->k.stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+          res = ST_BARRIER;
+        }
+      }
+      box[0] = res;
+      box[1] = posted;
+    }
+    __syncthreads();
+    const int res = box[0];
+    seq += (uint32_t)box[1];
+    if constexpr (LK::kTable) {
+      if (res != NOT_TAKEN)
+        for (int i = threadIdx.x; i < nl; i += T) {
+          lk.R[i] = P.lst[2 * (l0 + i)];
+          lk.n[i] = (int32_t)P.lst[2 * (l0 + i) + 1];
+        }
+    }
+    __syncthreads();
+    return res;
+  }
+};
+
+// A helper workgroup: waits for its leader's jobs and solves them with the
+// XCD's other helpers until the leader closes the mailbox, the launch aborts
+// or no job comes for IDLE_TICKS (then it closes the mailbox itself, unless a
+// job arrived meanwhile).
+__device__ __forceinline__ void helper_loop(const Params& P, ClusterG& cg, SolveLds& S, Tally* tl,
+                                            int* box, double* tjob) {
+  uint32_t* cw = cg.cw;
+  uint32_t seen = 0;
+  for (;;) {
+    if (threadIdx.x == 0) {
+      int leave = 0;
+      uint32_t v = seen;
+      const uint64_t t0 = wall_clock64();
+      for (;;) {
+        v = __hip_atomic_load(&cw[CL_MB], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (v != seen) break;
+        if (__hip_atomic_load(&P.bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+          leave = 1;
+          break;
+        }
+        if (wall_clock64() - t0 > IDLE_TICKS) {
+          uint32_t e = seen;
+          if (__hip_atomic_compare_exchange_strong(&cw[CL_MB], &e, CL_CLOSED, __ATOMIC_RELAXED,
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+            v = CL_CLOSED;
+            break;
+          }
+        }
+        __builtin_amdgcn_s_sleep(10);  // ~270 ns: 31 pollers stay light on the L2
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      if (leave)  // later posts must fail rather than wait for helpers that left
+        __hip_atomic_exchange(&cw[CL_MB], CL_CLOSED, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (leave || v == CL_CLOSED) {
+        box[0] = -1;
+      } else {
+        box[0] = (int)__hip_atomic_load(&cw[CL_SC], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        box[1] = (int)__hip_atomic_load(&cw[CL_N], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        box[2] = (int)v;
+        box[3] = (int)__hip_atomic_load(&cw[CL_AB], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        box[4] = (int)__hip_atomic_load(&cw[CL_SNEW], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        tjob[0] = __longlong_as_double((long long)__hip_atomic_load(
+            reinterpret_cast<uint64_t*>(cw + CL_T), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      }
+    }
+    __syncthreads();
+    const int sc = box[0], n = box[1], ab = box[3], s_new = box[4];
+    const double t = tjob[0];
+    seen = (uint32_t)box[2];
+    __syncthreads();
+    if (sc < 0) break;
+    int rc = ST_OVERFLOW;
+    int64_t rr = 0, ff = 0, is = 0;
+    // the same job for every helper: all of them solve it or none does
+    if (sc < P.num_scen && n > 0 && n <= cg.nh * LDS_FLOWS && n <= P.ctl[sc].f1 - P.ctl[sc].f0 &&
+        P.ctl[sc].lds_paths && (ab == 0 || ab == 1) && s_new >= 0 &&
+        s_new <= P.ctl[sc].f1 - P.ctl[sc].f0) {
+      ScenCtl* C = &P.ctl[sc];
+      const int f0 = C->f0;
+      const Slots sl = ab ? Slots{P.act1 + f0, P.tau1 + f0, P.srate1 + f0}
+                          : Slots{P.act0 + f0, P.tau0 + f0, P.srate0 + f0};
+      const Resel rs{sl, P.arrslot + f0, s_new, t};
+      LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
+      Clock clk(false, tl->clk);
+      rc = solve_lds(cg, P, lk, C, P.arr + f0, n, rr, ff, is, clk, S, true, &rs);
+    }
+    long w = (long)is;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) w += __shfl_xor(w, o, 64);
+    if (lane_id() == 0 && w != 0)
+      __hip_atomic_fetch_add(reinterpret_cast<uint64_t*>(cw + CL_ISW), (uint64_t)w, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    if (cg.rank == 0 && threadIdx.x == 0) {
+      __hip_atomic_store(&cw[CL_RC], (uint32_t)rc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(reinterpret_cast<uint64_t*>(cw + CL_ROUNDS), (uint64_t)rr, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(reinterpret_cast<uint64_t*>(cw + CL_FSW), (uint64_t)ff, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+    drain();
+    __syncthreads();
+    if (threadIdx.x == 0)  // drained above: rates and statistics are in the XCD's L2
+      __hip_atomic_fetch_add(&cw[CL_DONE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 // ------------------------------------------------------------- event loop
@@ -1246,9 +1597,9 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, Lists
   }
 }
 
-template <class G, class LK>
+template <class G, class LK, class AS = NoAssist>
 __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const int sc, SolveLds* S,
-                                           Tally* tl, const FlowCache& fc) {
+                                           Tally* tl, const FlowCache& fc, AS* as = nullptr) {
   ScenCtl* C = &P.ctl[sc];
   Lists* K = g.lists(C);
   const int f0 = C->f0;
@@ -1278,6 +1629,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     tl->psw = resume ? C->pending_swept : 0;
     tl->sel = resume ? C->reselected : 0;
     tl->wide = resume ? C->wide_solves : 0;
+    tl->asst = resume ? C->assisted : 0;
   }
   int64_t& rounds = tl->rounds;
   int64_t& fsw = tl->fsw;
@@ -1573,7 +1925,19 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
         const Resel rs{sl, arrSlot, slots0, t};
         bool fused = false;  // take-back and slot writes done inside the solve
         if constexpr (!IsGrid<G>::value) {
-          if (C->lds_paths && nSel <= 64 * (int)blockDim.x) {
+          int ar = NOT_TAKEN;
+          if constexpr (AS::kOn) {
+            // a large re-solve goes to the helper workgroups of the XCD, which
+            // also take the flows back and write their slots
+            if (C->lds_paths && as->takes(nSel)) {
+              ar = as->solve(g, P, lk, C, sc, nSel, ab, slots0, t, rounds, fsw, isw);
+              if (ar != NOT_TAKEN && threadIdx.x == 0) tl->asst += 1;
+            }
+          }
+          if (ar != NOT_TAKEN) {
+            rc = ar;
+            fused = true;
+          } else if (C->lds_paths && nSel <= 64 * (int)blockDim.x) {
             rc = solve_mask(g, P, lk, C, arrs, nSel, rounds, fsw, isw, clk, true, fc, &rs);
             fused = true;
           } else {
@@ -1691,6 +2055,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     C->pending_swept = tl->psw;
     C->reselected = tl->sel;
     C->wide_solves = tl->wide;
+    C->assisted = tl->asst;
     C->status = status;
     for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)tl->clk[k];
   }
@@ -1788,6 +2153,89 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   }
 }
 
+// One workgroup per CU, 1024 threads.  Every workgroup registers on its XCD;
+// the first of each XCD leads: it claims parts one at a time and runs their
+// event loops as the block kernel does, handing re-solves of at least
+// P.assist_min flows to the other workgroups of its XCD (its helpers).  With
+// no helpers (a lone workgroup on its XCD, or registration timed out) a
+// leader solves everything itself.  Every part is claimed by exactly one
+// leader, whatever the number of leaders.
+__global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
+  __shared__ double lds[32];
+  __shared__ int ldsi[128];
+  __shared__ Tally tally;
+  __shared__ Lists lists;
+  __shared__ int flag;
+  __shared__ int box[8];
+  __shared__ double tjob[1];
+  __shared__ int claim;
+  __shared__ __align__(16) unsigned char pool[POOL_BYTES];
+  static_assert(sizeof(SolveLds) <= POOL_BYTES, "helper pool");
+  if (threadIdx.x == 0) {
+    const uint32_t x = xcc_id();
+    uint32_t* cw = P.bar + CL_BASE + CL_STRIDE * x;
+    const uint32_t rank = __hip_atomic_fetch_add(&cw[CL_REG], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t prev =
+        __hip_atomic_fetch_add(&P.bar[BAR_REG], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    bool ok = true;
+    if (prev == gridDim.x - 1)
+      __hip_atomic_store(&P.bar[BAR_REG_GEN], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      ok = wait_ne(P.bar, &P.bar[BAR_REG_GEN], 0u, BARRIER_TIMEOUT_TICKS);
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const uint32_t on_xcd = __hip_atomic_load(&cw[CL_REG], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    box[0] = (int)x;
+    box[1] = (int)rank;
+    box[2] = ok ? (int)on_xcd - 1 : 0;  // helpers on the XCD
+  }
+  __syncthreads();
+  const int x = box[0], rank = box[1], nh = box[2];
+  uint32_t* cw = P.bar + CL_BASE + CL_STRIDE * x;
+  __syncthreads();
+  if (rank != 0) {
+    if (nh > 0) {
+      ClusterG cg{lds, ldsi, &flag, P.bar, cw, 0u, rank - 1, nh, false};
+      helper_loop(P, cg, *reinterpret_cast<SolveLds*>(pool), &tally, box, tjob);
+    }
+    return;
+  }
+  BlockG g{lds, ldsi, &lists};
+  Assist as{P.bar, cw, nh, P.assist_min > 0 ? P.assist_min : 1, 0u, box};
+  for (;;) {
+    if (threadIdx.x == 0)
+      claim = (int)__hip_atomic_fetch_add(&P.bar[BAR_NEXT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const int sc = claim;
+    __syncthreads();
+    if (sc >= P.num_scen) break;
+    ScenCtl* C = &P.ctl[sc];
+    if (threadIdx.x == 0) {
+      lists = Lists{};
+      C->k = Lists{};  // counters of the helpers' solves
+    }
+    const int nl = C->l1 - C->l0;
+    const bool in_lds = link_pool_bytes(nl) <= POOL_BYTES;
+    if (in_lds)  // the helpers' stamps start from zero with their counter
+      for (int l = C->l0 + (int)threadIdx.x; l < C->l1; l += blockDim.x) P.fl[l] = 0;
+    __syncthreads();
+    const int used = in_lds ? (link_pool_bytes(nl) + 15) & ~15 : 0;
+    const int ncache = (POOL_BYTES - used) / FLOW_LDS_BYTES;
+    const FlowCache fc{reinterpret_cast<uint4*>(pool + used),
+                       reinterpret_cast<int32_t*>(pool + used + 16 * ncache), ncache};
+    if (in_lds) {
+      LinksShared lk(pool, C->l0, nl, P.inv_scale);
+      event_loop(g, P, lk, sc, nullptr, &tally, fc, &as);
+    } else {
+      LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
+      event_loop(g, P, lk, sc, nullptr, &tally, fc, &as);
+    }
+    __syncthreads();
+  }
+  // no more jobs: the helpers leave
+  if (threadIdx.x == 0)
+    __hip_atomic_exchange(&cw[CL_MB], CL_CLOSED, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 hipError_t launch_block(const Params& p, int blocks, int threads, hipStream_t s) {
   if (threads <= 512)
     hipLaunchKernelGGL(netsim_block_kernel<512>, dim3(blocks), dim3(threads), 0, s, p);
@@ -1801,6 +2249,24 @@ hipError_t launch_grid(const Params& p, int blocks, int threads, hipStream_t s) 
   void* args[] = {&copy};
   return hipLaunchCooperativeKernel((const void*)netsim_grid_kernel, dim3(blocks), dim3(threads),
                                     args, 0, s);
+}
+
+hipError_t launch_cluster(const Params& p, int blocks, hipStream_t s) {
+  Params copy = p;
+  void* args[] = {&copy};
+  return hipLaunchCooperativeKernel((const void*)netsim_cluster_kernel, dim3(blocks), dim3(1024), args, 0,
+                                    s);
+}
+
+hipError_t cluster_capacity(int device, int* blocks) {
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, netsim_cluster_kernel, 1024, 0);
+  if (e != hipSuccess) return e;
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, device);
+  if (e != hipSuccess) return e;
+  *blocks = per_cu * prop.multiProcessorCount;
+  return hipSuccess;
 }
 
 hipError_t grid_capacity(int device, int threads, int* blocks) {

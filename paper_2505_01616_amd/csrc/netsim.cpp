@@ -235,6 +235,8 @@ constexpr int32_t kMaxPartsPerScen = 1024;
 // Link components per part for the incremental re-solve; more are merged
 // into the last one (a coarser partition is still safe).
 constexpr int32_t kMaxComp = 4096;
+// Cluster layout: smallest re-solve the helper workgroups take by default.
+constexpr int32_t kAssistMinFlows = 4096;
 
 netsim_status prepare(netsim_t* h) {
   const int32_t S = (int32_t)h->scen.size();
@@ -506,7 +508,7 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.comp2, sizeof(int32_t) * Fz},
       {(void**)&P.unf0, sizeof(int32_t) * Fz},
       {(void**)&P.unf1, sizeof(int32_t) * Fz},
-      {(void**)&P.bar, sizeof(uint32_t) * 1024},
+      {(void**)&P.bar, sizeof(uint32_t) * netsim_dev::BAR_WORDS},
       {(void**)&P.slots, sizeof(uint64_t) * 8},
   };
   size_t total = 0;
@@ -577,7 +579,7 @@ netsim_status reset_state(netsim_t* h, hipStream_t st) {
   he = hipMemsetAsync(P.nact, 0, sizeof(int32_t) * Lz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.base, 0, sizeof(double) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.rate, 0, sizeof(double) * Fz, st);
-  if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 1024, st);
+  if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * netsim_dev::BAR_WORDS, st);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemsetAsync (reset)");
   he = hipStreamSynchronize(st);
   if (he != hipSuccess) return hip_fail(h, he, "hipStreamSynchronize (reset)");
@@ -599,6 +601,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
   P.debug = h->opt.debug;
   P.max_rounds = h->opt.max_rounds > 0 ? h->opt.max_rounds
                                        : (int32_t)std::min<int64_t>(h->F + 1, std::numeric_limits<int32_t>::max());
+  P.assist_min = h->opt.assist_min_flows > 0 ? h->opt.assist_min_flows : kAssistMinFlows;
   const int32_t S = h->num_parts;
   int exec = h->opt.exec;
   if (exec == NETSIM_EXEC_AUTO) {
@@ -615,7 +618,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
   // (a launch that continues a run must not see the last launch's counts)
   uint64_t inf_slots[8];
   for (auto& x : inf_slots) x = 0x7FF0000000000000ull;
-  hipError_t he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * 1024, st);
+  hipError_t he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * netsim_dev::BAR_WORDS, st);
   if (he == hipSuccess) he = hipMemcpyAsync(P.slots, inf_slots, sizeof(inf_slots), hipMemcpyHostToDevice, st);
   if (he != hipSuccess) return hip_fail(h, he, "reset of the grid synchronisation words");
   hipEvent_t e0, e1;
@@ -624,7 +627,12 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
   if (he != hipSuccess) return hip_fail(h, he, "hipEventCreate");
   he = hipEventRecord(e0, st);
   if (he == hipSuccess) {
-    if (exec == NETSIM_EXEC_GRID) {
+    if (exec == NETSIM_EXEC_CLUSTER && !solve_only) {
+      int blocks = 0;
+      he = netsim_dev::cluster_capacity(h->opt.device, &blocks);
+      if (he == hipSuccess && blocks < 1) he = hipErrorInvalidConfiguration;
+      if (he == hipSuccess) he = netsim_dev::launch_cluster(P, blocks, st);
+    } else if (exec == NETSIM_EXEC_GRID) {
       const int threads = 1024;
       int cap = 0;
       he = netsim_dev::grid_capacity(h->opt.device, threads, &cap);
@@ -753,6 +761,7 @@ netsim_status simulate(netsim_t* h, hipStream_t st, bool resume, int64_t max_eve
     s.pending_swept += c.pending_swept;
     s.reselected += c.reselected;
     s.wide_solves += c.wide_solves;
+    s.assisted_solves += c.assisted;
     s.sim_time = std::max(s.sim_time, c.t);
     if (c.status != 0) s.complete = 0;
   }

@@ -24,7 +24,7 @@ OK, E_INVALID, E_NOMEM, E_DEVICE, E_STATE, E_LIMIT = 0, -1, -2, -3, -4, -5
 TOPO_LEAF_SPINE, TOPO_RAIL, TOPO_FAT_TREE = 1, 2, 3
 RING_ALLREDUCE, RING_REDUCE_SCATTER, RING_ALL_GATHER = 0, 1, 2
 MODE_CHAINED, MODE_FLAT, MODE_AGGREGATED = 0, 1, 2
-EXEC_AUTO, EXEC_GRID, EXEC_BLOCK = 0, 1, 2
+EXEC_AUTO, EXEC_GRID, EXEC_BLOCK, EXEC_CLUSTER = 0, 1, 2, 3
 
 STATUS_NAMES = {OK: "NETSIM_OK", E_INVALID: "NETSIM_E_INVALID", E_NOMEM: "NETSIM_E_NOMEM",
                 E_DEVICE: "NETSIM_E_DEVICE", E_STATE: "NETSIM_E_STATE", E_LIMIT: "NETSIM_E_LIMIT"}
@@ -34,7 +34,8 @@ class netsim_options(ctypes.Structure):
     _fields_ = [("device", ctypes.c_int32), ("exec", ctypes.c_int32),
                 ("max_events", ctypes.c_int64), ("until", ctypes.c_double),
                 ("max_rounds", ctypes.c_int32), ("block_threads", ctypes.c_int32),
-                ("debug", ctypes.c_int32), ("single_clock", ctypes.c_int32)]
+                ("debug", ctypes.c_int32), ("single_clock", ctypes.c_int32),
+                ("assist_min_flows", ctypes.c_int32)]
 
 
 class netsim_topology(ctypes.Structure):
@@ -59,7 +60,8 @@ class netsim_stats(ctypes.Structure):
                 ("reselected", ctypes.c_int64), ("wide_solves", ctypes.c_int64),
                 ("complete", ctypes.c_int32), ("parts", ctypes.c_int32),
                 ("sim_time", ctypes.c_double), ("device_seconds", ctypes.c_double),
-                ("upload_seconds", ctypes.c_double), ("phase_seconds", ctypes.c_double * 8)]
+                ("upload_seconds", ctypes.c_double), ("phase_seconds", ctypes.c_double * 8),
+                ("assisted_solves", ctypes.c_int64)]
 
     def as_dict(self):
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
@@ -160,11 +162,11 @@ def netsim_default_options() -> netsim_options:
 
 
 def make_options(device=0, exec=EXEC_AUTO, max_events=0, until=math.inf, max_rounds=0,
-                 block_threads=0, debug=0, single_clock=0) -> netsim_options:
+                 block_threads=0, debug=0, single_clock=0, assist_min_flows=0) -> netsim_options:
     o = netsim_default_options()
     o.device, o.exec, o.max_events, o.until = device, exec, max_events, until
     o.max_rounds, o.block_threads, o.debug = max_rounds, block_threads, debug
-    o.single_clock = single_clock
+    o.single_clock, o.assist_min_flows = single_clock, assist_min_flows
     return o
 
 

@@ -1,0 +1,148 @@
+"""GPU tests of the cluster layout (NETSIM_EXEC_CLUSTER): one leader
+workgroup per XCD runs the parts' event loops as the block layout does and
+hands re-solves of at least assist_min_flows flows to the other workgroups of
+its XCD, which run the multi-workgroup solve over link state in global memory.
+
+The re-solve is the same computation on the same integer link state, so the
+finish times and the solve statistics must equal the block layout's bit for
+bit (the block layout is held to the oracle in test_gpu_parity); with
+assist_min_flows = 1 every re-solve goes to the helpers, which exercises the
+hand-over on every event.  One case also goes straight to the oracle."""
+
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import sim as osim
+from workloads import configs, micro
+from workloads.program import Program
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-6
+# statistics that do not depend on where a solve ran (a re-solve of more than
+# 64 x 1024 flows is "wide" in the block layout only)
+SAME = ("events", "solves", "rounds", "flows_swept", "incidences_swept", "active_swept",
+        "pending_swept", "reselected", "completed_flows")
+
+
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2505_01616_amd import netsim as ns
+    from paper_2505_01616_amd import program as prog
+    return ns, prog
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _rel(a, b):
+    a, b = np.asarray(a), np.asarray(b)
+    fa, fb = np.isfinite(a), np.isfinite(b)
+    assert np.array_equal(fa, fb), "different sets of finished flows"
+    return float(np.max(np.abs(a[fa] - b[fa]) / np.maximum(np.abs(b[fa]), 1e-300))) if fa.any() else 0.0
+
+
+def _both(program, assist_min, **opt):
+    ns, pr = _gpu()
+    a, sa = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK, **opt))
+    b, sb = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=assist_min,
+                                                    **opt))
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y, equal_nan=True)
+    for k in SAME:
+        assert sa[k] == sb[k], (k, sa[k], sb[k])
+    assert sa["assisted_solves"] == 0
+    assert sb["complete"] == 1
+    return sa, sb
+
+
+@pytest.mark.parametrize("single_clock", [0, 1])
+@pytest.mark.parametrize("assist_min", [1, 256])
+def test_cluster_equals_block(single_clock, assist_min):
+    """Tensor-parallel rings and pipeline sends (several parts, or one):
+    every re-solve (assist_min = 1) or the larger ones handed to helpers."""
+    _say(f"test_cluster_equals_block single_clock={single_clock} assist_min={assist_min}")
+    sa, sb = _both(configs.c2(2, tp_reps=6), assist_min, single_clock=single_clock)
+    assert 0 <= sb["assisted_solves"] <= sb["solves"]
+    if assist_min == 1:
+        assert sb["assisted_solves"] > 0
+    _say("  solves", sb["solves"], "assisted", sb["assisted_solves"], "parts", sb["parts"])
+
+
+def test_cluster_against_oracle():
+    """One clock per scenario: finish times within 1e-6 of the oracle's and
+    the oracle's event and solve counts, every re-solve run by the helpers."""
+    ns, pr = _gpu()
+    _say("test_cluster_against_oracle")
+    program = configs.c2(2, tp_reps=6)
+    ref = osim.run_scenario(program.scenarios[0])
+    fins, st = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=1,
+                                                       single_clock=1))
+    assert _rel(fins[0], ref.finish) < TOL
+    assert st["events"] == ref.events and st["solves"] == ref.solves
+    assert st["assisted_solves"] > 0
+
+
+def test_cluster_expert_parallel_alltoall():
+    """The expert-parallel all-to-all (fat tree, Zipf dispatch) reduced to two
+    server blocks of four groups: re-solves of ~16k flows at every phase
+    start, with the default threshold."""
+    _say("test_cluster_expert_parallel_alltoall")
+    sa, sb = _both(configs.c4(4, blocks=2, locals_=4, phases=2), 0)
+    assert sb["assisted_solves"] > 0
+    _say("  block s", sa["device_seconds"], "cluster s", sb["device_seconds"],
+         "assisted", sb["assisted_solves"], "of", sb["solves"])
+
+
+def test_cluster_link_state_in_global_memory():
+    """One clock over the whole 4096-GPU fat tree: the part has ~20k links,
+    more than shared memory holds, so the leader's link state and stamps
+    are in global memory and shared with the helpers."""
+    _say("test_cluster_link_state_in_global_memory")
+    sa, sb = _both(configs.c4(4, blocks=2, locals_=2, phases=2), 1024, single_clock=1)
+    assert sa["parts"] == 1 and sb["assisted_solves"] > 0
+
+
+def test_cluster_many_parts_few_leaders():
+    """200 random dynamic cases as 200 scenarios, far more parts than XCDs:
+    leaders claim parts one after another; each scenario against the oracle."""
+    _say("test_cluster_many_parts_few_leaders")
+    scs = []
+    for seed in range(200):
+        scs += micro.random_dynamic(seed, integer_caps=(seed % 2 == 0)).scenarios
+    sa, sb = _both(Program("micro-batch", scs), 1, single_clock=1)
+    assert sb["parts"] == len(scs) and sb["assisted_solves"] > 0
+    ns, pr = _gpu()
+    fins, _ = pr.run_program(Program("micro-batch", scs),
+                             ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=1, single_clock=1))
+    for s, sc in enumerate(scs):
+        assert _rel(fins[s], osim.run_scenario(sc).finish) < TOL, s
+
+
+def test_cluster_advance_in_pieces():
+    """Runs continued over several launches keep the helpers' counters and
+    stamps consistent: pieces equal one run and the block layout's run."""
+    ns, pr = _gpu()
+    _say("test_cluster_advance_in_pieces")
+    program = configs.c2(2, tp_reps=6)
+    ref, _ = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK))
+    ref = np.concatenate(ref)
+    T = float(np.nanmax(ref))
+    ld = pr.load_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=1))
+    try:
+        h = ld.handle
+        for frac in (0.25, 0.5, 0.75):
+            ns.netsim_advance(h, until=frac * T)
+            got = ns.netsim_get_finish(h)
+            assert np.array_equal(np.isfinite(got), ref <= frac * T)
+            assert np.array_equal(got[np.isfinite(got)], ref[np.isfinite(got)])
+        ns.netsim_advance(h)
+        assert np.array_equal(ns.netsim_get_finish(h), ref)
+        assert ns.netsim_get_stats(h)["assisted_solves"] > 0
+    finally:
+        ld.close()
