@@ -134,7 +134,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1, help="timed complete simulations")
     ap.add_argument("--warmup", type=int, default=1, help="untimed complete simulations first")
-    ap.add_argument("--exec", choices=["grid", "block", "auto"], default="auto")
+    ap.add_argument("--exec", choices=["grid", "block", "cluster", "auto"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM counters)")
@@ -168,7 +168,8 @@ def main():
     if args.rollback:
         print(json.dumps(rollback_bench(ns, prog, program, stream)), flush=True)
         return
-    ex = {"grid": ns.EXEC_GRID, "block": ns.EXEC_BLOCK, "auto": ns.EXEC_AUTO}[args.exec]
+    ex = {"grid": ns.EXEC_GRID, "block": ns.EXEC_BLOCK, "cluster": ns.EXEC_CLUSTER,
+          "auto": ns.EXEC_AUTO}[args.exec]
     ld = prog.load_program(program, ns.make_options(exec=ex))
     h = ld.handle
     keys = ("events", "solves", "rounds", "flows_swept", "incidences_swept", "active_swept",
@@ -197,6 +198,8 @@ def main():
         wall = time.perf_counter() - t0
         parts = st["parts"]
         sim_time = st["sim_time"]
+        layout = st["layout"]
+        assisted = st["assisted_solves"]
     finally:
         ld.close()
     dev = tot["device_seconds"]
@@ -204,7 +207,8 @@ def main():
     events_per_s = tot["events"] / dev
     abytes = algorithmic_bytes(tot)
     achieved = abytes / dev / 1e9
-    kernel = "netsim_grid_kernel" if args.exec == "grid" else "netsim_block_kernel"
+    kernel = {ns.EXEC_GRID: "netsim_grid_kernel", ns.EXEC_BLOCK: "netsim_block_kernel",
+              ns.EXEC_CLUSTER: "netsim_cluster_kernel"}[layout]
     traffic = traffic_from_profile(kernel, args.steps)
     line = {
         "metric": "max-min rate solves/sec + events/sec (4096-GPU all-to-all); achieved HBM GB/s",
@@ -222,13 +226,15 @@ def main():
         "config": {"workload": "c4: 4096 GPUs, 3-tier fat-tree 2:1 at the core, 64 EP groups x 64 "
                                "ranks, 4 all-to-all phases, Zipf(1.2) bytes mean 4 MiB, seed 4; "
                                "one step = the complete simulation",
-                   "flows": nflows, "incidences": nnz, "exec": args.exec, "parts": parts},
+                   "flows": nflows, "incidences": nnz, "exec": args.exec, "parts": parts,
+                   "layout": kernel},
         "events_per_s": events_per_s,
         "events_per_step": tot["events"] / args.steps,
         "solves_per_step": tot["solves"] / args.steps,
         "rounds_per_solve": tot["rounds"] / max(tot["solves"], 1),
         "reselected_per_solve": tot["reselected"] / max(tot["solves"], 1),
         "wide_solves": tot["wide_solves"],
+        "assisted_solves_per_step": assisted,
         "wall_s_incl_state_reset": wall,
         "sim_time_s": sim_time,
         "phase_seconds_summed_over_parts": dict(zip(

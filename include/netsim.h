@@ -59,7 +59,9 @@ enum { NETSIM_RING_ALLREDUCE = 0, NETSIM_RING_REDUCE_SCATTER = 1, NETSIM_RING_AL
 enum { NETSIM_MODE_CHAINED = 0, NETSIM_MODE_FLAT = 1, NETSIM_MODE_AGGREGATED = 2 };
 /* Execution layout (netsim_options.exec). */
 enum {
-  NETSIM_EXEC_AUTO = 0,  /* grid for a single part with > 65536 flows without predecessors, else block */
+  NETSIM_EXEC_AUTO = 0,  /* grid for a single part with > 65536 flows without
+                            predecessors; cluster with no more parts than XCDs
+                            and a part with > 16384 of them; else block        */
   NETSIM_EXEC_GRID = 1,  /* whole GPU on one part at a time (grid barriers)      */
   NETSIM_EXEC_BLOCK = 2,  /* one workgroup per part (workgroup barriers)         */
   NETSIM_EXEC_CLUSTER = 3 /* one leader workgroup per XCD runs parts as in block
@@ -174,6 +176,9 @@ typedef struct {
   double phase_seconds[8];
   int64_t assisted_solves;   /* NETSIM_EXEC_CLUSTER: re-solves run by the helper
                                 workgroups (counted in solves and rounds too)    */
+  int32_t layout;            /* execution layout of the last launch (NETSIM_EXEC_GRID,
+                                _BLOCK or _CLUSTER; AUTO resolved)                */
+  int32_t reserved;
 } netsim_stats;
 
 /* Fills *opt with the defaults (device 0, auto layout, no limits). */

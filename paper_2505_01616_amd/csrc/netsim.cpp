@@ -56,6 +56,7 @@ struct netsim {
   bool has_result = false;
   int64_t F = 0, L = 0, nnz = 0, nsucc = 0;
   int32_t num_parts = 0;              // independent parts (each with its own clock)
+  int32_t layout = 0;                 // execution layout of the last launch (NETSIM_EXEC_*)
   std::vector<int32_t> dev_of_flow;   // id -> device flow index
   std::vector<std::vector<int32_t>> dev_link;  // scenario, local link -> device link (-1 unused)
   std::vector<int32_t> h_cnt0;
@@ -235,8 +236,10 @@ constexpr int32_t kMaxPartsPerScen = 1024;
 // Link components per part for the incremental re-solve; more are merged
 // into the last one (a coarser partition is still safe).
 constexpr int32_t kMaxComp = 4096;
-// Cluster layout: smallest re-solve the helper workgroups take by default.
+// Cluster layout: smallest re-solve the helper workgroups take by default;
+// compute units per XCD on gfx950 (the number of leaders is CUs / this).
 constexpr int32_t kAssistMinFlows = 4096;
+constexpr int kCusPerXcd = 32;
 
 netsim_status prepare(netsim_t* h) {
   const int32_t S = (int32_t)h->scen.size();
@@ -604,16 +607,30 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
   P.assist_min = h->opt.assist_min_flows > 0 ? h->opt.assist_min_flows : kAssistMinFlows;
   const int32_t S = h->num_parts;
   int exec = h->opt.exec;
-  if (exec == NETSIM_EXEC_AUTO) {
-    // the whole GPU on one part only when its first solve alone exceeds
-    // what one workgroup solves in shared memory: more than 64 x 1024 flows
-    // without predecessors (a part whose flows chain through dependencies
-    // keeps few of them active at once, however many it has)
+  // flows without predecessors in the widest part (a part whose flows chain
+  // through dependencies keeps few of them active at once, however many it has)
+  int64_t widest = 0;
+  for (const ScenCtl& c : h->h_ctl0) {
     int64_t roots = 0;
-    if (S == 1)
-      for (int32_t c : h->h_cnt0) roots += c == 0;
-    exec = (S == 1 && roots > 65536) ? NETSIM_EXEC_GRID : NETSIM_EXEC_BLOCK;
+    for (int32_t d = c.f0; d < c.f1; ++d) roots += h->h_cnt0[(size_t)d] == 0;
+    widest = std::max(widest, roots);
   }
+  if (exec == NETSIM_EXEC_AUTO) {
+    // the whole GPU on one part when its first solve alone exceeds what one
+    // workgroup solves in shared memory (more than 64 x 1024 flows); the
+    // cluster layout when there are no more parts than XCDs (one leader
+    // each) and some part starts wide enough for re-solves the helpers
+    // speed up; otherwise one workgroup per part
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->opt.device) != hipSuccess)
+      cus = 0;
+    const int xcds = cus / kCusPerXcd;
+    if (S == 1 && widest > 65536) exec = NETSIM_EXEC_GRID;
+    else if (!solve_only && S <= xcds && widest > 16384) exec = NETSIM_EXEC_CLUSTER;
+    else exec = NETSIM_EXEC_BLOCK;
+  }
+  if (exec == NETSIM_EXEC_CLUSTER && solve_only) exec = NETSIM_EXEC_BLOCK;
+  h->layout = exec;
   // grid-barrier words and min-reduction slots start fresh in every launch
   // (a launch that continues a run must not see the last launch's counts)
   uint64_t inf_slots[8];
@@ -627,7 +644,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
   if (he != hipSuccess) return hip_fail(h, he, "hipEventCreate");
   he = hipEventRecord(e0, st);
   if (he == hipSuccess) {
-    if (exec == NETSIM_EXEC_CLUSTER && !solve_only) {
+    if (exec == NETSIM_EXEC_CLUSTER) {
       int blocks = 0;
       he = netsim_dev::cluster_capacity(h->opt.device, &blocks);
       if (he == hipSuccess && blocks < 1) he = hipErrorInvalidConfiguration;
@@ -648,12 +665,6 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
       // without predecessors (its solves may need more than the 64 x 512
       // items one 512-thread workgroup solves in shared memory); otherwise
       // 512, which spills no registers and has cheaper barriers
-      int64_t widest = 0;
-      for (const ScenCtl& c : h->h_ctl0) {
-        int64_t roots = 0;
-        for (int32_t d = c.f0; d < c.f1; ++d) roots += h->h_cnt0[(size_t)d] == 0;
-        widest = std::max(widest, roots);
-      }
       int threads = h->opt.block_threads > 0 ? h->opt.block_threads : widest > 16384 ? 1024 : 512;
       threads = std::max(64, std::min(1024, threads / 64 * 64));
       const int blocks = std::max(1, std::min<int32_t>(S, 1 << 20));
@@ -762,6 +773,7 @@ netsim_status simulate(netsim_t* h, hipStream_t st, bool resume, int64_t max_eve
     s.reselected += c.reselected;
     s.wide_solves += c.wide_solves;
     s.assisted_solves += c.assisted;
+    s.layout = h->layout;
     s.sim_time = std::max(s.sim_time, c.t);
     if (c.status != 0) s.complete = 0;
   }

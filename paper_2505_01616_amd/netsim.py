@@ -61,7 +61,8 @@ class netsim_stats(ctypes.Structure):
                 ("complete", ctypes.c_int32), ("parts", ctypes.c_int32),
                 ("sim_time", ctypes.c_double), ("device_seconds", ctypes.c_double),
                 ("upload_seconds", ctypes.c_double), ("phase_seconds", ctypes.c_double * 8),
-                ("assisted_solves", ctypes.c_int64)]
+                ("assisted_solves", ctypes.c_int64), ("layout", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
     def as_dict(self):
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}

@@ -146,3 +146,20 @@ def test_cluster_advance_in_pieces():
         assert ns.netsim_get_stats(h)["assisted_solves"] > 0
     finally:
         ld.close()
+
+
+def test_auto_picks_the_layout():
+    """AUTO: the cluster layout for the 4096-GPU all-to-all (8 parts, each
+    starting with 32k flows), one workgroup per part for many small parts,
+    the whole grid for one very wide part; solve-only runs never use the
+    cluster layout."""
+    ns, pr = _gpu()
+    _say("test_auto_picks_the_layout")
+    _, st = pr.run_program(configs.c4(4), ns.make_options(until=1e-4))
+    assert st["layout"] == ns.EXEC_CLUSTER and st["parts"] == 8
+    _, st = pr.run_program(configs.c2(2, tp_reps=6), ns.make_options())
+    assert st["layout"] == ns.EXEC_BLOCK
+    _, st = pr.run_program(configs.c4(4), ns.make_options(until=1e-4, single_clock=1))
+    assert st["layout"] == ns.EXEC_GRID and st["parts"] == 1
+    _, st = pr.run_program(configs.c4(4), ns.make_options(exec=ns.EXEC_CLUSTER, until=1e-4))
+    assert st["layout"] == ns.EXEC_CLUSTER

@@ -173,7 +173,7 @@ def test_c4_one_group_full_run():
         assert _rel(fins[0], ref.finish) < TOL
 
 
-@pytest.mark.parametrize("exec_", ["block", "grid"])
+@pytest.mark.parametrize("exec_", ["block", "grid", "cluster"])
 def test_c4_full_size_prefix(exec_):
     """Full 4096-GPU C4 (8 independent parts of 8 expert groups each),
     simulated up to the last completion among the oracle's first 150 events
@@ -191,7 +191,7 @@ def test_c4_full_size_prefix(exec_):
     ref = osim.run_flowset(fs, until=T)
     done = ref.finish[np.isfinite(ref.finish)]
     assert len(done) >= 50 and np.all(np.abs(done - T) > 1e-10 * T)
-    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
+    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID, "cluster": ns.EXEC_CLUSTER}[exec_]
     fins, stats = pr.run_program(program, ns.make_options(exec=ex, until=T))
     assert stats["complete"] == 0 and stats["parts"] == 8
     assert _rel(fins[0], ref.finish) < TOL
