@@ -92,7 +92,12 @@ typedef struct {
                                 a part has > 16384 flows without predecessors,
                                 else 512                                        */
   int32_t debug;             /* bit 0: consistency checks on the device; bit 1:
-                                phase timers (netsim_stats.phase_seconds)        */
+                                phase timers (netsim_stats.phase_seconds); test
+                                hooks of NETSIM_EXEC_CLUSTER: bit 2 makes helper
+                                workgroups leave as soon as they have no job (the
+                                leaders then solve alone), bit 3 makes their
+                                barrier give up at once (the run then fails with
+                                NETSIM_E_DEVICE, "grid barrier timed out")       */
   int32_t single_clock;      /* 1: one part (one clock) per scenario             */
   int32_t assist_min_flows;  /* NETSIM_EXEC_CLUSTER: smallest re-solve handed to the
                                 helper workgroups; 0 = 4096                      */

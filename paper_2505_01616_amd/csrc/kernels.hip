@@ -277,6 +277,11 @@ constexpr uint32_t CL_CLOSED = 0xFFFFFFFFu;
 constexpr int NOT_TAKEN = 2;              // the helpers have left: solve locally
 // A helper with no job for this long leaves (its leader then solves alone).
 constexpr uint64_t IDLE_TICKS = 6000000000ull;  // 60 s at 100 MHz
+// Test hooks (Params::debug): helpers that leave as soon as they have no job
+// (their leader then solves alone), and a helper barrier that gives up at
+// once (the launch aborts and the part reports a barrier time-out).  Both
+// only shorten the kernel's own bounded waits.
+constexpr int DEBUG_HELPERS_LEAVE = 4, DEBUG_HELPER_BARRIER_GIVES_UP = 8;
 static_assert(CL_BASE + 16 * CL_STRIDE <= BAR_WORDS, "cluster words");
 
 // Waits (one thread) until *p != v, giving up when the abort word is set or
@@ -313,7 +318,8 @@ __device__ __forceinline__ void drain() { __builtin_amdgcn_s_waitcnt(0); }
 //
 // Barrier: workgroups add one to a counter that only grows and wait until it
 // reaches (barriers passed) x (helpers), so no arrival has to reset it.  A
-// wait longer than BARRIER_TIMEOUT_TICKS raises the launch's abort word.
+// wait longer than `patience` (BARRIER_TIMEOUT_TICKS) raises the launch's
+// abort word.
 struct ClusterG {
   double* lds;
   int* ldsi;
@@ -323,6 +329,7 @@ struct ClusterG {
   uint32_t gen;
   int rank, nh;   // rank among the helpers, number of helpers
   bool ab;
+  uint64_t patience;  // barrier time-out (ticks)
   __device__ Lists* lists(ScenCtl* C) const { return &C->k; }
   __device__ int tid() const { return rank * blockDim.x + threadIdx.x; }
   __device__ int block_base() const { return rank * blockDim.x; }
@@ -350,13 +357,13 @@ struct ClusterG {
     ab = *flag != 0;
   }
   // Waits until the counter reaches target (counted modulo 2^32), giving up
-  // on the abort word or after BARRIER_TIMEOUT_TICKS (then raising it).
+  // on the abort word or after `patience` ticks (then raising it).
   __device__ __forceinline__ void wait_reach(uint32_t* p, uint32_t target) {
     const uint64_t t0 = wall_clock64();
     while ((int32_t)(__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
       __builtin_amdgcn_s_sleep(1);
       if (__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return;
-      if (wall_clock64() - t0 > BARRIER_TIMEOUT_TICKS) {
+      if (wall_clock64() - t0 > patience) {
         __hip_atomic_store(&bar[BAR_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return;
       }
@@ -1446,6 +1453,7 @@ struct Assist {
 __device__ __forceinline__ void helper_loop(const Params& P, ClusterG& cg, SolveLds& S, Tally* tl,
                                             int* box, double* tjob) {
   uint32_t* cw = cg.cw;
+  const uint64_t idle = (P.debug & DEBUG_HELPERS_LEAVE) ? 0 : IDLE_TICKS;
   uint32_t seen = 0;
   for (;;) {
     if (threadIdx.x == 0) {
@@ -1459,7 +1467,7 @@ __device__ __forceinline__ void helper_loop(const Params& P, ClusterG& cg, Solve
           leave = 1;
           break;
         }
-        if (wall_clock64() - t0 > IDLE_TICKS) {
+        if (wall_clock64() - t0 > idle) {
           uint32_t e = seen;
           if (__hip_atomic_compare_exchange_strong(&cw[CL_MB], &e, CL_CLOSED, __ATOMIC_RELAXED,
                                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
@@ -2194,7 +2202,8 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
   __syncthreads();
   if (rank != 0) {
     if (nh > 0) {
-      ClusterG cg{lds, ldsi, &flag, P.bar, cw, 0u, rank - 1, nh, false};
+      const uint64_t patience = (P.debug & DEBUG_HELPER_BARRIER_GIVES_UP) ? 0 : BARRIER_TIMEOUT_TICKS;
+      ClusterG cg{lds, ldsi, &flag, P.bar, cw, 0u, rank - 1, nh, false, patience};
       helper_loop(P, cg, *reinterpret_cast<SolveLds*>(pool), &tally, box, tjob);
     }
     return;

@@ -163,3 +163,40 @@ def test_auto_picks_the_layout():
     assert st["layout"] == ns.EXEC_GRID and st["parts"] == 1
     _, st = pr.run_program(configs.c4(4), ns.make_options(exec=ns.EXEC_CLUSTER, until=1e-4))
     assert st["layout"] == ns.EXEC_CLUSTER
+
+
+def test_cluster_leader_solves_alone_when_helpers_leave():
+    """Test hook (debug bit 2): helpers leave as soon as they have no job, so
+    a leader's posts find the mailbox closed and it solves its re-solves
+    itself; the result is still the block layout's, bit for bit."""
+    ns, pr = _gpu()
+    _say("test_cluster_leader_solves_alone_when_helpers_leave")
+    program = configs.c2(2, tp_reps=6)
+    a, sa = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK, single_clock=1))
+    b, sb = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=1,
+                                                    single_clock=1, debug=4))
+    assert np.array_equal(a[0], b[0]) and sb["complete"] == 1
+    for k in SAME:
+        assert sa[k] == sb[k], k
+    assert sb["assisted_solves"] < sb["solves"] // 2
+    _say("  assisted", sb["assisted_solves"], "of", sb["solves"])
+
+
+def test_cluster_helper_barrier_timeout_is_an_error():
+    """Test hook (debug bit 3): the helpers' barrier gives up at once, which
+    aborts the launch; every wait of the kernel ends, the run reports the
+    time-out as an error, and a later run is whole again."""
+    ns, pr = _gpu()
+    _say("test_cluster_helper_barrier_timeout_is_an_error")
+    program = configs.c2(2, tp_reps=6)
+    ref, _ = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK, single_clock=1))
+    ld = pr.load_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=1,
+                                                  single_clock=1, debug=8))
+    try:
+        with pytest.raises(ns.NetsimError, match="barrier timed out"):
+            ns.netsim_run(ld.handle)
+    finally:
+        ld.close()
+    fins, st = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=1,
+                                                       single_clock=1))
+    assert np.array_equal(fins[0], ref[0]) and st["complete"] == 1 and st["assisted_solves"] > 0
