@@ -308,13 +308,16 @@ __device__ __forceinline__ void drain() { __builtin_amdgcn_s_waitcnt(0); }
 // time with a barrier of their own.
 //
 // Everything the helpers and their leader share lives in device memory and
-// is exchanged inside one XCD, whose L2 they all use.  So a release needs no
-// L2 write-back (what the agent-scope release adds, for other XCDs): each
-// wave drains its stores and atomics (they are then in that L2, or performed
-// at agent scope) before its workgroup signals.  An acquire stays
-// agent-scope: it drops this CU's L1 and the L2's clean copies, which the
-// agent-scope atomics on link state may have left stale (measured: dropping
-// only the L1 reads stale link state).
+// is exchanged inside one XCD, whose L2 they all use.  So a helper's release
+// needs no L2 write-back (what the agent-scope release adds, for other XCDs):
+// each wave drains its stores and atomics (they are then in that L2, or
+// performed at agent scope) before its workgroup signals.  Within a job the
+// helpers update link state only with agent-scope atomics and stamps only
+// with plain stores.  An acquire stays agent-scope: it drops this CU's L1 and
+// the L2's clean copies (measured: dropping only the L1 reads stale link
+// state).  The leader hands link state over with agent-scope stores (or,
+// when the state lives in global memory, after a full agent-scope release),
+// so the helpers' atomics never follow plain stores to the same words.
 //
 // Barrier: workgroups add one to a counter that only grows and wait until it
 // reaches (barriers passed) x (helpers), so no arrival has to reset it.  A
@@ -1380,9 +1383,11 @@ struct Assist {
     const int T = blockDim.x;
     const int l0 = C->l0, nl = C->l1 - C->l0;
     if constexpr (LK::kTable) {
+      // agent-scope stores, as the helpers' updates of these words are
       for (int i = threadIdx.x; i < nl; i += T) {
-        P.lst[2 * (l0 + i)] = lk.R[i];
-        P.lst[2 * (l0 + i) + 1] = (int64_t)lk.n[i];
+        __hip_atomic_store(&P.lst[2 * (l0 + i)], lk.R[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&P.lst[2 * (l0 + i) + 1], (int64_t)lk.n[i], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
       }
     }
     drain();
@@ -1397,7 +1402,11 @@ struct Assist {
       __hip_atomic_store(&cw[CL_SNEW], (uint32_t)s_new, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(reinterpret_cast<uint64_t*>(cw + CL_T), (uint64_t)__double_as_longlong(t),
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      drain();  // the job and the link state reach the XCD's L2 before the post
+      // link state in global memory was last updated by this workgroup's
+      // workgroup-scope atomics: a full agent-scope release (an L2
+      // write-back) puts it where the helpers' agent-scope atomics act on it;
+      // a copied-out state was stored at agent scope and is drained already
+      if constexpr (!LK::kTable) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
       uint32_t expect = seq;
       if (__hip_atomic_compare_exchange_strong(&cw[CL_MB], &expect, seq + 1, __ATOMIC_RELAXED,
                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
