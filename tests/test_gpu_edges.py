@@ -32,6 +32,14 @@ def _gpu():
 def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
+def _layout(ns, name):
+    """Options of an execution layout; the cluster layout hands every
+    re-solve to the helper workgroups (assist_min_flows = 1)."""
+    if name == "cluster":
+        return dict(exec=ns.EXEC_CLUSTER, assist_min_flows=1)
+    return dict(exec={"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[name])
+
+
 
 def _rel(a, b):
     a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
@@ -105,15 +113,15 @@ def test_degenerate_cases():
         assert _rel(fins[s], osim.run_scenario(sc).finish) < TOL
 
 
-@pytest.mark.parametrize("exec_", ["block", "grid"])
+@pytest.mark.parametrize("exec_", ["block", "grid", "cluster"])
 def test_long_paths(exec_):
     """Paths of up to 14 links: beyond the 16-byte path record."""
     ns, pr = _gpu()
     _say(f"test_long_paths exec={exec_}")
     scs = [micro.random_dynamic(s, max_links=14, max_flows=16).scenarios[0] for s in range(60)]
     assert max(max(len(op.path) for op in sc.ops if hasattr(op, "path")) for sc in scs) > 6
-    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
-    fins, st = pr.run_program(Program("long", scs), ns.make_options(exec=ex, single_clock=1))
+    ex = _layout(ns, exec_)
+    fins, st = pr.run_program(Program("long", scs), ns.make_options(**ex, single_clock=1))
     for s, sc in enumerate(scs):
         ref = osim.run_scenario(sc)
         assert _rel(fins[s], ref.finish) < TOL, s

@@ -35,6 +35,14 @@ def _gpu():
 def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
+def _layout(ns, name):
+    """Options of an execution layout; the cluster layout hands every
+    re-solve to the helper workgroups (assist_min_flows = 1)."""
+    if name == "cluster":
+        return dict(exec=ns.EXEC_CLUSTER, assist_min_flows=1)
+    return dict(exec={"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[name])
+
+
 
 def _rel(a, b):
     a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
@@ -72,13 +80,13 @@ def _scenarios():
 
 
 @pytest.mark.parametrize("single_clock", [0, 1])
-@pytest.mark.parametrize("exec_", ["block", "grid"])
+@pytest.mark.parametrize("exec_", ["block", "grid", "cluster"])
 def test_tree_hier_latency(exec_, single_clock):
     ns, pr, _ = _gpu()
     _say(f"test_tree_hier_latency exec={exec_} single_clock={single_clock}")
     scs = _scenarios()
-    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
-    fins, st = pr.run_program(Program("next4", scs), ns.make_options(exec=ex, single_clock=single_clock))
+    ex = _layout(ns, exec_)
+    fins, st = pr.run_program(Program("next4", scs), ns.make_options(**ex, single_clock=single_clock))
     assert st["complete"] == 1
     for s, sc in enumerate(scs):
         ref = osim.run_scenario(sc)
@@ -122,7 +130,7 @@ def test_training_step_with_latency(alg):
     assert _rel([sync[s] for s in sorted(sync)], [ref.stream_sync[s] for s in sorted(sync)]) < TOL
 
 
-@pytest.mark.parametrize("exec_", ["block", "grid"])
+@pytest.mark.parametrize("exec_", ["block", "grid", "cluster"])
 def test_latency_pieces_and_rollback(exec_):
     """With latencies: advancing in pieces equals one run bit for bit; moving
     a finished flow's start back in time, then advancing, equals a fresh
@@ -130,8 +138,8 @@ def test_latency_pieces_and_rollback(exec_):
     ns, pr, _ = _gpu()
     _say(f"test_latency_pieces_and_rollback exec={exec_}")
     program = Program("next4", _scenarios()[:2])
-    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
-    opt = dict(exec=ex)
+    ex = _layout(ns, exec_)
+    opt = dict(ex)
 
     def fresh(updates):
         ld = pr.load_program(program, ns.make_options(**opt))

@@ -35,6 +35,14 @@ def _gpu():
 def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
+def _layout(ns, name):
+    """Options of an execution layout; the cluster layout hands every
+    re-solve to the helper workgroups (assist_min_flows = 1)."""
+    if name == "cluster":
+        return dict(exec=ns.EXEC_CLUSTER, assist_min_flows=1)
+    return dict(exec={"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[name])
+
+
 
 def _rel(a, b):
     a, b = np.asarray(a), np.asarray(b)
@@ -63,15 +71,15 @@ def _oracle(sc, updates):
     return osim.run_flowset(fs).finish
 
 
-@pytest.mark.parametrize("exec_", ["block", "grid"])
+@pytest.mark.parametrize("exec_", ["block", "grid", "cluster"])
 def test_advance_in_pieces_equals_one_run(exec_):
     ns, pr = _gpu()
     _say(f"test_advance_in_pieces exec={exec_}")
     program = configs.c2(2, tp_reps=6)
-    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
-    ref = _fresh(program, {}, exec=ex)
+    ex = _layout(ns, exec_)
+    ref = _fresh(program, {}, **ex)
     T = float(np.nanmax(ref))
-    ld = pr.load_program(program, ns.make_options(exec=ex))
+    ld = pr.load_program(program, ns.make_options(**ex))
     try:
         h = ld.handle
         for frac in (0.2, 0.5, 0.8):
@@ -86,7 +94,7 @@ def test_advance_in_pieces_equals_one_run(exec_):
     finally:
         ld.close()
     # by numbers of events
-    ld = pr.load_program(program, ns.make_options(exec=ex))
+    ld = pr.load_program(program, ns.make_options(**ex))
     try:
         h = ld.handle
         for _ in range(100):

@@ -29,6 +29,14 @@ def _gpu():
 def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
+def _layout(ns, name):
+    """Options of an execution layout; the cluster layout hands every
+    re-solve to the helper workgroups (assist_min_flows = 1)."""
+    if name == "cluster":
+        return dict(exec=ns.EXEC_CLUSTER, assist_min_flows=1)
+    return dict(exec={"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[name])
+
+
 
 def _rel(a, b):
     a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
@@ -76,13 +84,13 @@ def test_every_collective_kind(mode):
 
 
 @pytest.mark.parametrize("single_clock", [0, 1])
-@pytest.mark.parametrize("exec_", ["block", "grid"])
+@pytest.mark.parametrize("exec_", ["block", "grid", "cluster"])
 def test_small_training_step(exec_, single_clock):
     ns, _ = _gpu()
     _say(f"test_small_training_step exec={exec_} single_clock={single_clock}")
-    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
+    ex = _layout(ns, exec_)
     st, ref = _check(training_step(seed=6, tp=4, pp=2, dp=2, microbatches=3, layers=2),
-                     exec=ex, single_clock=single_clock)
+                     **ex, single_clock=single_clock)
     if single_clock:
         assert st["events"] == ref.events and st["solves"] == ref.solves
 
@@ -106,7 +114,7 @@ def test_stream_calls_after_a_run_are_refused():
         ld.close()
 
 
-@pytest.mark.parametrize("exec_", ["block", "grid"])
+@pytest.mark.parametrize("exec_", ["block", "grid", "cluster"])
 def test_compute_duration_change_rolls_back(exec_):
     """A computation found longer than assumed after the simulation passed it
     (the situation time rollback exists for): its flow's start (the
@@ -117,11 +125,11 @@ def test_compute_duration_change_rolls_back(exec_):
     ns, ptr = _gpu()
     _say(f"test_compute_duration_change_rolls_back exec={exec_}")
     tr = training_step(seed=8, tp=4, pp=2, dp=2, microbatches=3, layers=2)
-    ex = {"block": ns.EXEC_BLOCK, "grid": ns.EXEC_GRID}[exec_]
+    ex = _layout(ns, exec_)
     computes = [k for k, op in enumerate(tr.ops) if type(op).__name__ == "Compute"]
     k = computes[len(computes) // 3]
     new_d = tr.ops[k].duration + 4e-4
-    ld = ptr.load_trace(tr, ns.make_options(exec=ex))
+    ld = ptr.load_trace(tr, ns.make_options(**ex))
     try:
         h = ld.handle
         ns.netsim_advance(h)
@@ -135,7 +143,7 @@ def test_compute_duration_change_rolls_back(exec_):
         ld.close()
     tr2 = copy.deepcopy(tr)
     tr2.ops[k].duration = new_d
-    fin2, _, _, _ = ptr.run_trace(tr2, ns.make_options(exec=ex))
+    fin2, _, _, _ = ptr.run_trace(tr2, ns.make_options(**ex))
     assert np.array_equal(got, fin2)
     assert np.sum(got != before) > 0
     ref = otl.simulate(tr2)
