@@ -7,7 +7,7 @@ events, each ending in a max-min rate solve).  The simulator splits the
 workload into its independent parts (the eight groups of expert-parallel
 ranks that share fabric links) and runs each with its own clock; by default
 (AUTO) each part gets the workgroups of one XCD: a leader running its event
-loop and 31 helpers solving its large re-solves (--exec block: one workgroup
+loop and 15 helpers solving its large re-solves (--exec block: one workgroup
 per part).  Events and solves are counted per part.  Each step is one kernel
 launch, timed with HIP events on the launch stream; W warm-up steps run
 first.  Inputs (flows, routes, capacities) are resident in HBM

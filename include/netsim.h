@@ -66,9 +66,9 @@ enum {
   NETSIM_EXEC_BLOCK = 2,  /* one workgroup per part (workgroup barriers)         */
   NETSIM_EXEC_CLUSTER = 3 /* one leader workgroup per XCD runs parts as in block
                              mode and hands re-solves of at least
-                             assist_min_flows flows to the other workgroups of its
-                             XCD (one per CU, cooperative launch); results equal
-                             block mode's bit for bit.  Rate solves without an
+                             assist_min_flows flows to assist_helpers other
+                             workgroups of its XCD (one per CU, cooperative
+                             launch); results equal block mode's bit for bit.  Rate solves without an
                              event loop (netsim_solve_rates) run as in block mode */
 };
 
@@ -101,6 +101,8 @@ typedef struct {
   int32_t single_clock;      /* 1: one part (one clock) per scenario             */
   int32_t assist_min_flows;  /* NETSIM_EXEC_CLUSTER: smallest re-solve handed to the
                                 helper workgroups; 0 = 4096                      */
+  int32_t assist_helpers;    /* NETSIM_EXEC_CLUSTER: helper workgroups per leader,
+                                at most the other workgroups of its XCD; 0 = 15  */
 } netsim_options;
 
 /*

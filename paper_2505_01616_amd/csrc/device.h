@@ -77,6 +77,7 @@ struct Params {
   int32_t max_rounds;
   int32_t debug;           // run internal consistency checks
   int32_t assist_min;      // cluster kernel: smallest re-solve handed to helper workgroups
+  int32_t assist_helpers;  // cluster kernel: helper workgroups per leader (at most)
   double scale;            // fixed-point units per B/s (a power of two)
   double inv_scale;
   // static flow / link data (device order)

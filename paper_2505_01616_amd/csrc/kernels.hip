@@ -2173,9 +2173,10 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
 // One workgroup per CU, 1024 threads.  Every workgroup registers on its XCD;
 // the first of each XCD leads: it claims parts one at a time and runs their
 // event loops as the block kernel does, handing re-solves of at least
-// P.assist_min flows to the other workgroups of its XCD (its helpers).  With
-// no helpers (a lone workgroup on its XCD, or registration timed out) a
-// leader solves everything itself.  Every part is claimed by exactly one
+// P.assist_min flows to up to P.assist_helpers other workgroups of its XCD
+// (its helpers; the XCD's remaining workgroups return at once).  With no
+// helpers (a lone workgroup on its XCD, or registration timed out) a leader
+// solves everything itself.  Every part is claimed by exactly one
 // leader, whatever the number of leaders.
 __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
   __shared__ double lds[32];
@@ -2203,14 +2204,17 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
     const uint32_t on_xcd = __hip_atomic_load(&cw[CL_REG], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     box[0] = (int)x;
     box[1] = (int)rank;
-    box[2] = ok ? (int)on_xcd - 1 : 0;  // helpers on the XCD
+    // helpers: the XCD's other workgroups, at most P.assist_helpers of them
+    // (every helper arrives on one counter at each barrier, and arrivals on
+    // one word serialise: fewer helpers, each with more flows, are faster)
+    box[2] = ok ? min((int)on_xcd - 1, max(P.assist_helpers, 0)) : 0;
   }
   __syncthreads();
   const int x = box[0], rank = box[1], nh = box[2];
   uint32_t* cw = P.bar + CL_BASE + CL_STRIDE * x;
   __syncthreads();
-  if (rank != 0) {
-    if (nh > 0) {
+  if (rank != 0) {  // workgroups beyond the helpers have nothing to do
+    if (nh > 0 && rank <= nh) {
       const uint64_t patience = (P.debug & DEBUG_HELPER_BARRIER_GIVES_UP) ? 0 : BARRIER_TIMEOUT_TICKS;
       ClusterG cg{lds, ldsi, &flag, P.bar, cw, 0u, rank - 1, nh, false, patience};
       helper_loop(P, cg, *reinterpret_cast<SolveLds*>(pool), &tally, box, tjob);

@@ -239,6 +239,9 @@ constexpr int32_t kMaxComp = 4096;
 // Cluster layout: smallest re-solve the helper workgroups take by default;
 // compute units per XCD on gfx950 (the number of leaders is CUs / this).
 constexpr int32_t kAssistMinFlows = 4096;
+// helper workgroups per leader by default (measured on the 4096-GPU
+// all-to-all: 7 -> 10.7 s, 11-17 -> 9.7-10.1 s, 23 -> 10.0 s, 31 -> 10.9 s)
+constexpr int32_t kAssistHelpers = 15;
 constexpr int kCusPerXcd = 32;
 
 netsim_status prepare(netsim_t* h) {
@@ -605,6 +608,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
   P.max_rounds = h->opt.max_rounds > 0 ? h->opt.max_rounds
                                        : (int32_t)std::min<int64_t>(h->F + 1, std::numeric_limits<int32_t>::max());
   P.assist_min = h->opt.assist_min_flows > 0 ? h->opt.assist_min_flows : kAssistMinFlows;
+  P.assist_helpers = h->opt.assist_helpers > 0 ? h->opt.assist_helpers : kAssistHelpers;
   const int32_t S = h->num_parts;
   int exec = h->opt.exec;
   // flows without predecessors in the widest part (a part whose flows chain

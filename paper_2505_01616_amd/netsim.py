@@ -35,7 +35,7 @@ class netsim_options(ctypes.Structure):
                 ("max_events", ctypes.c_int64), ("until", ctypes.c_double),
                 ("max_rounds", ctypes.c_int32), ("block_threads", ctypes.c_int32),
                 ("debug", ctypes.c_int32), ("single_clock", ctypes.c_int32),
-                ("assist_min_flows", ctypes.c_int32)]
+                ("assist_min_flows", ctypes.c_int32), ("assist_helpers", ctypes.c_int32)]
 
 
 class netsim_topology(ctypes.Structure):
@@ -163,11 +163,12 @@ def netsim_default_options() -> netsim_options:
 
 
 def make_options(device=0, exec=EXEC_AUTO, max_events=0, until=math.inf, max_rounds=0,
-                 block_threads=0, debug=0, single_clock=0, assist_min_flows=0) -> netsim_options:
+                 block_threads=0, debug=0, single_clock=0, assist_min_flows=0,
+                 assist_helpers=0) -> netsim_options:
     o = netsim_default_options()
     o.device, o.exec, o.max_events, o.until = device, exec, max_events, until
     o.max_rounds, o.block_threads, o.debug = max_rounds, block_threads, debug
-    o.single_clock, o.assist_min_flows = single_clock, assist_min_flows
+    o.single_clock, o.assist_min_flows, o.assist_helpers = single_clock, assist_min_flows, assist_helpers
     return o
 
 

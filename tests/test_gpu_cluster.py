@@ -47,11 +47,11 @@ def _rel(a, b):
     return float(np.max(np.abs(a[fa] - b[fa]) / np.maximum(np.abs(b[fa]), 1e-300))) if fa.any() else 0.0
 
 
-def _both(program, assist_min, **opt):
+def _both(program, assist_min, helpers=0, **opt):
     ns, pr = _gpu()
     a, sa = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK, **opt))
     b, sb = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=assist_min,
-                                                    **opt))
+                                                    assist_helpers=helpers, **opt))
     for x, y in zip(a, b):
         assert np.array_equal(x, y, equal_nan=True)
     for k in SAME:
@@ -63,11 +63,15 @@ def _both(program, assist_min, **opt):
 
 @pytest.mark.parametrize("single_clock", [0, 1])
 @pytest.mark.parametrize("assist_min", [1, 256])
-def test_cluster_equals_block(single_clock, assist_min):
+@pytest.mark.parametrize("helpers", [0, 1, 31])
+def test_cluster_equals_block(single_clock, assist_min, helpers):
     """Tensor-parallel rings and pipeline sends (several parts, or one):
-    every re-solve (assist_min = 1) or the larger ones handed to helpers."""
-    _say(f"test_cluster_equals_block single_clock={single_clock} assist_min={assist_min}")
-    sa, sb = _both(configs.c2(2, tp_reps=6), assist_min, single_clock=single_clock)
+    every re-solve (assist_min = 1) or the larger ones handed to the
+    default number of helpers, to one, or to every other workgroup of the
+    XCD."""
+    _say(f"test_cluster_equals_block single_clock={single_clock} assist_min={assist_min} "
+         f"helpers={helpers}")
+    sa, sb = _both(configs.c2(2, tp_reps=6), assist_min, helpers, single_clock=single_clock)
     assert 0 <= sb["assisted_solves"] <= sb["solves"]
     if assist_min == 1:
         assert sb["assisted_solves"] > 0
