@@ -179,7 +179,9 @@ typedef struct {
    * [0] next-event search, [1] settling completions and releases, [2] solve
    * set-up and the share table of every round, [3] share/blocking sweep, [4]
    * wait after it, [5] freezing sweep, [6] wait after it, [7] choosing the
-   * flows to re-solve. */
+   * flows to re-solve.  In the cluster layout a re-solve run by helper
+   * workgroups counts with the first helper's times in [2]-[6]; the hand-over
+   * itself (copying link state, waking the helpers) is not counted. */
   double phase_seconds[8];
   int64_t assisted_solves;   /* NETSIM_EXEC_CLUSTER: re-solves run by the helper
                                 workgroups (counted in solves and rounds too)    */

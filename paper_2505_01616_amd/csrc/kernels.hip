@@ -273,6 +273,7 @@ constexpr int CL_RC = 33;                 // job status (first helper)
 constexpr int CL_ROUNDS = 34, CL_FSW = 36;  // job rounds and flows swept (int64, first helper)
 constexpr int CL_ISW = 48;                // incidences swept (int64, summed over the helpers)
 constexpr int CL_CNT = 64;               // barrier among the helpers (arrivals, growing)
+constexpr int CL_CLK = 96;                // job phase times of the first helper (int64 [8])
 constexpr uint32_t CL_CLOSED = 0xFFFFFFFFu;
 constexpr int NOT_TAKEN = 2;              // the helpers have left: solve locally
 // A helper with no job for this long leaves (its leader then solves alone).
@@ -513,6 +514,10 @@ struct Clock {
       acc[k] += now - acc[8];
       acc[8] = now;
     }
+  }
+  // restarts the current lap without counting the time since the last one
+  __device__ __forceinline__ void skip() {
+    if (on) acc[8] = wall_clock64();
   }
 };
 
@@ -1519,7 +1524,8 @@ __device__ __forceinline__ void helper_loop(const Params& P, ClusterG& cg, Solve
                           : Slots{P.act0 + f0, P.tau0 + f0, P.srate0 + f0};
       const Resel rs{sl, P.arrslot + f0, s_new, t};
       LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
-      Clock clk(false, tl->clk);
+      // the first helper times the job's phases (debug bit 1) for its leader
+      Clock clk((P.debug & 2) && cg.rank == 0 && threadIdx.x == 0, tl->clk);
       rc = solve_lds(cg, P, lk, C, P.arr + f0, n, rr, ff, is, clk, S, true, &rs);
     }
     long w = (long)is;
@@ -1529,6 +1535,10 @@ __device__ __forceinline__ void helper_loop(const Params& P, ClusterG& cg, Solve
       __hip_atomic_fetch_add(reinterpret_cast<uint64_t*>(cw + CL_ISW), (uint64_t)w, __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
     if (cg.rank == 0 && threadIdx.x == 0) {
+      if (P.debug & 2)
+        for (int k = 2; k < 7; ++k)
+          __hip_atomic_store(reinterpret_cast<uint64_t*>(cw + CL_CLK) + k, tl->clk[k], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&cw[CL_RC], (uint32_t)rc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(reinterpret_cast<uint64_t*>(cw + CL_ROUNDS), (uint64_t)rr, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
@@ -1948,7 +1958,17 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
             // also take the flows back and write their slots
             if (C->lds_paths && as->takes(nSel)) {
               ar = as->solve(g, P, lk, C, sc, nSel, ab, slots0, t, rounds, fsw, isw);
-              if (ar != NOT_TAKEN && threadIdx.x == 0) tl->asst += 1;
+              if (ar != NOT_TAKEN) {
+                // phase times: the first helper's, in place of the hand-over
+                clk.skip();
+                if (threadIdx.x == 0) {
+                  tl->asst += 1;
+                  if (P.debug & 2)
+                    for (int k = 2; k < 7; ++k)
+                      tl->clk[k] += __hip_atomic_load(reinterpret_cast<uint64_t*>(as->cw + CL_CLK) + k,
+                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+              }
             }
           }
           if (ar != NOT_TAKEN) {

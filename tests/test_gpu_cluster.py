@@ -204,3 +204,19 @@ def test_cluster_helper_barrier_timeout_is_an_error():
     fins, st = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=1,
                                                        single_clock=1))
     assert np.array_equal(fins[0], ref[0]) and st["complete"] == 1 and st["assisted_solves"] > 0
+
+
+def test_cluster_phase_times_count_the_helpers():
+    """Phase timers (debug bit 1): a re-solve run by the helpers counts with
+    the first helper's phase times, so the solve phases are not empty and the
+    phases add up to no more than the device time of every part."""
+    ns, pr = _gpu()
+    _say("test_cluster_phase_times_count_the_helpers")
+    program = configs.c2(2, tp_reps=6)
+    _, st = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=1,
+                                                    single_clock=1, debug=2))
+    ph = st["phase_seconds"]
+    assert st["assisted_solves"] > 0
+    assert ph[3] > 0 and ph[5] > 0 and ph[0] > 0
+    assert sum(ph) <= st["device_seconds"] * st["parts"] * 1.01
+    _say("  phases", [round(x, 5) for x in ph], "device", st["device_seconds"])
