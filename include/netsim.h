@@ -60,15 +60,17 @@ enum { NETSIM_MODE_CHAINED = 0, NETSIM_MODE_FLAT = 1, NETSIM_MODE_AGGREGATED = 2
 /* Execution layout (netsim_options.exec). */
 enum {
   NETSIM_EXEC_AUTO = 0,  /* grid for a single part with > 65536 flows without
-                            predecessors; cluster with no more parts than XCDs
+                            predecessors; cluster with at most 4 parts per XCD
                             and a part with > 16384 of them; else block        */
   NETSIM_EXEC_GRID = 1,  /* whole GPU on one part at a time (grid barriers)      */
   NETSIM_EXEC_BLOCK = 2,  /* one workgroup per part (workgroup barriers)         */
-  NETSIM_EXEC_CLUSTER = 3 /* one leader workgroup per XCD runs parts as in block
-                             mode and hands re-solves of at least
+  NETSIM_EXEC_CLUSTER = 3 /* leader workgroups (one per XCD, or up to 4 per XCD
+                             when there are more parts than XCDs) run parts as
+                             in block mode and hand re-solves of at least
                              assist_min_flows flows to assist_helpers other
-                             workgroups of its XCD (one per CU, cooperative
-                             launch); results equal block mode's bit for bit.  Rate solves without an
+                             workgroups of their XCD (one workgroup per CU,
+                             cooperative launch); results equal block mode's
+                             bit for bit.  Rate solves without an
                              event loop (netsim_solve_rates) run as in block mode */
 };
 
@@ -102,7 +104,8 @@ typedef struct {
   int32_t assist_min_flows;  /* NETSIM_EXEC_CLUSTER: smallest re-solve handed to the
                                 helper workgroups; 0 = 4096                      */
   int32_t assist_helpers;    /* NETSIM_EXEC_CLUSTER: helper workgroups per leader,
-                                at most the other workgroups of its XCD; 0 = 15  */
+                                at most the other workgroups of its cluster (an
+                                XCD's workgroups shared among its leaders); 0 = 15 */
 } netsim_options;
 
 /*

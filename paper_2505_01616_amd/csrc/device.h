@@ -78,6 +78,7 @@ struct Params {
   int32_t debug;           // run internal consistency checks
   int32_t assist_min;      // cluster kernel: smallest re-solve handed to helper workgroups
   int32_t assist_helpers;  // cluster kernel: helper workgroups per leader (at most)
+  int32_t clusters_per_xcd;  // cluster kernel: leaders (with their helpers) per XCD
   double scale;            // fixed-point units per B/s (a power of two)
   double inv_scale;
   // static flow / link data (device order)
@@ -125,7 +126,7 @@ struct Params {
 };
 
 // Words of Params::bar, cleared before every launch.
-constexpr int BAR_WORDS = 3072;
+constexpr int BAR_WORDS = 9216;
 
 hipError_t launch_block(const Params& p, int blocks, int threads, hipStream_t s);
 hipError_t launch_grid(const Params& p, int blocks, int threads, hipStream_t s);

@@ -259,11 +259,14 @@ struct GridG {
   }
 };
 
-// Cluster kernel words: XCD x owns CL_STRIDE words from CL_BASE + CL_STRIDE*x
+// Cluster kernel words.  XCD x counts its workgroups in XREG_BASE + 16x; its
+// workgroups form up to CL_MAXC clusters (a leader and its helpers), and
+// cluster k of XCD x owns CL_STRIDE words from CL_BASE + CL_STRIDE*(x*CL_MAXC + k)
 // (offsets below, 64-byte lines apart where several writers meet).
 constexpr int BAR_NEXT = 48;  // next part to be claimed by a leader
+constexpr int XREG_BASE = 672;
+constexpr int CL_MAXC = 4;
 constexpr int CL_BASE = 1024, CL_STRIDE = 128;
-constexpr int CL_REG = 0;                 // workgroups registered on the XCD
 constexpr int CL_MB = 16;                 // jobs posted so far, or CL_CLOSED
 constexpr int CL_SC = 17, CL_N = 18;      // posted job: part, number of flows,
 constexpr int CL_AB = 19, CL_SNEW = 20;   //   slot buffer, first slot activated at this event,
@@ -283,7 +286,8 @@ constexpr uint64_t IDLE_TICKS = 6000000000ull;  // 60 s at 100 MHz
 // once (the launch aborts and the part reports a barrier time-out).  Both
 // only shorten the kernel's own bounded waits.
 constexpr int DEBUG_HELPERS_LEAVE = 4, DEBUG_HELPER_BARRIER_GIVES_UP = 8;
-static_assert(CL_BASE + 16 * CL_STRIDE <= BAR_WORDS, "cluster words");
+static_assert(XREG_BASE + 16 * 16 <= CL_BASE, "registration words");
+static_assert(CL_BASE + 16 * CL_MAXC * CL_STRIDE <= BAR_WORDS, "cluster words");
 
 // Waits (one thread) until *p != v, giving up when the abort word is set or
 // after `ticks` (then raising it).  Returns false if it gave up.
@@ -2190,14 +2194,16 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   }
 }
 
-// One workgroup per CU, 1024 threads.  Every workgroup registers on its XCD;
-// the first of each XCD leads: it claims parts one at a time and runs their
-// event loops as the block kernel does, handing re-solves of at least
-// P.assist_min flows to up to P.assist_helpers other workgroups of its XCD
-// (its helpers; the XCD's remaining workgroups return at once).  With no
-// helpers (a lone workgroup on its XCD, or registration timed out) a leader
-// solves everything itself.  Every part is claimed by exactly one
-// leader, whatever the number of leaders.
+// One workgroup per CU, 1024 threads.  Every workgroup registers on its XCD,
+// whose workgroups form P.clusters_per_xcd clusters of consecutive ranks (the
+// last takes the remainder).  The first workgroup of a cluster leads: it
+// claims parts one at a time and runs their event loops as the block kernel
+// does, handing re-solves of at least P.assist_min flows to up to
+// P.assist_helpers other workgroups of its cluster (its helpers; the
+// cluster's remaining workgroups return at once).  With no helpers (a lone
+// workgroup, or registration timed out) a leader solves everything itself.
+// Every part is claimed by exactly one leader, whatever the number of
+// leaders.
 __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
   __shared__ double lds[32];
   __shared__ int ldsi[128];
@@ -2211,8 +2217,8 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
   static_assert(sizeof(SolveLds) <= POOL_BYTES, "helper pool");
   if (threadIdx.x == 0) {
     const uint32_t x = xcc_id();
-    uint32_t* cw = P.bar + CL_BASE + CL_STRIDE * x;
-    const uint32_t rank = __hip_atomic_fetch_add(&cw[CL_REG], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t* xreg = P.bar + XREG_BASE + 16 * x;
+    const uint32_t rank = __hip_atomic_fetch_add(xreg, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t prev =
         __hip_atomic_fetch_add(&P.bar[BAR_REG], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     bool ok = true;
@@ -2221,17 +2227,23 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
     else
       ok = wait_ne(P.bar, &P.bar[BAR_REG_GEN], 0u, BARRIER_TIMEOUT_TICKS);
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    const uint32_t on_xcd = __hip_atomic_load(&cw[CL_REG], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    box[0] = (int)x;
-    box[1] = (int)rank;
-    // helpers: the XCD's other workgroups, at most P.assist_helpers of them
-    // (every helper arrives on one counter at each barrier, and arrivals on
-    // one word serialise: fewer helpers, each with more flows, are faster)
-    box[2] = ok ? min((int)on_xcd - 1, max(P.assist_helpers, 0)) : 0;
+    const int on_xcd = (int)__hip_atomic_load(xreg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // clusters of consecutive ranks; without a complete registration every
+    // workgroup is its own leader's only member (no helpers)
+    const int nc = ok ? max(1, min(min(P.clusters_per_xcd, CL_MAXC), on_xcd)) : 1;
+    const int size = max(on_xcd / nc, 1);
+    const int cid = min((int)rank / size, nc - 1);
+    const int members = cid == nc - 1 ? on_xcd - cid * size : size;
+    box[0] = (int)x * CL_MAXC + cid;
+    box[1] = (int)rank - cid * size;  // rank in the cluster
+    // helpers: the cluster's other workgroups, at most P.assist_helpers of
+    // them (every helper arrives on one counter at each barrier, and arrivals
+    // on one word serialise: fewer helpers, each with more flows, are faster)
+    box[2] = ok ? min(members - 1, max(P.assist_helpers, 0)) : 0;
   }
   __syncthreads();
-  const int x = box[0], rank = box[1], nh = box[2];
-  uint32_t* cw = P.bar + CL_BASE + CL_STRIDE * x;
+  const int cl = box[0], rank = box[1], nh = box[2];
+  uint32_t* cw = P.bar + CL_BASE + CL_STRIDE * cl;
   __syncthreads();
   if (rank != 0) {  // workgroups beyond the helpers have nothing to do
     if (nh > 0 && rank <= nh) {

@@ -242,6 +242,8 @@ constexpr int32_t kAssistMinFlows = 4096;
 // helper workgroups per leader by default (measured on the 4096-GPU
 // all-to-all: 7 -> 10.7 s, 11-17 -> 9.7-10.1 s, 23 -> 10.0 s, 31 -> 10.9 s)
 constexpr int32_t kAssistHelpers = 15;
+// leaders per XCD at most (the cluster kernel's word layout has room for 4)
+constexpr int kMaxClustersPerXcd = 4;
 constexpr int kCusPerXcd = 32;
 
 netsim_status prepare(netsim_t* h) {
@@ -630,7 +632,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
       cus = 0;
     const int xcds = cus / kCusPerXcd;
     if (S == 1 && widest > 65536) exec = NETSIM_EXEC_GRID;
-    else if (!solve_only && S <= xcds && widest > 16384) exec = NETSIM_EXEC_CLUSTER;
+    else if (!solve_only && S <= kMaxClustersPerXcd * xcds && widest > 16384) exec = NETSIM_EXEC_CLUSTER;
     else exec = NETSIM_EXEC_BLOCK;
   }
   if (exec == NETSIM_EXEC_CLUSTER && solve_only) exec = NETSIM_EXEC_BLOCK;
@@ -652,6 +654,12 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
       int blocks = 0;
       he = netsim_dev::cluster_capacity(h->opt.device, &blocks);
       if (he == hipSuccess && blocks < 1) he = hipErrorInvalidConfiguration;
+      // as many leaders as parts (up to kMaxClustersPerXcd per XCD), so that
+      // every part runs at once with the helpers that leaves it
+      int cus = 0;
+      if (he == hipSuccess) he = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->opt.device);
+      const int xcds = std::max(1, cus / kCusPerXcd);
+      P.clusters_per_xcd = std::max(1, std::min(kMaxClustersPerXcd, (S + xcds - 1) / xcds));
       if (he == hipSuccess) he = netsim_dev::launch_cluster(P, blocks, st);
     } else if (exec == NETSIM_EXEC_GRID) {
       const int threads = 1024;

@@ -220,3 +220,30 @@ def test_cluster_phase_times_count_the_helpers():
     assert ph[3] > 0 and ph[5] > 0 and ph[0] > 0
     assert sum(ph) <= st["device_seconds"] * st["parts"] * 1.01
     _say("  phases", [round(x, 5) for x in ph], "device", st["device_seconds"])
+
+
+def _c4_batch(n, blocks=2, locals_=4, phases=2):
+    """n expert-parallel all-to-all what-if scenarios (different seeds), each
+    split into `blocks` parts."""
+    return Program("c4-batch", [configs.c4(4 + k, blocks=blocks, locals_=locals_,
+                                           phases=phases).scenarios[0] for k in range(n)])
+
+
+@pytest.mark.parametrize("n", [5, 12])
+def test_cluster_several_leaders_per_xcd(n):
+    """More wide parts than XCDs (10 and 24 parts): two and three leaders per
+    XCD, each with its own helpers; bit-identical to the block layout."""
+    _say(f"test_cluster_several_leaders_per_xcd n={n}")
+    sa, sb = _both(_c4_batch(n), 0)
+    assert sb["parts"] == 2 * n and sb["assisted_solves"] > 0
+    _say("  block s", sa["device_seconds"], "cluster s", sb["device_seconds"])
+
+
+def test_auto_picks_the_cluster_layout_for_a_batch():
+    """AUTO: 16 parts starting with 32k flows each (two full-size all-to-all
+    scenarios) take the cluster layout with two leaders per XCD."""
+    ns, pr = _gpu()
+    _say("test_auto_picks_the_cluster_layout_for_a_batch")
+    program = Program("c4x2", [configs.c4(4).scenarios[0], configs.c4(5).scenarios[0]])
+    _, st = pr.run_program(program, ns.make_options(until=1e-4))
+    assert st["layout"] == ns.EXEC_CLUSTER and st["parts"] == 16
