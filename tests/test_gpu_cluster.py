@@ -247,3 +247,37 @@ def test_auto_picks_the_cluster_layout_for_a_batch():
     program = Program("c4x2", [configs.c4(4).scenarios[0], configs.c4(5).scenarios[0]])
     _, st = pr.run_program(program, ns.make_options(until=1e-4))
     assert st["layout"] == ns.EXEC_CLUSTER and st["parts"] == 16
+
+
+def test_complete_alltoall_cluster_equals_block_and_is_causal():
+    """The bench's workload, complete (4096 GPUs, 8 parts, every flow of the
+    four phases): the cluster layout (AUTO's choice) equals the block layout
+    bit for bit, every flow finishes, and no flow finishes before its release
+    (its last predecessor's finish plus its lag) plus its bytes over the
+    narrowest link of its path -- a bound that holds at any size."""
+    from oracle import flows as oflows
+    ns, pr = _gpu()
+    _say("test_complete_alltoall_cluster_equals_block_and_is_causal")
+    program = configs.c4(4)
+    a, sa = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK))
+    b, sb = pr.run_program(program, ns.make_options())
+    assert sb["layout"] == ns.EXEC_CLUSTER and sb["complete"] == 1
+    assert np.array_equal(a[0], b[0])
+    for k in SAME:
+        assert sa[k] == sb[k], k
+    fin = b[0]
+    assert np.all(np.isfinite(fin))
+    fs = oflows.expand(program.scenarios[0])
+    deg = np.diff(fs.dep_off)
+    base = np.zeros(fs.F)
+    has = deg > 0
+    if has.any():
+        seg = np.maximum.reduceat(fin[fs.dep_ids], fs.dep_off[:-1][has])
+        base[has] = seg
+    mincap = np.full(fs.F, np.inf)
+    plen = np.diff(fs.path_off)
+    wp = plen > 0
+    mincap[wp] = np.minimum.reduceat(fs.cap[fs.path_link], fs.path_off[:-1][wp])
+    lower = base + fs.start + np.where(wp, fs.nbytes / mincap, 0.0)
+    assert np.all(fin >= lower * (1 - 1e-12))
+    _say("  block s", sa["device_seconds"], "cluster s", sb["device_seconds"])
