@@ -349,33 +349,37 @@ struct ClusterG {
     drain();
     __syncthreads();
     if (threadIdx.x == 0) {
+      // the arrival and a look at the abort word travel together; an abort
+      // raised meanwhile is seen at a later barrier or in a wait (the word
+      // stays set, so a helper that leaves early cannot strand the others)
+      const uint32_t target = (gen + 1) * (uint32_t)nh;
       uint32_t a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (a == 0) {
-        const uint32_t target = (gen + 1) * (uint32_t)nh;
-        const uint32_t prev =
-            __hip_atomic_fetch_add(&cw[CL_CNT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (prev + 1 != target) wait_reach(&cw[CL_CNT], target);
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+      const uint32_t prev =
+          __hip_atomic_fetch_add(&cw[CL_CNT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (a == 0 && prev + 1 != target && !wait_reach(&cw[CL_CNT], target)) a = 1;
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       *flag = (int)a;
     }
     gen += 1;
     __syncthreads();
     ab = *flag != 0;
   }
-  // Waits until the counter reaches target (counted modulo 2^32), giving up
-  // on the abort word or after `patience` ticks (then raising it).
-  __device__ __forceinline__ void wait_reach(uint32_t* p, uint32_t target) {
+  // Waits until the counter reaches target (counted modulo 2^32); the first
+  // poll and every 16th after it give up on the abort word or after
+  // `patience` ticks (then raising it).  Returns false if it gave up.
+  __device__ __forceinline__ bool wait_reach(uint32_t* p, uint32_t target) {
     const uint64_t t0 = wall_clock64();
-    while ((int32_t)(__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+    for (uint32_t i = 1;
+         (int32_t)(__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0; ++i) {
       __builtin_amdgcn_s_sleep(1);
-      if (__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return;
+      if ((i & 15) != 1) continue;
+      if (__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return false;
       if (wall_clock64() - t0 > patience) {
         __hip_atomic_store(&bar[BAR_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return;
+        return false;
       }
     }
+    return true;
   }
   template <class T>
   __device__ T add(T* p, T v) {
@@ -1186,7 +1190,7 @@ __device__ __forceinline__ void take_back(G& g, const Params& P, LK& lk, const i
 }
 
 // ---------------------------------------------- shared-memory-resident solve
-// Grid layout: each workgroup takes a contiguous slice of the active list (at
+// Grid layout: each workgroup takes every nb-th flow of the active list (at
 // most LDS_FLOWS flows), copies the flow ids and their path records into
 // shared memory once, and keeps its unfrozen flows as a shared-memory list.
 // Only link state and the rates are touched outside, so a round costs one
@@ -1208,9 +1212,11 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
   Lists* K = g.lists(C);
   const int tid = g.tid();
   const int nb = g.nblocks();
-  const int per = (n0 + nb - 1) / nb;
-  const int c0 = min(n0, g.block_id() * per);
-  const int nl = min(n0, c0 + per) - c0;
+  // items b, b + nb, b + 2nb, ... of the list: interleaved, so every
+  // workgroup keeps a like share of unfrozen flows through the rounds (the
+  // list follows activation order, and contiguous slices freeze unevenly)
+  const int b0 = g.block_id();
+  const int nl = b0 < n0 ? (n0 - 1 - b0) / nb + 1 : 0;
   const int l0 = C->l0;
   const int cap = C->f1 - C->f0;
   int* bc = g.ldsi + 120;  // counters read by thread 0 after a barrier, for the block
@@ -1222,7 +1228,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
   // take-back too: remaining bytes brought up to rs->t, its rate and one
   // unfrozen flow returned to its links
   for (int j = threadIdx.x; j < nl; j += blockDim.x) {
-    int f = list0[c0 + j];
+    int f = list0[b0 + j * nb];
     const bool ok = in_range(f, C->f0, cap);
     if (!ok) { bad = 2; f = C->f0; }
     const uint4 rec = P.path16[f];
@@ -1230,7 +1236,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     S.path[j] = rec;
     S.u[0][j] = (uint16_t)j;
     if (rs && ok) {
-      const int sl = rs->at[c0 + j];
+      const int sl = rs->at[b0 + j * nb];
       if ((unsigned)sl >= (unsigned)cap) { bad = 2; continue; }
       const bool fresh = sl >= rs->s_new;
       int64_t qv = 0;
@@ -1346,7 +1352,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     // predicted completion, by the thread that took it back
     for (int j = threadIdx.x; j < nl; j += blockDim.x) {
       const int f = S.fid[j];
-      const int sl = rs->at[c0 + j];
+      const int sl = rs->at[b0 + j * nb];
       if ((unsigned)sl >= (unsigned)cap) continue;
       const double m = S.mf[j];
       rs->sl.rate[sl] = m;
@@ -1433,6 +1439,10 @@ struct Assist {
           }
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        // a helper that gave up at a barrier raised the abort word before it
+        // counted itself done, even if the others finished the job without it
+        if (ok && __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)
+          ok = false;
         if (ok) {
           res = (int)__hip_atomic_load(&cw[CL_RC], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           auto w64 = [&](int k) { return reinterpret_cast<uint64_t*>(cw + k); };
