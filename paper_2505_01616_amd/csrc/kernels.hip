@@ -1588,8 +1588,8 @@ __device__ __forceinline__ void helper_loop(const Params& P, ClusterG& cg, Solve
 // flow's rate is re-solved, after which tau = t + rem / rate.  So an event
 // reads a kept flow's tau (next-event search) and rate (re-solve selection)
 // and writes nothing for it.  A finished flow leaves a hole (id -1, tau
-// +inf); when holes outnumber live slots, the live ones are compacted into
-// the other buffer.
+// +inf); when holes are more than an eighth of the slots, the live ones are
+// compacted into the other buffer.
 constexpr double KEEP = 1.0 - 1e-9;  // safety margin below theta
 
 // Flow f becomes active at time t: remaining bytes, active counts on its
@@ -2047,10 +2047,11 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       if (threadIdx.x == 0) tl->solves += 1;  // the active set changed: one rate solve (possibly empty)
       if (rc != 0) { status = rc; break; }
     }
-    // compaction: when holes outnumber live slots, copy the live ones into
-    // the other buffer
+    // compaction: when holes are more than an eighth of the slots, copy the
+    // live ones into the other buffer (every event sweeps all slots, holes
+    // included, and a compaction costs about one sweep)
     const int holes = g.load(&K->holes);
-    if (2 * holes > nSlots) {
+    if (8 * holes > nSlots) {
       const Slots nx = slots(ab ^ 1);
       int32_t* const cnts[1] = {&K->slots2};
       sweep_append<1>(
