@@ -1724,8 +1724,11 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       g.store(&K->slots2, 0);
     }
     // next event time: earliest predicted completion or release (four
-    // slots of a thread in flight at a time)
-    double mine = INF;
+    // slots of a thread in flight at a time).  Each thread also keeps the
+    // slot of its earliest completion and its second earliest time: when
+    // only the earliest is due the thread finishes it without looking again.
+    double mine = INF, mine2 = INF;
+    int smin = 0;
     for (int s0 = tid; s0 < nSlots; s0 += 4 * T) {
       double v[4];
 #pragma unroll
@@ -1734,7 +1737,15 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
         v[u] = s < nSlots ? sl.tau[s] : INF;
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) mine = v[u] < mine ? v[u] : mine;
+      for (int u = 0; u < 4; ++u) {
+        if (v[u] < mine) {
+          mine2 = mine;
+          mine = v[u];
+          smin = s0 + u * T;
+        } else if (v[u] < mine2) {
+          mine2 = v[u];
+        }
+      }
     }
     double loc = mine;
     for (int i = tid; i < nPend; i += T) {
@@ -1763,9 +1774,32 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     int32_t* compCnt = &K->comp[q % 3];
     if (tid == 0) g.store(&K->comp[(q + 1) % 3], 0);
     int err = 0;
-    // completions: only threads holding a slot that is due look again
-    if (mine <= thr) {
-      // only threads holding a due slot look again, four slots in flight
+    // completions: only threads holding a slot that is due look at it
+    auto finish_slot = [&](int s) {
+      const int f = sl.id[s];
+      if (!in_range(f, f0, cap)) { err = 1; return; }
+      const double r = sl.rate[s];
+      // the last byte leaves now; it arrives the path latency later
+      P.finish[f] = P.lat ? tn + P.lat[f] : tn;
+      g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
+      const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
+      for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
+        const int l = P.plink[k];
+        lk.addNact(g, l, -1);
+        lk.addR(g, l, qv);  // its share returns to the link
+      }
+      if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
+      g.store(&K->changed[ib], 1);
+      sl.id[s] = -1;
+      sl.tau[s] = INF;
+      g.add(&K->holes, 1);
+      const int c = g.add(compCnt, 1);
+      if (c < cap) compOut[c] = f; else err = 1;
+    };
+    if (mine <= thr && !(mine2 <= thr)) {
+      finish_slot(smin);  // the thread's only due slot
+    } else if (mine <= thr) {
+      // several due slots: look at every slot again, four in flight
       for (int s0 = tid; s0 < nSlots; s0 += 4 * T) {
         double v[4];
 #pragma unroll
@@ -1774,29 +1808,8 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
           v[u] = s < nSlots ? sl.tau[s] : INF;
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int s = s0 + u * T;
-          if (!(v[u] <= thr)) continue;
-          const int f = sl.id[s];
-          if (!in_range(f, f0, cap)) { err = 1; continue; }
-          const double r = sl.rate[s];
-          // the last byte leaves now; it arrives the path latency later
-          P.finish[f] = P.lat ? tn + P.lat[f] : tn;
-          g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
-          const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
-          for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
-            const int l = P.plink[k];
-            lk.addNact(g, l, -1);
-            lk.addR(g, l, qv);  // its share returns to the link
-          }
-          if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
-          g.store(&K->changed[ib], 1);
-          sl.id[s] = -1;
-          sl.tau[s] = INF;
-          g.add(&K->holes, 1);
-          const int c = g.add(compCnt, 1);
-          if (c < cap) compOut[c] = f; else err = 1;
-        }
+        for (int u = 0; u < 4; ++u)
+          if (v[u] <= thr) finish_slot(s0 + u * T);
       }
     }
     // releases due now
