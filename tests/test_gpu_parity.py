@@ -258,6 +258,32 @@ def test_c5_full_batched():
              "events", st["events"], "parts", st["parts"])
 
 
+def test_c4_part_complete():
+    """One part of the expert-parallel all-to-all at full width (the eight
+    expert groups of one 64-server block, one dispatch phase, ~32k flows) run
+    to the end: ~27k events, the large re-solves handed to the helper
+    workgroups (AUTO picks the cluster layout) and many slot compactions.
+    The event count equals the oracle's, the makespan and a seeded 3000-flow
+    sample of finish times agree with the stored complete oracle run to 1e-6,
+    and the block layout gives the same bits."""
+    ns, pr = _gpu()
+    _say("test_c4_part_complete")
+    gold = _golden("c4_part_summary.json")
+    program = configs.c4(4, blocks=1, locals_=8, phases=1)
+    fins, st = pr.run_program(program, ns.make_options())
+    assert st["layout"] == ns.EXEC_CLUSTER and st["assisted_solves"] > 0 and st["complete"] == 1
+    assert st["parts"] == 1 and st["events"] == gold["events"]  # one part: the oracle's own events
+    fin = fins[0]
+    assert len(fin) == gold["flows"] and int(np.isfinite(fin).sum()) == gold["finished"]
+    ids = np.array(gold["sample_ids"])
+    assert _rel(fin[ids], np.array(gold["sample_finish"])) < TOL
+    assert abs(float(np.max(fin)) - gold["makespan"]) <= TOL * gold["makespan"]
+    bfins, _ = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK))
+    assert np.array_equal(bfins[0], fin, equal_nan=True)
+    _say(f"c4 part: device s {st['device_seconds']:.3f}, events {st['events']} (oracle {gold['events']}), "
+         f"assisted {st['assisted_solves']}")
+
+
 def test_c3_full_size():
     """Full C3 (ill-conditioned in fp64): sampled flows finishing before the
     horizon of the oracle's perturbed runs agree to 1e-6; the makespan and
