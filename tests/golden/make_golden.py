@@ -1,7 +1,7 @@
 """Writes the stored oracle values used by the full-size GPU parity tests.
 
 Calls only the oracle (``oracle/``) and the seeded workload generator.  Run
-from the repository root:  python tests/golden/make_golden.py [c3] [c5] [c4part]
+from the repository root:  python tests/golden/make_golden.py [c3] [c5] [c4part] [c4part4]
 
 c5_makespans.json   per-scenario makespan of all 256 C5 scenarios (fp64 oracle)
 c4_part_summary.json  one part of the 4096-GPU expert-parallel all-to-all at
@@ -9,6 +9,9 @@ c4_part_summary.json  one part of the 4096-GPU expert-parallel all-to-all at
                     one dispatch phase, ~32k flows): makespan, event and solve
                     counts and a seeded sample of per-flow finish times of the
                     complete run
+c4_part4_summary.json the same part with all four phases and their barriers:
+                    the flows of one of the eight independent parts of the
+                    full 4096-GPU workload
 c3_summary.json     C3 (full size): makespan, a seeded sample of per-flow
                     finish times, and the oracle's own spread under changes
                     of every capacity by k ulps, k in -5..-1 and 1..6 (C3 is
@@ -96,30 +99,33 @@ def c3():
     print(f"c3: {time.time() - t0:.0f} s, horizon {horizon:.4g}", flush=True)
 
 
-def c4part():
+def c4part(phases=1):
     t0 = time.time()
-    prog = configs.c4(4, blocks=1, locals_=8, phases=1)
+    prog = configs.c4(4, blocks=1, locals_=8, phases=phases)
     fs = oflows.expand(prog.scenarios[0])
     ref = osim.run_flowset(fs)
     rng = np.random.default_rng(44)
     sample = np.sort(rng.choice(fs.F, size=3000, replace=False))
     data = {
-        "config": "c4 seed 4, blocks=1, locals_=8, phases=1 (one 64-server block, 8 expert groups)",
+        "config": f"c4 seed 4, blocks=1, locals_=8, phases={phases} (one 64-server block, 8 expert groups)",
         "writer": "tests/golden/make_golden.py",
         "flows": int(fs.F), "events": ref.events, "solves": ref.solves, "makespan": ref.makespan,
         "finished": int(np.isfinite(ref.finish).sum()),
         "sample_ids": sample.tolist(), "sample_finish": ref.finish[sample].tolist(),
     }
-    with open(os.path.join(HERE, "c4_part_summary.json"), "w") as fh:
+    name = "c4_part_summary.json" if phases == 1 else f"c4_part{phases}_summary.json"
+    with open(os.path.join(HERE, name), "w") as fh:
         json.dump(data, fh)
-    print(f"c4part: {time.time() - t0:.0f} s, {ref.events} events", flush=True)
+    print(f"c4part phases={phases}: {time.time() - t0:.0f} s, {ref.events} events", flush=True)
 
 
 if __name__ == "__main__":
-    which = sys.argv[1:] or ["c5", "c3", "c4part"]
+    which = sys.argv[1:] or ["c5", "c3", "c4part", "c4part4"]
     if "c5" in which:
         c5()
     if "c3" in which:
         c3()
     if "c4part" in which:
         c4part()
+    if "c4part4" in which:
+        c4part(phases=4)

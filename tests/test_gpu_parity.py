@@ -284,6 +284,28 @@ def test_c4_part_complete():
          f"assisted {st['assisted_solves']}")
 
 
+def test_c4_full_size_first_part_complete():
+    """The full 4096-GPU all-to-all exactly as bench.py runs it (AUTO, 8
+    parts, all four phases, to the end).  Its first 129,048 flows are the
+    eight expert groups of the first 64-server block: they share no link and
+    no dependency with the other flows, so the oracle's complete run of that
+    block alone (stored: ~111k events) is their exact reference.  The
+    makespan of the block and a seeded 3000-flow sample agree to 1e-6."""
+    ns, pr = _gpu()
+    _say("test_c4_full_size_first_part_complete")
+    gold = _golden("c4_part4_summary.json")
+    program = configs.c4(4)
+    fins, st = pr.run_program(program, ns.make_options())
+    assert st["complete"] == 1 and st["parts"] == 8 and st["layout"] == ns.EXEC_CLUSTER
+    part = fins[0][:gold["flows"]]
+    assert int(np.isfinite(part).sum()) == gold["finished"]
+    ids = np.array(gold["sample_ids"])
+    assert _rel(part[ids], np.array(gold["sample_finish"])) < TOL
+    assert abs(float(np.max(part)) - gold["makespan"]) <= TOL * gold["makespan"]
+    _say(f"c4 full, first part: device s {st['device_seconds']:.2f}, oracle events of the part "
+         f"{gold['events']}, GPU part events (all parts) {st['events']}")
+
+
 def test_c3_full_size():
     """Full C3 (ill-conditioned in fp64): sampled flows finishing before the
     horizon of the oracle's perturbed runs agree to 1e-6; the makespan and
