@@ -159,3 +159,27 @@ def test_workload_sizes():
         assert fs.F == 16384 + 2 * (pp - 1) * 16384 // pp
         dp = 16384 // (tp * pp)
         assert np.sum(fs.nbytes == 2 * (dp - 1) * (4 * GiB / dp)) == 16384
+
+
+def test_c4_first_block_is_an_independent_prefix():
+    """The full 4096-GPU all-to-all begins with the flows of its first
+    64-server block, flow for flow those of the one-block workload (same
+    routes, bytes, lags and dependencies), and no later flow shares a link
+    with them or depends on them: the complete oracle run of the one-block
+    workload is therefore the exact reference for those flows of the full
+    run (a stored fixture of the GPU parity tests relies on this)."""
+    a = flows.expand(configs.c4(4, blocks=1, locals_=8, phases=4).scenarios[0])
+    b = flows.expand(configs.c4(4).scenarios[0])
+    F, nnz, nd = a.F, int(a.path_off[-1]), int(a.dep_off[-1])
+    assert F == 129048 and b.F == 8 * F
+    for k in ("src", "dst", "nbytes", "start"):
+        assert np.array_equal(getattr(a, k), getattr(b, k)[:F]), k
+    assert np.array_equal(a.cap, b.cap)
+    assert np.array_equal(a.path_off, b.path_off[:F + 1])
+    assert np.array_equal(a.path_link, b.path_link[:nnz])
+    assert np.array_equal(a.dep_off, b.dep_off[:F + 1])
+    assert np.array_equal(a.dep_ids, b.dep_ids[:nd])
+    used = np.zeros(len(b.cap), bool)
+    used[a.path_link] = True
+    assert not used[b.path_link[nnz:]].any()
+    assert not (b.dep_ids[nd:] < F).any()
