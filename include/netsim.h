@@ -64,14 +64,17 @@ enum {
                             and a part with > 16384 of them; else block        */
   NETSIM_EXEC_GRID = 1,  /* whole GPU on one part at a time (grid barriers)      */
   NETSIM_EXEC_BLOCK = 2,  /* one workgroup per part (workgroup barriers)         */
-  NETSIM_EXEC_CLUSTER = 3 /* leader workgroups (one per XCD, or up to 4 per XCD
+  NETSIM_EXEC_CLUSTER = 3, /* leader workgroups (one per XCD, or up to 4 per XCD
                              when there are more parts than XCDs) run parts as
                              in block mode and hand re-solves of at least
                              assist_min_flows flows to assist_helpers other
                              workgroups of their XCD (one workgroup per CU,
                              cooperative launch); results equal block mode's
                              bit for bit.  Rate solves without an
-                             event loop (netsim_solve_rates) run as in block mode */
+                             event loop (netsim_solve_once) run as in block mode */
+  NETSIM_EXEC_EXACT = 4   /* reported in netsim_stats.layout when
+                             netsim_options.exact is set (one workgroup per
+                             scenario, the exact-arithmetic kernel)            */
 };
 
 /*
@@ -99,13 +102,36 @@ typedef struct {
                                 workgroups leave as soon as they have no job (the
                                 leaders then solve alone), bit 3 makes their
                                 barrier give up at once (the run then fails with
-                                NETSIM_E_DEVICE, "grid barrier timed out")       */
+                                NETSIM_E_DEVICE, "grid barrier timed out"); bit
+                                4 keeps exact-mode link state in global memory
+                                even where it fits shared memory                 */
   int32_t single_clock;      /* 1: one part (one clock) per scenario             */
   int32_t assist_min_flows;  /* NETSIM_EXEC_CLUSTER: smallest re-solve handed to the
                                 helper workgroups; 0 = 4096                      */
   int32_t assist_helpers;    /* NETSIM_EXEC_CLUSTER: helper workgroups per leader,
                                 at most the other workgroups of its cluster (an
                                 XCD's workgroups shared among its leaders); 0 = 15 */
+  int32_t exact;             /* 1: the arithmetic of a sequential fp64 program
+                                (Section 4.2's water-filling taken literally):
+                                one clock per scenario (single_clock implied);
+                                each rate solve freezes one bottleneck level per
+                                iteration -- s_l = R_l/n_l, s* = min_l s_l, every
+                                link with s_l <= s*(1 + 1e-12) is a bottleneck
+                                and its unfrozen flows get rate s*, then
+                                R_l -= k_l*s* (product rounded, then the
+                                difference), n_l -= k_l; every active flow's
+                                remaining bytes drop by rate*(t_next - t) at
+                                every event; a flow finishes when
+                                t + rem/rate <= t_next(1 + 1e-12).  One workgroup
+                                per scenario (exec, assist_* ignored; stats.layout
+                                = NETSIM_EXEC_EXACT).  Finish times are the same
+                                bit for bit for any workgroup size.  0: the
+                                default solver (local-minimum rounds, int64
+                                residuals, remaining bytes updated when a rate
+                                changes, independent parts on their own clocks):
+                                the same allocation in exact arithmetic, with
+                                different rounding                              */
+  int32_t reserved;
 } netsim_options;
 
 /*
@@ -189,7 +215,7 @@ typedef struct {
   int64_t assisted_solves;   /* NETSIM_EXEC_CLUSTER: re-solves run by the helper
                                 workgroups (counted in solves and rounds too)    */
   int32_t layout;            /* execution layout of the last launch (NETSIM_EXEC_GRID,
-                                _BLOCK or _CLUSTER; AUTO resolved)                */
+                                _BLOCK, _CLUSTER or _EXACT; AUTO resolved)        */
   int32_t reserved;
 } netsim_stats;
 

@@ -120,6 +120,15 @@ struct Params {
   int32_t* comp0; int32_t* comp1; int32_t* comp2;
   int32_t* unf0; int32_t* unf1;
   int32_t* arr;            // flows activated in the current event
+  // exact mode (the oracle's arithmetic; exact.hip), per device link
+  const double* capf;      // [L] capacity in B/s
+  double* xR;              // [L] residual capacity (fp64)
+  double* xs;              // [L] fair share of the current level
+  int32_t* xn;             // [L] unfrozen flows
+  int32_t* xk;             // [L] flows frozen at the current level
+  int32_t* xlive0; int32_t* xlive1;  // [L] links with unfrozen flows (per part on [l0, l1))
+  int32_t exact_lds_bytes; // dynamic shared memory of the exact kernel (link state
+                           // of a part with at most exact_lds_bytes / 24 links)
   ScenCtl* ctl;            // [num_scen]
   uint32_t* bar;           // synchronisation words [BAR_WORDS] (layout in kernels.hip)
   uint64_t* slots;         // grid min-reduction slots [4]
@@ -137,5 +146,10 @@ hipError_t grid_capacity(int device, int threads, int* blocks);
 // launch, 1024 threads per workgroup; blocks from cluster_capacity).
 hipError_t launch_cluster(const Params& p, int blocks, hipStream_t s);
 hipError_t cluster_capacity(int device, int* blocks);
+// Exact mode: one workgroup per part (one part per scenario), the oracle's
+// arithmetic (exact.hip); p.exact_lds_bytes of dynamic shared memory.
+hipError_t launch_exact(const Params& p, int blocks, int threads, hipStream_t s);
+// Bytes of exact-mode link state per link.
+int exact_link_bytes();
 
 }  // namespace netsim_dev

@@ -245,6 +245,10 @@ constexpr int32_t kAssistHelpers = 15;
 // leaders per XCD at most (the cluster kernel's word layout has room for 4)
 constexpr int kMaxClustersPerXcd = 4;
 constexpr int kCusPerXcd = 32;
+// Exact mode: dynamic shared memory for link state (24 bytes per link: up
+// to 6,485 links per part) and threads per workgroup.
+constexpr int64_t kExactLdsBytes = 152 * 1024;
+constexpr int kExactThreads = 512;
 
 netsim_status prepare(netsim_t* h) {
   const int32_t S = (int32_t)h->scen.size();
@@ -267,7 +271,7 @@ netsim_status prepare(netsim_t* h) {
     const int64_t nf = (int64_t)sc.flows.size();
     if (nf == 0) continue;
     const int32_t P0 = (int32_t)part_scen.size();
-    if (h->opt.single_clock) {
+    if (h->opt.single_clock || h->opt.exact) {
       for (int64_t id : sc.flows) part_of_id[(size_t)id] = P0;
       part_scen.push_back(s);
       continue;
@@ -362,11 +366,15 @@ netsim_status prepare(netsim_t* h) {
   if (maxcap > 0.0) std::frexp(maxcap, &ex);
   h->scale = std::ldexp(1.0, 61 - ex);
   std::vector<int64_t> R0((size_t)std::max<int64_t>(ld, 1));
+  std::vector<double> capf((size_t)std::max<int64_t>(ld, 1), 0.0);
   for (int32_t s = 0; s < S; ++s) {
     const Scen& sc = h->scen[s];
     for (size_t l = 0; l < sc.cap.size(); ++l) {
       const int32_t d = h->dev_link[(size_t)s][l];
-      if (d >= 0) R0[(size_t)d] = (int64_t)std::llrint(sc.cap[l] * h->scale);
+      if (d >= 0) {
+        R0[(size_t)d] = (int64_t)std::llrint(sc.cap[l] * h->scale);
+        capf[(size_t)d] = sc.cap[l];
+      }
     }
   }
   // paths, bytes, start in device order
@@ -471,6 +479,7 @@ netsim_status prepare(netsim_t* h) {
   h->h_ctl0 = ctl;
   // one device allocation, carved into aligned arrays
   const size_t Fz = (size_t)std::max<int64_t>(F, 1), Lz = (size_t)std::max<int64_t>(ld, 1);
+  const size_t XL = h->opt.exact ? Lz : 1;
   struct Part { void** dst; size_t bytes; };
   Params& P = h->prm;
   P = Params{};
@@ -518,6 +527,14 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.unf1, sizeof(int32_t) * Fz},
       {(void**)&P.bar, sizeof(uint32_t) * netsim_dev::BAR_WORDS},
       {(void**)&P.slots, sizeof(uint64_t) * 8},
+      // exact mode: link state in fp64 (one element each otherwise)
+      {(void**)&P.capf, sizeof(double) * XL},
+      {(void**)&P.xR, sizeof(double) * XL},
+      {(void**)&P.xs, sizeof(double) * XL},
+      {(void**)&P.xn, sizeof(int32_t) * XL},
+      {(void**)&P.xk, sizeof(int32_t) * XL},
+      {(void**)&P.xlive0, sizeof(int32_t) * XL},
+      {(void**)&P.xlive1, sizeof(int32_t) * XL},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.bytes + 255) & ~size_t(255);
@@ -547,6 +564,7 @@ netsim_status prepare(netsim_t* h) {
       {comp_of_dev.data(), P.comp, sizeof(int32_t) * comp_of_dev.size()},
       {path16.data(), P.path16, sizeof(uint16_t) * path16.size()},
       {lat.data(), P.lat, any_lat ? sizeof(double) * lat.size() : 0},
+      {capf.data(), P.capf, h->opt.exact ? sizeof(double) * capf.size() : 0},
   };
   for (const Up& u : ups) {
     if (u.bytes == 0) continue;
@@ -636,6 +654,7 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
     else exec = NETSIM_EXEC_BLOCK;
   }
   if (exec == NETSIM_EXEC_CLUSTER && solve_only) exec = NETSIM_EXEC_BLOCK;
+  if (h->opt.exact) exec = NETSIM_EXEC_EXACT;
   h->layout = exec;
   // grid-barrier words and min-reduction slots start fresh in every launch
   // (a launch that continues a run must not see the last launch's counts)
@@ -650,7 +669,22 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
   if (he != hipSuccess) return hip_fail(h, he, "hipEventCreate");
   he = hipEventRecord(e0, st);
   if (he == hipSuccess) {
-    if (exec == NETSIM_EXEC_CLUSTER) {
+    if (exec == NETSIM_EXEC_EXACT) {
+      // link state in shared memory for every part whose links fit the pool
+      // (sized by the largest such part, so small parts leave room for more
+      // workgroups per CU); larger parts keep theirs in global memory
+      const int64_t per = netsim_dev::exact_link_bytes();
+      int64_t lds = 0;
+      for (const ScenCtl& c : h->h_ctl0) {
+        const int64_t b = (int64_t)(c.l1 - c.l0) * per;
+        if (b <= kExactLdsBytes) lds = std::max(lds, b);
+      }
+      P.exact_lds_bytes = (int32_t)((lds + 15) & ~int64_t(15));
+      int threads = h->opt.block_threads > 0 ? h->opt.block_threads : kExactThreads;
+      threads = std::max(64, std::min(1024, threads / 64 * 64));
+      const int blocks = std::max(1, std::min<int32_t>(S, 1 << 20));
+      he = netsim_dev::launch_exact(P, blocks, threads, st);
+    } else if (exec == NETSIM_EXEC_CLUSTER) {
       int blocks = 0;
       he = netsim_dev::cluster_capacity(h->opt.device, &blocks);
       if (he == hipSuccess && blocks < 1) he = hipErrorInvalidConfiguration;

@@ -24,7 +24,7 @@ OK, E_INVALID, E_NOMEM, E_DEVICE, E_STATE, E_LIMIT = 0, -1, -2, -3, -4, -5
 TOPO_LEAF_SPINE, TOPO_RAIL, TOPO_FAT_TREE = 1, 2, 3
 RING_ALLREDUCE, RING_REDUCE_SCATTER, RING_ALL_GATHER = 0, 1, 2
 MODE_CHAINED, MODE_FLAT, MODE_AGGREGATED = 0, 1, 2
-EXEC_AUTO, EXEC_GRID, EXEC_BLOCK, EXEC_CLUSTER = 0, 1, 2, 3
+EXEC_AUTO, EXEC_GRID, EXEC_BLOCK, EXEC_CLUSTER, EXEC_EXACT = 0, 1, 2, 3, 4
 
 STATUS_NAMES = {OK: "NETSIM_OK", E_INVALID: "NETSIM_E_INVALID", E_NOMEM: "NETSIM_E_NOMEM",
                 E_DEVICE: "NETSIM_E_DEVICE", E_STATE: "NETSIM_E_STATE", E_LIMIT: "NETSIM_E_LIMIT"}
@@ -35,7 +35,8 @@ class netsim_options(ctypes.Structure):
                 ("max_events", ctypes.c_int64), ("until", ctypes.c_double),
                 ("max_rounds", ctypes.c_int32), ("block_threads", ctypes.c_int32),
                 ("debug", ctypes.c_int32), ("single_clock", ctypes.c_int32),
-                ("assist_min_flows", ctypes.c_int32), ("assist_helpers", ctypes.c_int32)]
+                ("assist_min_flows", ctypes.c_int32), ("assist_helpers", ctypes.c_int32),
+                ("exact", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class netsim_topology(ctypes.Structure):
@@ -164,11 +165,12 @@ def netsim_default_options() -> netsim_options:
 
 def make_options(device=0, exec=EXEC_AUTO, max_events=0, until=math.inf, max_rounds=0,
                  block_threads=0, debug=0, single_clock=0, assist_min_flows=0,
-                 assist_helpers=0) -> netsim_options:
+                 assist_helpers=0, exact=0) -> netsim_options:
     o = netsim_default_options()
     o.device, o.exec, o.max_events, o.until = device, exec, max_events, until
     o.max_rounds, o.block_threads, o.debug = max_rounds, block_threads, debug
     o.single_clock, o.assist_min_flows, o.assist_helpers = single_clock, assist_min_flows, assist_helpers
+    o.exact = exact
     return o
 
 

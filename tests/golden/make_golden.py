@@ -1,7 +1,8 @@
 """Writes the stored oracle values used by the full-size GPU parity tests.
 
 Calls only the oracle (``oracle/``) and the seeded workload generator.  Run
-from the repository root:  python tests/golden/make_golden.py [c3] [c5] [c4part] [c4part4]
+from the repository root:
+  python tests/golden/make_golden.py [c3] [c5] [c4part] [c4part4] [c3full] [c4blocks]
 
 c5_makespans.json   per-scenario makespan of all 256 C5 scenarios (fp64 oracle)
 c4_part_summary.json  one part of the 4096-GPU expert-parallel all-to-all at
@@ -17,6 +18,16 @@ c3_summary.json     C3 (full size): makespan, a seeded sample of per-flow
                     of every capacity by k ulps, k in -5..-1 and 1..6 (C3 is
                     ill-conditioned in fp64; eleven perturbations, run in
                     parallel processes)
+c3_finish.npz       C3 (full size): the complete per-flow finish times of the
+                    unperturbed oracle run (f64store format), with
+c3_full.json        its event, solve and progressive-filling iteration counts
+c4_blocks_finish.npz  the 4096-GPU all-to-all at full size (four phases):
+                    complete per-flow finish times of each of its eight
+                    independent 64-server blocks (flows b*129048 ..
+                    (b+1)*129048-1 of the full workload; a block shares no
+                    link and no dependency with another), each run by the
+                    oracle on its own clock, in parallel processes
+c4_blocks.json      per block: event, solve and iteration counts, makespan
 """
 
 from __future__ import annotations
@@ -35,6 +46,9 @@ sys.path.insert(0, ROOT)
 from oracle import flows as oflows  # noqa: E402
 from oracle import sim as osim  # noqa: E402
 from workloads import configs  # noqa: E402
+
+sys.path.insert(0, HERE)
+import f64store  # noqa: E402
 
 
 def c5():
@@ -119,8 +133,68 @@ def c4part(phases=1):
     print(f"c4part phases={phases}: {time.time() - t0:.0f} s, {ref.events} events", flush=True)
 
 
+def c3full():
+    t0 = time.time()
+    fs = oflows.expand(configs.c3(3).scenarios[0])
+    ref = osim.run_flowset(fs)
+    assert ref.complete and np.all(np.isfinite(ref.finish))
+    f64store.save(os.path.join(HERE, "c3_finish.npz"), finish=ref.finish)
+    with open(os.path.join(HERE, "c3_full.json"), "w") as fh:
+        json.dump({"config": "c3 seed 3 (full size)", "writer": "tests/golden/make_golden.py",
+                   "flows": int(fs.F), "events": ref.events, "solves": ref.solves,
+                   "iterations": ref.iterations, "flows_swept": ref.flows_swept,
+                   "incidences_swept": ref.incidences_swept, "makespan": ref.makespan,
+                   "oracle_seconds": time.time() - t0}, fh, indent=1)
+    print(f"c3full: {time.time() - t0:.0f} s, {ref.events} events, "
+          f"{ref.iterations} iterations", flush=True)
+
+
+C4_BLOCK_FLOWS = 129048
+
+
+def c4_block_flowset(fs, b):
+    """Flows b*129048 .. (b+1)*129048-1 of the full 4096-GPU all-to-all as a
+    flow set of their own (dependency ids shifted; links unchanged)."""
+    f0, f1 = b * C4_BLOCK_FLOWS, (b + 1) * C4_BLOCK_FLOWS
+    p0, p1 = fs.path_off[f0], fs.path_off[f1]
+    d0, d1 = fs.dep_off[f0], fs.dep_off[f1]
+    dids = fs.dep_ids[d0:d1] - f0
+    assert dids.size == 0 or (dids.min() >= 0 and dids.max() < f1 - f0)
+    return oflows.FlowSet(fs.cap, fs.src[f0:f1], fs.dst[f0:f1], fs.nbytes[f0:f1],
+                          fs.start[f0:f1], fs.path_off[f0:f1 + 1] - p0,
+                          fs.path_link[p0:p1], fs.dep_off[f0:f1 + 1] - d0, dids)
+
+
+def _c4_block_run(b):
+    t0 = time.time()
+    fs = oflows.expand(configs.c4(4).scenarios[0])
+    assert fs.F == 8 * C4_BLOCK_FLOWS
+    sub = c4_block_flowset(fs, b)
+    del fs
+    r = osim.run_flowset(sub)
+    assert r.complete and np.all(np.isfinite(r.finish))
+    print(f"c4 block {b}: {time.time() - t0:.0f} s, {r.events} events", flush=True)
+    return b, r.finish, {"block": b, "events": r.events, "solves": r.solves,
+                         "iterations": r.iterations, "makespan": r.makespan,
+                         "oracle_seconds": time.time() - t0}
+
+
+def c4blocks():
+    from multiprocessing import Pool
+    t0 = time.time()
+    with Pool(8) as pool:
+        res = sorted(pool.map(_c4_block_run, range(8)))
+    f64store.save(os.path.join(HERE, "c4_blocks_finish.npz"),
+                  **{f"block{b}": fin for b, fin, _ in res})
+    with open(os.path.join(HERE, "c4_blocks.json"), "w") as fh:
+        json.dump({"config": "c4 seed 4 (full size, four phases)",
+                   "writer": "tests/golden/make_golden.py",
+                   "block_flows": C4_BLOCK_FLOWS, "blocks": [m for _, _, m in res]}, fh, indent=1)
+    print(f"c4blocks: {time.time() - t0:.0f} s", flush=True)
+
+
 if __name__ == "__main__":
-    which = sys.argv[1:] or ["c5", "c3", "c4part", "c4part4"]
+    which = sys.argv[1:] or ["c5", "c3", "c4part", "c4part4", "c3full", "c4blocks"]
     if "c5" in which:
         c5()
     if "c3" in which:
@@ -129,3 +203,7 @@ if __name__ == "__main__":
         c4part()
     if "c4part4" in which:
         c4part(phases=4)
+    if "c3full" in which:
+        c3full()
+    if "c4blocks" in which:
+        c4blocks()
