@@ -2,7 +2,7 @@
 
 Calls only the oracle (``oracle/``) and the seeded workload generator.  Run
 from the repository root:
-  python tests/golden/make_golden.py [c3] [c5] [c4part] [c4part4] [c3full] [c4blocks]
+  python tests/golden/make_golden.py [c3] [c5] [c4part] [c3full] [c4blocks]
 
 c5_makespans.json   per-scenario makespan of all 256 C5 scenarios (fp64 oracle)
 c4_part_summary.json  one part of the 4096-GPU expert-parallel all-to-all at
@@ -10,9 +10,6 @@ c4_part_summary.json  one part of the 4096-GPU expert-parallel all-to-all at
                     one dispatch phase, ~32k flows): makespan, event and solve
                     counts and a seeded sample of per-flow finish times of the
                     complete run
-c4_part4_summary.json the same part with all four phases and their barriers:
-                    the flows of one of the eight independent parts of the
-                    full 4096-GPU workload
 c3_summary.json     C3 (full size): makespan, a seeded sample of per-flow
                     finish times, and the oracle's own spread under changes
                     of every capacity by k ulps, k in -5..-1 and 1..6 (C3 is
@@ -194,15 +191,13 @@ def c4blocks():
 
 
 if __name__ == "__main__":
-    which = sys.argv[1:] or ["c5", "c3", "c4part", "c4part4", "c3full", "c4blocks"]
+    which = sys.argv[1:] or ["c5", "c3", "c4part", "c3full", "c4blocks"]
     if "c5" in which:
         c5()
     if "c3" in which:
         c3()
     if "c4part" in which:
         c4part()
-    if "c4part4" in which:
-        c4part(phases=4)
     if "c3full" in which:
         c3full()
     if "c4blocks" in which:
