@@ -479,6 +479,42 @@ netsim_status netsim_get_stats(const netsim_t* h, netsim_stats* stats);
 netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active,
                                 const int64_t* active_ids, double* rates_out);
 
+/*
+ * Allocation-free rate solve, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  The same solve as netsim_solve_once with
+ * netsim_options.exact = 1 -- every flow active, one progressive-filling
+ * level per iteration in fp64 -- on arrays the caller already holds in
+ * device memory, with no handle:
+ *   d_capacity_Bps[num_links]      link capacities (finite, > 0);
+ *   d_path_off[num_flows + 1]      int32 path offsets (d_path_off[0] = 0);
+ *   d_path_link[d_path_off[num_flows]]  int32 link ids (0 .. num_links-1,
+ *                                  distinct within a path, every path
+ *                                  non-empty);
+ *   d_rates[num_flows]             output: the max-min rate of every flow;
+ *   d_status[2]                    output (int64): [0] a netsim_status
+ *                                  (NETSIM_OK, NETSIM_E_INVALID for a bad
+ *                                  path or capacity -- [1] then holds the
+ *                                  offending flow index, or num_flows + the
+ *                                  link index --, NETSIM_E_LIMIT for the
+ *                                  round watchdog), [1] on success the
+ *                                  number of progressive-filling iterations.
+ * The call only checks its scalar arguments and enqueues one kernel on
+ * hip_stream (NULL: the default stream); it never synchronises, so the
+ * caller reads d_status and d_rates after the stream has reached that
+ * point.  Limits: num_links <= 65536, num_flows <= 262144 (NETSIM_E_LIMIT
+ * beyond).  Working memory is one static device array of about 5 MB per
+ * device, held until the process ends and found once per device; nothing
+ * is allocated or freed by the call.  Calls that overlap on one device
+ * (different host threads, or different streams of one device) share that
+ * array and race: serialise them.  The caller owns every array; none is
+ * retained after the kernel ends.
+ */
+netsim_status netsim_solve_rates_noalloc(int32_t device, int32_t num_links,
+                                         const double* d_capacity_Bps, int32_t num_flows,
+                                         const int32_t* d_path_off, const int32_t* d_path_link,
+                                         double* d_rates, int64_t* d_status, void* hip_stream);
+
 /* Message of the last failure on h (or of the calling thread when h is NULL). */
 const char* netsim_last_error(const netsim_t* h);
 

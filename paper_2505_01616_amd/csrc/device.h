@@ -153,3 +153,8 @@ hipError_t launch_exact(const Params& p, int blocks, int threads, hipStream_t s)
 int exact_link_bytes();
 
 }  // namespace netsim_dev
+
+namespace netsim_host {
+// Message returned by netsim_last_error(NULL) on the calling thread.
+void set_thread_error(const char* msg);
+}  // namespace netsim_host

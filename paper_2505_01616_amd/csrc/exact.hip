@@ -32,8 +32,12 @@
 // integer counts.  Nothing depends on the order in which threads run, so the
 // finish times are the same bit for bit for any workgroup size.
 #include "device.h"
+#include "netsim.h"
 
 #include <math.h>
+
+#include <mutex>
+#include <string>
 
 #pragma clang fp contract(off)
 
@@ -548,6 +552,102 @@ __global__ __launch_bounds__(1024) void netsim_exact_kernel(Params P) {
 
 int exact_link_bytes() { return XLINK_BYTES; }
 
+// ------------------------------------------- allocation-free rate solve
+// Scratch of netsim_solve_rates_noalloc: per link R, s (f64), n, k and two
+// live lists (i32); per flow the solve list and two unfrozen lists (i32);
+// a status block.  The array lives in device memory for the whole process
+// (one copy per device); host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device.
+constexpr int NA_MAX_LINKS = 1 << 16;
+constexpr int NA_MAX_FLOWS = 1 << 18;
+constexpr size_t NA_LINK_BYTES = (size_t)NA_MAX_LINKS * (8 + 8 + 4 + 4 + 4 + 4);
+constexpr size_t NA_FLOW_BYTES = (size_t)NA_MAX_FLOWS * (4 + 4 + 4);
+constexpr size_t NA_HEAD_BYTES = 256;  // kept free (alignment of what follows)
+constexpr int ST_BAD_INPUT = -100;
+constexpr size_t NA_SCRATCH_BYTES = NA_HEAD_BYTES + NA_LINK_BYTES + NA_FLOW_BYTES;
+
+// One workgroup: validates the caller's CSR (offsets from 0, non-decreasing;
+// every path non-empty, its link ids in range and distinct; capacities
+// finite and > 0), then runs the exact solve over all F flows with link
+// state in the scratch array.
+__global__ __launch_bounds__(1024) void netsim_noalloc_solve_kernel(const double* cap, int L,
+                                                                    const int32_t* poff,
+                                                                    const int32_t* plink, int F,
+                                                                    double* rates, int64_t* status_out,
+                                                                    unsigned char* ws, int max_rounds) {
+  __shared__ XShared sh;
+  __shared__ int bad;
+  double* R = reinterpret_cast<double*>(ws + NA_HEAD_BYTES);
+  double* S = R + NA_MAX_LINKS;
+  int32_t* n = reinterpret_cast<int32_t*>(S + NA_MAX_LINKS);
+  int32_t* k = n + NA_MAX_LINKS;
+  int32_t* live0 = k + NA_MAX_LINKS;
+  int32_t* live1 = live0 + NA_MAX_LINKS;
+  int32_t* U = live1 + NA_MAX_LINKS;
+  int32_t* unf0 = U + NA_MAX_FLOWS;
+  int32_t* unf1 = unf0 + NA_MAX_FLOWS;
+  const int T = blockDim.x, tid = threadIdx.x;
+  if (tid == 0) bad = INT32_MAX;
+  __syncthreads();
+  if (tid == 0 && F > 0 && poff[0] != 0) atomicMin(&bad, 0);
+  for (int f = tid; f < F; f += T) {
+    const int e0 = poff[f], e1 = poff[f + 1];
+    bool ok = e1 > e0;
+    for (int e = e0; ok && e < e1; ++e) {
+      const int l = plink[e];
+      ok = l >= 0 && l < L;
+      for (int q = e0; ok && q < e; ++q) ok = plink[q] != l;
+    }
+    if (!ok) atomicMin(&bad, f);
+    U[f] = f;
+  }
+  for (int l = tid; l < L; l += T) {
+    const double c = cap[l];
+    if (!(c > 0.0) || !(c < XINF)) atomicMin(&bad, F + l);
+  }
+  __syncthreads();
+  int status = ST_BAD_INPUT;
+  int64_t levels = 0;
+  if (bad == INT32_MAX) {
+    Params P{};
+    P.poff = poff;
+    P.plink = plink;
+    P.capf = cap;
+    P.rate = rates;
+    P.xR = R;
+    P.xs = S;
+    P.xn = n;
+    P.xk = k;
+    P.xlive0 = live0;
+    P.xlive1 = live1;
+    P.unf0 = unf0;
+    P.unf1 = unf1;
+    P.max_rounds = max_rounds;
+    ScenCtl C{};
+    C.f0 = 0;
+    C.f1 = F;
+    C.l0 = 0;
+    C.l1 = L;
+    XLinks<false> lk{R, S, n, k, 0};
+    if (tid == 0) {
+      sh.fsw = 0;
+      sh.isw = 0;
+    }
+    __syncthreads();
+    int rb = 0;
+    status = F > 0 ? exact_solve<false>(P, &C, lk, sh, rb, U, F, levels) : ST_DONE;
+  }
+  if (tid == 0) {
+    // the C status codes of include/netsim.h
+    status_out[0] = status == ST_DONE ? 0 : status == ST_BAD_INPUT ? -1 : status == ST_ROUNDS ? -5 : -3;
+    status_out[1] = status == ST_BAD_INPUT ? (int64_t)bad : levels;
+  }
+}
+
+// The scratch array's device address on each device, found once per device.
+unsigned char* g_scratch_ptr[64];
+std::mutex g_scratch_mu;
+
 hipError_t launch_exact(const Params& p, int blocks, int threads, hipStream_t s) {
   if (p.exact_lds_bytes > 0) {
     hipError_t e = hipFuncSetAttribute((const void*)netsim_exact_kernel,
@@ -559,3 +659,46 @@ hipError_t launch_exact(const Params& p, int blocks, int threads, hipStream_t s)
 }
 
 }  // namespace netsim_dev
+
+// Scratch of the allocation-free entry point (see NA_* above).
+static __device__ __align__(256) unsigned char scratch[netsim_dev::NA_SCRATCH_BYTES];
+
+extern "C" netsim_status netsim_solve_rates_noalloc(int32_t device, int32_t num_links,
+                                                    const double* d_capacity_Bps, int32_t num_flows,
+                                                    const int32_t* d_path_off,
+                                                    const int32_t* d_path_link, double* d_rates,
+                                                    int64_t* d_status, void* hip_stream) {
+  using namespace netsim_dev;
+  auto fail = [](netsim_status code, const std::string& m) {
+    netsim_host::set_thread_error(m.c_str());
+    return code;
+  };
+  if (device < 0 || device >= 64) return fail(NETSIM_E_INVALID, "solve_rates_noalloc: bad device");
+  if (num_links < 0 || num_flows < 0) return fail(NETSIM_E_INVALID, "solve_rates_noalloc: negative size");
+  if (num_links > NA_MAX_LINKS || num_flows > NA_MAX_FLOWS)
+    return fail(NETSIM_E_LIMIT, "solve_rates_noalloc: more than " + std::to_string(NA_MAX_LINKS) +
+                                    " links or " + std::to_string(NA_MAX_FLOWS) + " flows");
+  if (!d_status || !d_path_off || (num_links > 0 && !d_capacity_Bps) ||
+      (num_flows > 0 && (!d_path_link || !d_rates)))
+    return fail(NETSIM_E_INVALID, "solve_rates_noalloc: NULL array");
+  hipError_t he = hipSetDevice(device);
+  if (he != hipSuccess) return fail(NETSIM_E_DEVICE, std::string("hipSetDevice: ") + hipGetErrorString(he));
+  unsigned char* ws = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+      void* p = nullptr;
+      he = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (he != hipSuccess || !p)
+        return fail(NETSIM_E_DEVICE, std::string("hipGetSymbolAddress: ") + hipGetErrorString(he));
+      g_scratch_ptr[device] = static_cast<unsigned char*>(p);
+    }
+    ws = g_scratch_ptr[device];
+  }
+  hipLaunchKernelGGL(netsim_noalloc_solve_kernel, dim3(1), dim3(1024), 0,
+                     static_cast<hipStream_t>(hip_stream), d_capacity_Bps, num_links, d_path_off,
+                     d_path_link, num_flows, d_rates, d_status, ws, num_flows + 1);
+  he = hipGetLastError();
+  if (he != hipSuccess) return fail(NETSIM_E_DEVICE, std::string("solve_rates_noalloc: ") + hipGetErrorString(he));
+  return NETSIM_OK;
+}

@@ -40,6 +40,10 @@ struct Scen {
 
 }  // namespace
 
+namespace netsim_host {
+void set_thread_error(const char* msg) { g_thread_err = msg; }
+}  // namespace netsim_host
+
 struct netsim {
   netsim_options opt{};
   std::vector<Scen> scen;

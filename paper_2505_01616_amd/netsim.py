@@ -119,6 +119,7 @@ _SIGS = {
     "netsim_update_start": (_I32, [_H, _I64, _D]),
     "netsim_gc": (_I32, [_H, _D]),
     "netsim_num_checkpoints": (_I32, [_H, ctypes.POINTER(_I64)]),
+    "netsim_solve_rates_noalloc": (_I32, [_I32, _I32, _P, _I32, _P, _P, _P, _P, _P]),
     "netsim_last_error": (ctypes.c_char_p, [_H]),
     "netsim_destroy": (None, [_H]),
 }
@@ -429,6 +430,15 @@ def netsim_num_checkpoints(h) -> int:
     n = _I64()
     _check(h, load_library().netsim_num_checkpoints(h, ctypes.byref(n)))
     return n.value
+
+
+def netsim_solve_rates_noalloc(device, num_links, d_cap, num_flows, d_path_off, d_path_link,
+                               d_rates, d_status, stream=None):
+    """Arguments are device addresses (ints, e.g. torch tensors' data_ptr());
+    enqueues the solve and returns; d_status[0] holds the solve's status."""
+    _check(None, load_library().netsim_solve_rates_noalloc(
+        int(device), int(num_links), _P(d_cap), int(num_flows), _P(d_path_off), _P(d_path_link),
+        _P(d_rates), _P(d_status), _stream(stream)))
 
 
 def netsim_last_error(h=None) -> str:
