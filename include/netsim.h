@@ -217,6 +217,11 @@ typedef struct {
   int32_t layout;            /* execution layout of the last launch (NETSIM_EXEC_GRID,
                                 _BLOCK, _CLUSTER or _EXACT; AUTO resolved)        */
   int32_t reserved;
+  int64_t links_swept;       /* sum over rounds of the links whose share the round
+                                computed (links with unfrozen flows): every level
+                                of exact mode; the share-table passes of the
+                                default solver (rounds run by helper workgroups,
+                                which have no such pass, add nothing)            */
 } netsim_stats;
 
 /* Fills *opt with the defaults (device 0, auto layout, no limits). */
@@ -478,6 +483,23 @@ netsim_status netsim_get_stats(const netsim_t* h, netsim_stats* stats);
  */
 netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active,
                                 const int64_t* active_ids, double* rates_out);
+
+/*
+ * Measurement of the two sweeps of a wide exact rate solve (the link-major
+ * per-link unfrozen count that starts the solve, and the first level's
+ * freezing sweep over the unfrozen flows' path records), as the whole-GPU
+ * solve of netsim_solve_once runs them for active_ids[0..n_active) of
+ * scenario scen (handle in exact mode; every id a distinct flow of the
+ * scenario with a path).  Each of `reps` repetitions first writes
+ * flush_bytes (0: none) of a scratch buffer to evict the caches, then times
+ * the count kernel into count_ms[r], writes the buffer again, runs the
+ * level's link pass and times the freezing sweep into freeze_ms[r] (HIP
+ * events on hip_stream).  Allocates the scratch buffer for the call.
+ * Leaves no simulation position: the next netsim_advance starts from t = 0.
+ */
+netsim_status netsim_bench_sweeps(netsim_t* h, int32_t scen, int64_t n_active,
+                                  const int64_t* active_ids, int32_t reps, int64_t flush_bytes,
+                                  void* hip_stream, double* count_ms, double* freeze_ms);
 
 /*
  * Allocation-free rate solve, for callers that cannot allocate device memory

@@ -26,6 +26,8 @@ struct Lists {
   int32_t solve_rc;        // status of a solve run by one workgroup
   int32_t fault;           // 1: bad fair share, 2: a work list overflowed or held a bad id
   uint32_t stamp;          // last freezing-round number used by the part's solves
+  int32_t pad;
+  int64_t lsw;             // links with unfrozen flows summed over the share-table passes
 };
 
 // Control block of one part in device memory.  A part is a set of flows of
@@ -52,6 +54,7 @@ struct ScenCtl {
   int64_t active_swept, pending_swept;
   int64_t reselected, wide_solves;
   int64_t assisted;        // re-solves run by helper workgroups (cluster kernel)
+  int64_t links_swept;     // links with unfrozen flows summed over link passes
   int32_t status;          // 0 ran to the end, 1 stopped at a limit, < 0 fault
   int32_t reserved;
   int64_t ticks[8];        // wall-clock ticks per phase (first thread of the group)
@@ -66,6 +69,18 @@ enum : int32_t {
   ST_ROUNDS = -5,          // round watchdog
   ST_BARRIER = -6,         // grid barrier timed out
   ST_OVERFLOW = -7         // a work list exceeded its capacity
+};
+
+// Counters of a wide exact solve run by the sweep kernels (sweep.hip), in
+// device memory: level minima (bit patterns of doubles, by level parity),
+// unfrozen and live list sizes (by parity), statistics.
+struct XGrid {
+  unsigned long long gmin[2];
+  int32_t cu[2];           // unfrozen flows entering the level of that parity
+  int32_t cl[2];           // live links entering the level of that parity
+  int32_t fault;           // 1: a non-positive or infinite level minimum
+  int32_t done;            // 1 once a level started with no unfrozen flow
+  unsigned long long levels, fsw, isw, lsw;  // iterations; flows, incidences, links swept
 };
 
 struct Params {
@@ -127,6 +142,13 @@ struct Params {
   int32_t* xn;             // [L] unfrozen flows
   int32_t* xk;             // [L] flows frozen at the current level
   int32_t* xlive0; int32_t* xlive1;  // [L] links with unfrozen flows (per part on [l0, l1))
+  // link-major incidence (exact mode): the flows of device link l are
+  // lfid[lfoff[l] .. lfoff[l+1]-1] (ascending), lflink[e] the link of entry e
+  const int32_t* lfoff;    // [L+1]
+  const int32_t* lfid;     // [nnz]
+  const int32_t* lflink;   // [nnz]
+  uint8_t* xact;           // [F] 1 while a flow of a wide exact solve is unfrozen
+  XGrid* xgrid;            // counters of a wide exact solve
   int32_t exact_lds_bytes; // dynamic shared memory of the exact kernel (link state
                            // of a part with at most exact_lds_bytes / 24 links)
   ScenCtl* ctl;            // [num_scen]
@@ -151,6 +173,16 @@ hipError_t cluster_capacity(int device, int* blocks);
 hipError_t launch_exact(const Params& p, int blocks, int threads, hipStream_t s);
 // Bytes of exact-mode link state per link.
 int exact_link_bytes();
+// A wide exact solve of part C's n flows listed in act0 + C.f0, on the whole
+// GPU (sweep.hip): begin (clear link state, flag the flows), count (per-link
+// unfrozen counts over the part's link-major incidences [e0, e1)), then per
+// level j = 0, 1, ... links and freeze, until xgrid->cu[j & 1] is 0.
+hipError_t grid_solve_begin(const Params& P, const ScenCtl& C, int n, hipStream_t s);
+hipError_t grid_solve_count(const Params& P, int e0, int e1, hipStream_t s);
+hipError_t grid_solve_links(const Params& P, const ScenCtl& C, int j, hipStream_t s);
+hipError_t grid_solve_freeze(const Params& P, const ScenCtl& C, int n, int j, hipStream_t s);
+// Streaming write of `bytes` (a multiple of 16) over buf.
+hipError_t launch_flush(void* buf, size_t bytes, uint32_t tag, hipStream_t s);
 
 }  // namespace netsim_dev
 

@@ -60,6 +60,7 @@ struct XShared {
   int32_t changed;    // the active set changed in this event
   int32_t fault;      // a work list held an id outside the part
   int64_t fsw, isw;   // flows / incidences swept (summed over waves)
+  int64_t lsw;        // links with unfrozen flows, summed over levels
 };
 
 __device__ __forceinline__ double xwave_min(double v) {
@@ -247,6 +248,7 @@ __device__ int exact_solve(const Params& P, const ScenCtl* C, XLinks<LDS>& lk, X
     }
     const double sstar = xblock_min(loc, sh, rb);
     nl = sh.nlive[lb ^ 1];
+    if (tid == 0) sh.lsw += nl;  // links whose share this level computed
     if (!(sstar > 0.0) || !(sstar < XINF)) {
       status = ST_BAD_SHARE;
       break;
@@ -328,6 +330,7 @@ __device__ void exact_loop(const Params& P, int sc, XShared& sh, unsigned char* 
   if (tid == 0) {
     sh.fsw = resume ? C->flows_swept : 0;
     sh.isw = resume ? C->incidences_swept : 0;
+    sh.lsw = resume ? C->links_swept : 0;
     sh.fault = 0;
     sh.npend[pb] = np;  // releases append after the pending flows
   }
@@ -497,6 +500,7 @@ __device__ void exact_loop(const Params& P, int sc, XShared& sh, unsigned char* 
     C->rounds = rounds;
     C->flows_swept = sh.fsw;
     C->incidences_swept = sh.isw;
+    C->links_swept = sh.lsw;
     C->active_swept = asw;
     C->pending_swept = psw;
     C->status = status;
@@ -511,6 +515,7 @@ __device__ void exact_solve_only(const Params& P, int sc, XShared& sh, unsigned 
   if (threadIdx.x == 0) {
     sh.fsw = 0;
     sh.isw = 0;
+    sh.lsw = 0;
   }
   __syncthreads();
   int rb = 0;
@@ -523,6 +528,7 @@ __device__ void exact_solve_only(const Params& P, int sc, XShared& sh, unsigned 
     C->rounds = rounds;
     C->flows_swept = sh.fsw;
     C->incidences_swept = sh.isw;
+    C->links_swept = sh.lsw;
     C->status = rc;
   }
 }
@@ -632,6 +638,7 @@ __global__ __launch_bounds__(1024) void netsim_noalloc_solve_kernel(const double
     if (tid == 0) {
       sh.fsw = 0;
       sh.isw = 0;
+      sh.lsw = 0;
     }
     __syncthreads();
     int rb = 0;

@@ -623,10 +623,16 @@ struct LinksShared {
     fl[nl] = 0;
     sh[nl] = INF;
   }
-  // link pass of a round: the share of every link with an unfrozen flow
-  __device__ __forceinline__ void fill_table(int tid, int T, int nl) {
+  // link pass of a round: the share of every link with an unfrozen flow;
+  // returns how many of those this thread saw
+  __device__ __forceinline__ int fill_table(int tid, int T, int nl) {
+    int c = 0;
     for (int i = tid; i < nl; i += T)
-      if (n[i] > 0) sh[i] = ((double)R[i] / (double)n[i]) * inv;
+      if (n[i] > 0) {
+        sh[i] = ((double)R[i] / (double)n[i]) * inv;
+        ++c;
+      }
+    return c;
   }
   __device__ __forceinline__ void set(int l, int64_t Rv, int64_t nv) {
     R[l - l0] = Rv;
@@ -696,7 +702,10 @@ __device__ __forceinline__ double share_of(const LK& lk, int l) {
 template <class G, class LK>
 __device__ __forceinline__ void round_table(G& g, LK& lk, const ScenCtl* C) {
   if constexpr (LK::kTable) {
-    lk.fill_table(g.tid(), g.nthr(), C->l1 - C->l0);
+    int c = lk.fill_table(g.tid(), g.nthr(), C->l1 - C->l0);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+    if (lane_id() == 0 && c > 0) g.add(&g.lists(const_cast<ScenCtl*>(C))->lsw, (int64_t)c);
     g.sync();
   }
 }
@@ -1671,6 +1680,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     tl->sel = resume ? C->reselected : 0;
     tl->wide = resume ? C->wide_solves : 0;
     tl->asst = resume ? C->assisted : 0;
+    g.store(&K->lsw, (int64_t)0);  // this launch's share-table passes
   }
   int64_t& rounds = tl->rounds;
   int64_t& fsw = tl->fsw;
@@ -2121,6 +2131,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     C->reselected = tl->sel;
     C->wide_solves = tl->wide;
     C->assisted = tl->asst;
+    C->links_swept = (resume ? C->links_swept : 0) + g.load(&K->lsw);
     C->status = status;
     for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)tl->clk[k];
   }

@@ -67,6 +67,7 @@ struct netsim {
   std::vector<double> h_rel0;
   std::vector<int32_t> h_pend0;
   std::vector<ScenCtl> h_ctl0;
+  std::vector<int32_t> h_lfoff;       // exact mode: link-major incidence offsets
   double scale = 1.0;
   void* d_block = nullptr;            // one allocation holding every device array
   char* persist = nullptr;            // the persistent dynamic state inside it
@@ -253,6 +254,12 @@ constexpr int kCusPerXcd = 32;
 // to 6,485 links per part) and threads per workgroup.
 constexpr int64_t kExactLdsBytes = 152 * 1024;
 constexpr int kExactThreads = 512;
+// Exact mode: a rate solve without an event loop of at least this many flows
+// runs on the whole GPU (sweep.hip) instead of one workgroup; levels are
+// enqueued this many at a time between looks at the unfrozen count.
+constexpr int32_t kExactGridMin = 16384;
+constexpr int kGridLevelBatch = 64;
+constexpr int DEBUG_EXACT_GRID = 32;  // options.debug bit 5: every such solve on the whole GPU
 
 netsim_status prepare(netsim_t* h) {
   const int32_t S = (int32_t)h->scen.size();
@@ -465,6 +472,26 @@ netsim_status prepare(netsim_t* h) {
         succ[(size_t)fill[(size_t)pred]++] = h->dev_of_flow[(size_t)id];
       }
   }
+  // link-major incidence (exact mode's wide solves): flows of each device
+  // link in ascending device order, and each entry's link
+  const bool exact = h->opt.exact != 0;
+  std::vector<int32_t> lfoff, lfid, lflink;
+  if (exact) {
+    lfoff.assign((size_t)ld + 1, 0);
+    for (int64_t k = 0; k < h->nnz; ++k) lfoff[(size_t)plink[(size_t)k] + 1] += 1;
+    for (int64_t l = 0; l < ld; ++l) lfoff[(size_t)l + 1] += lfoff[(size_t)l];
+    lfid.assign((size_t)std::max<int64_t>(h->nnz, 1), 0);
+    lflink.assign((size_t)std::max<int64_t>(h->nnz, 1), 0);
+    std::vector<int32_t> fill(lfoff.begin(), lfoff.end() - 1);
+    for (int64_t d = 0; d < F; ++d)
+      for (int32_t k = poff[(size_t)d]; k < poff[(size_t)d + 1]; ++k) {
+        const int32_t l = plink[(size_t)k];
+        const int32_t at = fill[(size_t)l]++;
+        lfid[(size_t)at] = (int32_t)d;
+        lflink[(size_t)at] = l;
+      }
+  }
+  h->h_lfoff = lfoff;
   // initial dynamic state
   h->h_cnt0 = ndeps;
   h->h_rel0.assign((size_t)std::max<int64_t>(F, 1), 0.0);
@@ -539,6 +566,11 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.xk, sizeof(int32_t) * XL},
       {(void**)&P.xlive0, sizeof(int32_t) * XL},
       {(void**)&P.xlive1, sizeof(int32_t) * XL},
+      {(void**)&P.lfoff, sizeof(int32_t) * (XL + 1)},
+      {(void**)&P.lfid, sizeof(int32_t) * (exact ? lfid.size() : 1)},
+      {(void**)&P.lflink, sizeof(int32_t) * (exact ? lflink.size() : 1)},
+      {(void**)&P.xact, exact ? Fz : 1},
+      {(void**)&P.xgrid, sizeof(netsim_dev::XGrid)},
   };
   size_t total = 0;
   for (auto& p : parts) total += (p.bytes + 255) & ~size_t(255);
@@ -569,6 +601,9 @@ netsim_status prepare(netsim_t* h) {
       {path16.data(), P.path16, sizeof(uint16_t) * path16.size()},
       {lat.data(), P.lat, any_lat ? sizeof(double) * lat.size() : 0},
       {capf.data(), P.capf, h->opt.exact ? sizeof(double) * capf.size() : 0},
+      {lfoff.data(), P.lfoff, sizeof(int32_t) * lfoff.size()},
+      {lfid.data(), P.lfid, sizeof(int32_t) * lfid.size()},
+      {lflink.data(), P.lflink, sizeof(int32_t) * lflink.size()},
   };
   for (const Up& u : ups) {
     if (u.bytes == 0) continue;
@@ -823,6 +858,7 @@ netsim_status simulate(netsim_t* h, hipStream_t st, bool resume, int64_t max_eve
     s.reselected += c.reselected;
     s.wide_solves += c.wide_solves;
     s.assisted_solves += c.assisted;
+    s.links_swept += c.links_swept;
     s.layout = h->layout;
     s.sim_time = std::max(s.sim_time, c.t);
     if (c.status != 0) s.complete = 0;
@@ -839,6 +875,37 @@ netsim_status simulate(netsim_t* h, hipStream_t st, bool resume, int64_t max_eve
   return rc;
 }
 
+
+// A wide exact solve of the n flows of part p listed in its act0 slice, on
+// the whole GPU (sweep.hip).  Levels are enqueued in batches; the host reads
+// the unfrozen count after each batch.  Adds the solve's statistics to *out.
+netsim_status grid_solve(netsim_t* h, hipStream_t st, int32_t p, int32_t n, netsim_dev::XGrid* out) {
+  const Params& P = h->prm;
+  const ScenCtl& C = h->h_ctl0[(size_t)p];
+  hipError_t he = netsim_dev::grid_solve_begin(P, C, n, st);
+  if (he == hipSuccess)
+    he = netsim_dev::grid_solve_count(P, h->h_lfoff[(size_t)C.l0], h->h_lfoff[(size_t)C.l1], st);
+  const int64_t limit = h->opt.max_rounds > 0 ? h->opt.max_rounds : (int64_t)n + 1;
+  netsim_dev::XGrid g{};
+  for (int j = 0; he == hipSuccess;) {
+    for (int b = 0; b < kGridLevelBatch && he == hipSuccess; ++b, ++j) {
+      he = netsim_dev::grid_solve_links(P, C, j, st);
+      if (he == hipSuccess) he = netsim_dev::grid_solve_freeze(P, C, n, j, st);
+    }
+    if (he == hipSuccess) he = hipMemcpyAsync(&g, P.xgrid, sizeof g, hipMemcpyDeviceToHost, st);
+    if (he == hipSuccess) he = hipStreamSynchronize(st);
+    if (he != hipSuccess) break;
+    if (g.fault) return fail(h, NETSIM_E_DEVICE, "device solver fault: non-positive fair share");
+    if (g.done || g.cu[j & 1] == 0) break;
+    if ((int64_t)g.levels > limit) return fail(h, NETSIM_E_LIMIT, "device solver fault: round watchdog fired");
+  }
+  if (he != hipSuccess) return hip_fail(h, he, "wide exact solve");
+  out->levels += g.levels;
+  out->fsw += g.fsw;
+  out->isw += g.isw;
+  out->lsw += g.lsw;
+  return NETSIM_OK;
+}
 
 // Part of device flow d (parts hold consecutive device flows).
 int32_t part_of_dev(const netsim_t* h, int32_t d) {
@@ -1741,6 +1808,16 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, con
     for (int64_t e = h->p_off[(size_t)id]; e < h->p_off[(size_t)id + 1]; ++e)
       nact[(size_t)h->dev_link[(size_t)scen][(size_t)h->p_link[(size_t)e]]] += 1;
   }
+  // exact mode: wide solves on the whole GPU, the others one workgroup each
+  std::vector<std::pair<int32_t, int32_t>> wide;
+  if (h->opt.exact)
+    for (int32_t k = 0; k < h->num_parts; ++k) {
+      ScenCtl& c = ctl[(size_t)k];
+      if (c.n_solve > 0 && (c.n_solve >= kExactGridMin || (h->opt.debug & DEBUG_EXACT_GRID))) {
+        wide.emplace_back(k, c.n_solve);
+        c.n_solve = 0;
+      }
+    }
   he = hipMemcpy(P.ctl, ctl.data(), sizeof(ScenCtl) * ctl.size(), hipMemcpyHostToDevice);
   if (he == hipSuccess && h->F > 0)
     he = hipMemcpy(P.act0, list.data(), sizeof(int32_t) * (size_t)h->F, hipMemcpyHostToDevice);
@@ -1752,6 +1829,29 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, con
   std::vector<ScenCtl> out;
   rc = collect(h, &out);
   if (rc) return rc;
+  netsim_dev::XGrid gs{};
+  if (!wide.empty()) {
+    hipEvent_t e0, e1;
+    he = hipEventCreate(&e0);
+    if (he == hipSuccess) he = hipEventCreate(&e1);
+    if (he != hipSuccess) return hip_fail(h, he, "hipEventCreate");
+    he = hipEventRecord(e0, nullptr);
+    for (const auto& w : wide) {
+      if (he != hipSuccess) break;
+      rc = grid_solve(h, nullptr, w.first, w.second, &gs);
+      if (rc) break;
+      out[(size_t)w.first].solves += 1;
+    }
+    float gms = 0.0f;
+    if (he == hipSuccess && !rc) he = hipEventRecord(e1, nullptr);
+    if (he == hipSuccess && !rc) he = hipEventSynchronize(e1);
+    if (he == hipSuccess && !rc) he = hipEventElapsedTime(&gms, e0, e1);
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (rc) return rc;
+    if (he != hipSuccess) return hip_fail(h, he, "wide exact solve timing");
+    ms += gms;
+  }
   std::vector<double> rate((size_t)std::max<int64_t>(h->F, 1));
   he = hipMemcpy(rate.data(), P.rate, sizeof(double) * (size_t)std::max<int64_t>(h->F, 1), hipMemcpyDeviceToHost);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (rates)");
@@ -1770,8 +1870,91 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, con
     h->stats.rounds += c.rounds;
     h->stats.flows_swept += c.flows_swept;
     h->stats.incidences_swept += c.incidences_swept;
+    h->stats.links_swept += c.links_swept;
     for (int j = 0; j < 8; ++j) h->stats.phase_seconds[j] += (double)c.ticks[j] / (1e3 * khz);
   }
+  h->stats.rounds += (int64_t)gs.levels;
+  h->stats.flows_swept += (int64_t)gs.fsw;
+  h->stats.incidences_swept += (int64_t)gs.isw;
+  h->stats.links_swept += (int64_t)gs.lsw;
+  h->stats.layout = h->opt.exact ? NETSIM_EXEC_EXACT : h->layout;
+  return NETSIM_OK;
+}
+
+netsim_status netsim_bench_sweeps(netsim_t* h, int32_t scen, int64_t n_active, const int64_t* active_ids,
+                                  int32_t reps, int64_t flush_bytes, void* hip_stream, double* count_ms,
+                                  double* freeze_ms) {
+  if (!h) return fail(nullptr, NETSIM_E_INVALID, "bench_sweeps: handle is NULL");
+  if (!h->opt.exact) return fail(h, NETSIM_E_STATE, "bench_sweeps: needs a handle in exact mode");
+  if (scen < 0 || scen >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "bench_sweeps: bad scenario");
+  if (n_active < 1 || n_active > std::numeric_limits<int32_t>::max() || !active_ids || reps < 1 ||
+      flush_bytes < 0 || !count_ms || !freeze_ms)
+    return fail(h, NETSIM_E_INVALID, "bench_sweeps: bad arguments");
+  const int64_t F = (int64_t)h->f_bytes.size();
+  std::vector<char> seen((size_t)F, 0);
+  for (int64_t k = 0; k < n_active; ++k) {
+    const int64_t id = active_ids[k];
+    if (id < 0 || id >= F || h->f_scen[(size_t)id] != scen) return fail(h, NETSIM_E_INVALID, "bench_sweeps: id not in the scenario");
+    if (seen[(size_t)id]) return fail(h, NETSIM_E_INVALID, "bench_sweeps: repeated id");
+    if (h->p_off[(size_t)id + 1] == h->p_off[(size_t)id]) return fail(h, NETSIM_E_INVALID, "bench_sweeps: flow without a path");
+    seen[(size_t)id] = 1;
+  }
+  netsim_status rc;
+  if (!h->prepared) {
+    rc = prepare(h);
+    if (rc) return rc;
+  }
+  hipError_t he = hipSetDevice(h->opt.device);
+  if (he != hipSuccess) return hip_fail(h, he, "hipSetDevice");
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  rc = reset_state(h, st);
+  if (rc) return rc;
+  int32_t p = -1;  // exact mode: one part per scenario
+  for (int32_t k = 0; k < h->num_parts; ++k)
+    if (h->h_ctl0[(size_t)k].scen == scen) p = k;
+  if (p < 0) return fail(h, NETSIM_E_INVALID, "bench_sweeps: the scenario has no flows");
+  const ScenCtl& C = h->h_ctl0[(size_t)p];
+  std::vector<int32_t> list((size_t)n_active);
+  for (int64_t k = 0; k < n_active; ++k) list[(size_t)k] = h->dev_of_flow[(size_t)active_ids[k]];
+  const Params& P = h->prm;
+  he = hipMemcpy(P.act0 + C.f0, list.data(), sizeof(int32_t) * list.size(), hipMemcpyHostToDevice);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (bench_sweeps setup)");
+  void* buf = nullptr;
+  const size_t fb = (size_t)flush_bytes / 16 * 16;
+  if (fb > 0 && hipMalloc(&buf, fb) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(h, NETSIM_E_NOMEM, "bench_sweeps: no memory for the flush buffer");
+  }
+  hipEvent_t ev[4] = {};
+  for (auto& e : ev)
+    if (he == hipSuccess) he = hipEventCreate(&e);
+  const int n = (int)n_active;
+  const int e0 = h->h_lfoff[(size_t)C.l0], e1 = h->h_lfoff[(size_t)C.l1];
+  for (int32_t r = 0; r < reps && he == hipSuccess; ++r) {
+    // cold caches before each sweep: a streaming write larger than the L2s
+    // and the Infinity Cache together
+    if (fb > 0) he = netsim_dev::launch_flush(buf, fb, (uint32_t)(2 * r), st);
+    if (he == hipSuccess) he = netsim_dev::grid_solve_begin(P, C, n, st);
+    if (he == hipSuccess) he = hipEventRecord(ev[0], st);
+    if (he == hipSuccess) he = netsim_dev::grid_solve_count(P, e0, e1, st);
+    if (he == hipSuccess) he = hipEventRecord(ev[1], st);
+    if (he == hipSuccess && fb > 0) he = netsim_dev::launch_flush(buf, fb, (uint32_t)(2 * r + 1), st);
+    if (he == hipSuccess) he = netsim_dev::grid_solve_links(P, C, 0, st);
+    if (he == hipSuccess) he = hipEventRecord(ev[2], st);
+    if (he == hipSuccess) he = netsim_dev::grid_solve_freeze(P, C, n, 0, st);
+    if (he == hipSuccess) he = hipEventRecord(ev[3], st);
+    if (he == hipSuccess) he = hipEventSynchronize(ev[3]);
+    float a = 0.0f, b = 0.0f;
+    if (he == hipSuccess) he = hipEventElapsedTime(&a, ev[0], ev[1]);
+    if (he == hipSuccess) he = hipEventElapsedTime(&b, ev[2], ev[3]);
+    count_ms[r] = a;
+    freeze_ms[r] = b;
+  }
+  for (auto& e : ev)
+    if (e) (void)hipEventDestroy(e);
+  if (buf) (void)hipFree(buf);
+  if (he != hipSuccess) return hip_fail(h, he, "bench_sweeps");
+  h->has_state = false;  // the device holds no simulation position now
   return NETSIM_OK;
 }
 

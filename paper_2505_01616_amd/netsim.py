@@ -63,7 +63,7 @@ class netsim_stats(ctypes.Structure):
                 ("sim_time", ctypes.c_double), ("device_seconds", ctypes.c_double),
                 ("upload_seconds", ctypes.c_double), ("phase_seconds", ctypes.c_double * 8),
                 ("assisted_solves", ctypes.c_int64), ("layout", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("reserved", ctypes.c_int32), ("links_swept", ctypes.c_int64)]
 
     def as_dict(self):
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
@@ -120,6 +120,7 @@ _SIGS = {
     "netsim_gc": (_I32, [_H, _D]),
     "netsim_num_checkpoints": (_I32, [_H, ctypes.POINTER(_I64)]),
     "netsim_solve_rates_noalloc": (_I32, [_I32, _I32, _P, _I32, _P, _P, _P, _P, _P]),
+    "netsim_bench_sweeps": (_I32, [_H, _I32, _I64, _P, _I32, _I64, _P, _P, _P]),
     "netsim_last_error": (ctypes.c_char_p, [_H]),
     "netsim_destroy": (None, [_H]),
 }
@@ -430,6 +431,16 @@ def netsim_num_checkpoints(h) -> int:
     n = _I64()
     _check(h, load_library().netsim_num_checkpoints(h, ctypes.byref(n)))
     return n.value
+
+
+def netsim_bench_sweeps(h, scen, active_ids, reps, flush_bytes, stream=None):
+    """Per-repetition device times (ms) of the count and freezing sweeps."""
+    ids = _arr(active_ids, np.int64)
+    a = np.zeros(int(reps))
+    b = np.zeros(int(reps))
+    _check(h, load_library().netsim_bench_sweeps(h, scen, len(ids), _ptr(ids), int(reps),
+                                                 int(flush_bytes), _stream(stream), _ptr(a), _ptr(b)))
+    return a, b
 
 
 def netsim_solve_rates_noalloc(device, num_links, d_cap, num_flows, d_path_off, d_path_link,

@@ -264,8 +264,10 @@ def test_exact_solve_once_full_width():
         stats = ns.netsim_get_stats(ld.handle)
     finally:
         ld.close()
-    _say("full-width exact solve: device s", stats["device_seconds"], "levels", stats["rounds"])
+    _say("full-width exact solve (whole GPU): device s", stats["device_seconds"], "levels",
+         stats["rounds"], "links swept", stats["links_swept"])
     _same(rates, ref)
+    assert stats["layout"] == ns.EXEC_EXACT
 
 
 def test_exact_watchdog_and_empty():
@@ -282,3 +284,73 @@ def test_exact_watchdog_and_empty():
     fins, stats = pr.run_program(Program("e", [empty, one]), ns.make_options(exact=1))
     assert len(fins[0]) == 0
     assert np.array_equal(fins[1], np.array([3.0, 3.0]))
+
+
+@pytest.mark.parametrize("mode", ["flat", "chained"])
+def test_wide_solve_on_the_whole_gpu_equals_one_workgroup(mode):
+    """The whole-GPU exact solve (count, links and freezing kernels) forced on
+    C1's first solve gives the one-workgroup exact solve's rates bit for bit,
+    with the same iteration, flow, incidence and link counts, and the
+    oracle's rates."""
+    ns, pr = _gpu()
+    _say(f"test_wide_solve_on_the_whole_gpu_equals_one_workgroup mode={mode}")
+    program = configs.c1(1, mode=mode)
+    fs = oflows.expand(program.scenarios[0])
+    act = np.nonzero((fs.nbytes > 0) & (np.diff(fs.dep_off) == 0))[0]
+    ref = osim.solve_rates(fs.cap, fs.path_off, fs.path_link, act)
+    out = {}
+    for name, dbg in (("block", 0), ("grid", 32)):
+        ld = pr.load_program(program, ns.make_options(exact=1, debug=dbg))
+        try:
+            out[name] = (ns.netsim_solve_once(ld.handle, 0, act), ns.netsim_get_stats(ld.handle))
+        finally:
+            ld.close()
+    (rb, sb), (rg, sg) = out["block"], out["grid"]
+    _same(rg, ref)
+    assert np.array_equal(rg, rb)
+    for k in ("rounds", "flows_swept", "incidences_swept", "links_swept"):
+        assert sg[k] == sb[k], k
+    assert sg["rounds"] > 1
+
+
+def test_wide_solve_long_paths():
+    """Paths of up to 10 links (no 16-byte path records: the CSR form of the
+    freezing sweep), random capacities, one wide solve against the oracle."""
+    ns, pr = _gpu()
+    _say("test_wide_solve_long_paths")
+    rng = np.random.default_rng(7)
+    L = 300
+    caps = rng.uniform(1.0, 50.0, L)
+    flows = []
+    for i in range(20000):
+        deg = int(rng.integers(1, 11))
+        flows.append({"path": list(rng.choice(L, size=deg, replace=False)), "nbytes": 1.0})
+    from helpers import explicit
+    sc = explicit(caps, flows)
+    fs = oflows.expand(sc)
+    act = np.arange(fs.F)
+    ref = osim.solve_rates(fs.cap, fs.path_off, fs.path_link, act)
+    ld = pr.load_program(Program("long", [sc]), ns.make_options(exact=1))
+    try:
+        rates = ns.netsim_solve_once(ld.handle, 0, act)
+        st = ns.netsim_get_stats(ld.handle)
+    finally:
+        ld.close()
+    _same(rates, ref)
+    assert st["rounds"] > 10
+
+
+def test_bench_sweeps_runs_and_leaves_no_position():
+    ns, pr = _gpu()
+    _say("test_bench_sweeps_runs_and_leaves_no_position")
+    program = configs.c4(4, blocks=1, locals_=8, phases=1)
+    fs = oflows.expand(program.scenarios[0])
+    act = np.nonzero(fs.nbytes > 0)[0]
+    ld = pr.load_program(program, ns.make_options(exact=1))
+    try:
+        a, b = ns.netsim_bench_sweeps(ld.handle, 0, act, 3, 64 << 20)
+        assert np.all(a > 0) and np.all(b > 0)
+        rates = ns.netsim_solve_once(ld.handle, 0, act)
+    finally:
+        ld.close()
+    _same(rates, osim.solve_rates(fs.cap, fs.path_off, fs.path_link, act))
