@@ -14,8 +14,10 @@ first.  Inputs (flows, routes, capacities) are resident in HBM
 before timing starts; the per-run state reset is outside the kernel time.
 
 Prints one JSON line, with the roofline of the event-loop kernel
-(algorithmic bytes per launch / launch duration, against 8 TB/s) and the
-CPU oracle's rate on a bounded sample of the same workload.
+(algorithmic bytes per launch / launch duration, against 8 TB/s), the
+cold-cache measurement of the wide exact solve's sweeps at the shape of one
+all-to-all phase (roofline_sweep), and the CPU oracle's rate on a bounded
+sample of the same workload (one independent block, on its own clock).
 """
 
 from __future__ import annotations
@@ -32,44 +34,139 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 
-# Algorithmic bytes: what each unit of work must move at least once per
-# visit (the byte model of the event-loop kernel).
-BYTES_PER_FLOW_ROUND = 28      # list entry 4 + path offsets 8 + min-share write 8 + read 8
-BYTES_PER_INCIDENCE_ROUND = 21  # link id 4+4 + residual capacity 8 + count 4 + flag 1
-BYTES_PER_ACTIVE_EVENT = 20    # slot: predicted completion 8 + flow id 4 + rate 8
-BYTES_PER_PENDING_EVENT = 28   # list in 4 + release time 8, twice, + list out 4
+# Algorithmic bytes of the max-min path: what progressive filling must move
+# per unit of work, whatever the layout (link state in shared memory counts
+# like link state in HBM).
+#   per round:   4 B link id + 8 B gathered share per unfrozen incidence;
+#                8 B path offsets + 1 B frozen flag per unfrozen flow;
+#                36 B per link whose share the round computes (R, n, k read;
+#                R, n, s written);
+#   per freeze:  9 B (rate + flag written) per flow frozen;
+#   per event:   24 B (remaining bytes, rate, predicted completion) per active
+#                flow; 12 B (id + release time) per pending flow looked at.
+B_INCIDENCE_ROUND = 12
+B_FLOW_ROUND = 9
+B_LINK_ROUND = 36
+B_FROZEN = 9
+B_ACTIVE_EVENT = 24
+B_PENDING_EVENT = 12
 
 
-def algorithmic_bytes(st: dict) -> float:
-    return (BYTES_PER_FLOW_ROUND * st["flows_swept"] + BYTES_PER_INCIDENCE_ROUND * st["incidences_swept"]
-            + BYTES_PER_ACTIVE_EVENT * st["active_swept"] + BYTES_PER_PENDING_EVENT * st["pending_swept"])
+def algorithmic_bytes(st: dict, frozen: int) -> float:
+    return (B_INCIDENCE_ROUND * st["incidences_swept"] + B_FLOW_ROUND * st["flows_swept"]
+            + B_LINK_ROUND * st["links_swept"] + B_FROZEN * frozen
+            + B_ACTIVE_EVENT * st["active_swept"] + B_PENDING_EVENT * st["pending_swept"])
 
 
-# The oracle is far too slow for the whole workload (a solve over ~258k
-# flows takes it ~0.1 s), so it is timed on a bounded sample: events 65..192
-# of the workload on one clock (the first 64 events are the arrivals of the
-# 64 groups; from then on every group is active), by differencing runs to 64
-# and 192 events.
-STEADY = (64, 192)
+# The oracle as it stands, on a bounded sample of the same work: one of the
+# eight independent 64-server blocks of the workload (the unit one part of
+# the GPU simulation runs, on its own clock as the part does), events 65 ..
+# 65 + SAMPLE_EVENTS of that block (the first 64 events are the arrivals of
+# its groups), timed as the difference of runs to 64 and to 64 +
+# SAMPLE_EVENTS events (about 15 s on one core).
+SAMPLE_EVENTS = 1000
+C4_BLOCK_FLOWS = 129048
 
 
-def cpu_baseline():
-    """The fp64 oracle (single thread, as it stands) on events 65..192 of C4."""
+def cpu_baseline(total_events: int):
+    """The fp64 oracle (single thread) on events 65..1064 of one C4 block."""
+    import platform
     from oracle import flows as oflows
     from oracle import sim as osim
     from workloads import configs
-    fs = oflows.expand(configs.c4(4).scenarios[0])
+    fs = oflows.expand(configs.c4(4, blocks=1).scenarios[0])
+    assert fs.F == C4_BLOCK_FLOWS
     t = []
-    for e in STEADY:
+    for e in (64, 64 + SAMPLE_EVENTS):
         t0 = time.perf_counter()
         r = osim.run_flowset(fs, max_events=e)
         t.append((time.perf_counter() - t0, r.solves, r.events))
     dt = t[1][0] - t[0][0]
-    return {"value": (t[1][1] - t[0][1]) / dt, "unit": "solves/s", "cores": 1, "kind": "oracle",
-            "events_per_s": (t[1][2] - t[0][2]) / dt, "seconds": t[0][0] + t[1][0],
-            "sample": f"events {STEADY[0] + 1}..{STEADY[1]} of the 4096-GPU all-to-all workload "
-                      f"(every group active, ~258k flows per solve), timed as the difference "
-                      f"of runs to {STEADY[0]} and {STEADY[1]} events; fp64 oracle, one thread"}
+    solves_per_s = (t[1][1] - t[0][1]) / dt
+    events_per_s = (t[1][2] - t[0][2]) / dt
+    cpu = platform.processor() or ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    cpu = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": solves_per_s, "unit": "solves/s", "cores": 1, "kind": "oracle",
+            "events_per_s": events_per_s, "seconds": t[0][0] + t[1][0], "cpu_model": cpu,
+            "host_threads": os.cpu_count(),
+            "projected_complete_s_at_sample_rate": total_events / events_per_s,
+            "sample": f"events 65..{64 + SAMPLE_EVENTS} of one 64-server block of the 4096-GPU "
+                      f"all-to-all (129,048 flows, the unit one GPU part simulates, on its own "
+                      f"clock), timed as the difference of runs to 64 and {64 + SAMPLE_EVENTS} "
+                      f"events; fp64 oracle, one thread; solves and events are per part as on "
+                      f"the GPU; the sample is the densest stretch of the run (the first "
+                      f"phase, every group active at full width), so the projection of the "
+                      f"workload's {total_events} part events at its rate is an upper bound"}
+
+
+def sweep_bench(ns, prog, stream, reps=20, flush=1 << 30):
+    """Cold-cache timing of the two sweeps of a wide exact solve at the shape
+    of the 4096-GPU workload at its start: the full workload loaded (one part
+    in exact mode: 1,032,384 flows, 5,144,576 incidences, 20,480 links), every
+    flow of the first all-to-all phase active (258,048 flows, 1,286,144
+    incidences).  The per-link count sweeps the part's whole link-major
+    incidence (flows of later phases count as inactive), the freezing sweep
+    the 258,048 unfrozen flows of the first level.  Before each sweep a 1 GiB
+    streaming write evicts the L2s and the Infinity Cache.  Then the complete
+    wide solve of that set (all its progressive-filling levels)."""
+    import numpy as np
+    from workloads import configs
+    program = configs.c4(4)
+    ld = prog.load_program(program, ns.make_options(exact=1))
+    h = ld.handle
+    try:
+        ex = ns.netsim_export_flows(h)
+        act = np.nonzero((ex["nbytes"] > 0) & (np.diff(ex["dep_off"]) == 0))[0]
+        nnz_all = int(len(ex["path_link"]))
+        nnz = int(np.diff(ex["path_off"])[act].sum())
+        links = int(len(np.unique(ex["path_link"])))
+        t = ns.netsim_bench_sweeps(h, 0, act, reps, flush, stream)
+        ns.netsim_solve_once(h, 0, act)
+        st = ns.netsim_get_stats(h)
+    finally:
+        ld.close()
+    F = len(act)
+    # freezing sweep of the first level (every flow unfrozen): the per-round
+    # terms of the byte model
+    frz_bytes = B_INCIDENCE_ROUND * nnz + B_FLOW_ROUND * F
+    # per-link count over the whole link-major incidence: flow id 4 B + its
+    # flag 1 B per entry; per link the offsets 4 B and the count 4 B
+    cnt_bytes = 5 * nnz_all + 8 * links
+    # work-efficient lower bound of one solve: every incidence and flow
+    # touched a constant number of times
+    we_bytes = 16 * nnz + 24 * F
+
+    def leg(kernel, ab, ev, kern):
+        e, k = float(np.median(ev)) * 1e-3, float(np.median(kern)) * 1e-3
+        return {"kernel": kernel, "algorithmic_bytes": ab,
+                "kernel_s": k, "achieved": ab / k / 1e9, "frac": ab / k / 1e9 / HBM_PEAK_GBPS,
+                "event_s": e, "achieved_incl_dispatch": ab / e / 1e9, "unit": "GB/s",
+                "kernel_s_min": float(np.min(kern)) * 1e-3}
+
+    sol = st["device_seconds"]
+    return {
+        "shape": {"flows_active": F, "incidences_active": nnz, "incidences_part": nnz_all,
+                  "links": links},
+        "flush_bytes": flush, "reps": reps,
+        "timing": "kernel_s: first workgroup start to last workgroup end on the device wall "
+                  "clock (median over reps); event_s: HIP events around the launch",
+        "freeze_sweep": leg("exact_freeze_kernel", frz_bytes, t["freeze_ms"], t["freeze_kernel_ms"]),
+        "link_count": leg("exact_count_kernel", cnt_bytes, t["count_ms"], t["count_kernel_ms"]),
+        "full_solve": {"device_s": sol, "levels": st["rounds"], "flows_swept": st["flows_swept"],
+                       "incidences_swept": st["incidences_swept"], "links_swept": st["links_swept"],
+                       "algorithmic_bytes": B_INCIDENCE_ROUND * st["incidences_swept"]
+                       + B_FLOW_ROUND * st["flows_swept"] + B_LINK_ROUND * st["links_swept"]
+                       + B_FROZEN * F,
+                       "work_efficient_bytes": we_bytes,
+                       "work_efficient_GBps": we_bytes / sol / 1e9},
+    }
 
 
 def traffic_from_profile(kernel: str, steps: int):
@@ -138,6 +235,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=1, help="untimed complete simulations first")
     ap.add_argument("--exec", choices=["grid", "block", "cluster", "auto"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the cold-cache sweep measurement of the wide exact solve")
+    ap.add_argument("--sweep-only", action="store_true",
+                    help="run only the cold-cache sweep measurement (one JSON line)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM counters)")
     ap.add_argument("--rollback", action="store_true",
@@ -170,12 +271,15 @@ def main():
     if args.rollback:
         print(json.dumps(rollback_bench(ns, prog, program, stream)), flush=True)
         return
+    if args.sweep_only:
+        print(json.dumps(sweep_bench(ns, prog, stream)), flush=True)
+        return
     ex = {"grid": ns.EXEC_GRID, "block": ns.EXEC_BLOCK, "cluster": ns.EXEC_CLUSTER,
           "auto": ns.EXEC_AUTO}[args.exec]
     ld = prog.load_program(program, ns.make_options(exec=ex))
     h = ld.handle
     keys = ("events", "solves", "rounds", "flows_swept", "incidences_swept", "active_swept",
-            "pending_swept", "reselected", "wide_solves")
+            "pending_swept", "reselected", "wide_solves", "links_swept")
     tot = {k: 0 for k in keys}
     tot["device_seconds"] = 0.0
     phases = [0.0] * 8
@@ -207,7 +311,8 @@ def main():
     dev = tot["device_seconds"]
     solves_per_s = tot["solves"] / dev
     events_per_s = tot["events"] / dev
-    abytes = algorithmic_bytes(tot)
+    # every re-solved flow is frozen once in its solve
+    abytes = algorithmic_bytes(tot, tot["reselected"])
     achieved = abytes / dev / 1e9
     kernel = {ns.EXEC_GRID: "netsim_grid_kernel", ns.EXEC_BLOCK: "netsim_block_kernel",
               ns.EXEC_CLUSTER: "netsim_cluster_kernel"}[layout]
@@ -245,10 +350,23 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic, "kernel": kernel,
                      "algorithmic_bytes_per_launch": abytes / args.steps,
-                     "launch_seconds": dev / args.steps},
+                     "launch_seconds": dev / args.steps,
+                     "links_swept_per_launch": tot["links_swept"] / args.steps},
     }
+    if not args.no_sweep:
+        sw = sweep_bench(ns, prog, stream)
+        fz, ct = sw["freeze_sweep"], sw["link_count"]
+        ab = fz["algorithmic_bytes"] + ct["algorithmic_bytes"]
+        ks = fz["kernel_s"] + ct["kernel_s"]
+        line["roofline_sweep"] = {"bound": "hbm", "achieved": ab / ks / 1e9, "peak": HBM_PEAK_GBPS,
+                                  "unit": "GB/s", "frac": ab / ks / 1e9 / HBM_PEAK_GBPS,
+                                  "kernel": "exact_count_kernel + exact_freeze_kernel",
+                                  "traffic": None, "detail": sw}
+        print(f"sweeps: freeze {fz['kernel_s'] * 1e6:.1f} us ({fz['achieved']:.0f} GB/s), count "
+              f"{ct['kernel_s'] * 1e6:.1f} us ({ct['achieved']:.0f} GB/s), full solve "
+              f"{sw['full_solve']['device_s']:.3f} s", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline and int(os.environ.get("RANK", "0")) == 0:
-        line["cpu_baseline"] = cpu_baseline()
+        line["cpu_baseline"] = cpu_baseline(tot["events"] // args.steps)
     print(json.dumps(line), flush=True)
 
 

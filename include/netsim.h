@@ -494,12 +494,16 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active,
  * flush_bytes (0: none) of a scratch buffer to evict the caches, then times
  * the count kernel into count_ms[r], writes the buffer again, runs the
  * level's link pass and times the freezing sweep into freeze_ms[r] (HIP
- * events on hip_stream).  Allocates the scratch buffer for the call.
+ * events on hip_stream, so dispatch is included).  count_kernel_ms and
+ * freeze_kernel_ms (may be NULL) receive the same sweeps timed inside the
+ * kernels: from the first workgroup's start to the last one's end on the
+ * device's constant wall clock.  Allocates the scratch buffers for the call.
  * Leaves no simulation position: the next netsim_advance starts from t = 0.
  */
 netsim_status netsim_bench_sweeps(netsim_t* h, int32_t scen, int64_t n_active,
                                   const int64_t* active_ids, int32_t reps, int64_t flush_bytes,
-                                  void* hip_stream, double* count_ms, double* freeze_ms);
+                                  void* hip_stream, double* count_ms, double* freeze_ms,
+                                  double* count_kernel_ms, double* freeze_kernel_ms);
 
 /*
  * Allocation-free rate solve, for callers that cannot allocate device memory

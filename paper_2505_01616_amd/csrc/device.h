@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace netsim_dev {
@@ -72,15 +73,28 @@ enum : int32_t {
 };
 
 // Counters of a wide exact solve run by the sweep kernels (sweep.hip), in
-// device memory: level minima (bit patterns of doubles, by level parity),
-// unfrozen and live list sizes (by parity), statistics.
-struct XGrid {
-  unsigned long long gmin[2];
-  int32_t cu[2];           // unfrozen flows entering the level of that parity
-  int32_t cl[2];           // live links entering the level of that parity
+// device memory.  The unfrozen-flow and live-link lists are kept in
+// per-workgroup segments: workgroup b of a sweep owns entries
+// [b * seg, (b + 1) * seg) of its list and its count, so a sweep compacts
+// with shared-memory counters only.  Per-workgroup results (minima, counts,
+// statistics) go to arrays that the next kernel (or the host) reduces: no
+// two workgroups update one word, since atomics on one address serialise in
+// the L2.  Header first (the host reads it).
+constexpr int XG_MAX_BLOCKS = 8192;
+struct XGridHead {
   int32_t fault;           // 1: a non-positive or infinite level minimum
   int32_t done;            // 1 once a level started with no unfrozen flow
-  unsigned long long levels, fsw, isw, lsw;  // iterations; flows, incidences, links swept
+  int32_t ublocks, useg;   // freezing sweep: workgroups, entries per segment
+  int32_t lblocks, lseg;   // link pass: workgroups, entries per segment
+  unsigned long long levels, fsw;  // iterations; flows swept
+  double sstar[2];         // level minimum, by parity (bottleneck pass -> freezing sweep)
+};
+struct XGrid : XGridHead {
+  int32_t ucnt[2][XG_MAX_BLOCKS];  // unfrozen flows per segment, by level parity
+  int32_t lcnt[2][XG_MAX_BLOCKS];  // live links per segment, by level parity
+  double bmin[2][XG_MAX_BLOCKS];   // per-workgroup minimum share of the link pass, by parity
+  unsigned long long isw[XG_MAX_BLOCKS];  // incidences swept, per freezing-sweep workgroup
+  unsigned long long lsw[XG_MAX_BLOCKS];  // links whose share was computed, per link-pass workgroup
 };
 
 struct Params {
@@ -143,11 +157,14 @@ struct Params {
   int32_t* xk;             // [L] flows frozen at the current level
   int32_t* xlive0; int32_t* xlive1;  // [L] links with unfrozen flows (per part on [l0, l1))
   // link-major incidence (exact mode): the flows of device link l are
-  // lfid[lfoff[l] .. lfoff[l+1]-1] (ascending), lflink[e] the link of entry e
+  // lfid[lfoff[l] .. lfoff[l+1]-1] (ascending); lfchunk[c] is the link of
+  // entry 256 c (the last link with lfoff[l] <= 256 c)
   const int32_t* lfoff;    // [L+1]
   const int32_t* lfid;     // [nnz]
-  const int32_t* lflink;   // [nnz]
-  uint8_t* xact;           // [F] 1 while a flow of a wide exact solve is unfrozen
+  const int32_t* lfchunk;  // [nnz/256 + 1]
+  const uint64_t* lfhead;  // [(nnz + 256)/64 + 1] bit e: entry e starts a link (or e >= nnz)
+  uint32_t* xmask;         // [F/32 + 1] bit f: flow f is active in the wide exact solve
+  uint8_t* xfz;            // [L] 1: the link is a bottleneck of the current level
   XGrid* xgrid;            // counters of a wide exact solve
   int32_t exact_lds_bytes; // dynamic shared memory of the exact kernel (link state
                            // of a part with at most exact_lds_bytes / 24 links)
@@ -174,13 +191,21 @@ hipError_t launch_exact(const Params& p, int blocks, int threads, hipStream_t s)
 // Bytes of exact-mode link state per link.
 int exact_link_bytes();
 // A wide exact solve of part C's n flows listed in act0 + C.f0, on the whole
-// GPU (sweep.hip): begin (clear link state, flag the flows), count (per-link
+// GPU (sweep.hip): begin (clear link state, mark the flows), count (per-link
 // unfrozen counts over the part's link-major incidences [e0, e1)), then per
-// level j = 0, 1, ... links and freeze, until xgrid->cu[j & 1] is 0.
+// level j = 0, 1, ... links and freeze, until xgrid->done or
+// xgrid->cu[j & 1] is 0.
 hipError_t grid_solve_begin(const Params& P, const ScenCtl& C, int n, hipStream_t s);
-hipError_t grid_solve_count(const Params& P, int e0, int e1, hipStream_t s);
+hipError_t grid_solve_count(const Params& P, const ScenCtl& C, int e0, int e1, hipStream_t s,
+                            unsigned long long* stamps = nullptr);
 hipError_t grid_solve_links(const Params& P, const ScenCtl& C, int j, hipStream_t s);
-hipError_t grid_solve_freeze(const Params& P, const ScenCtl& C, int n, int j, hipStream_t s);
+hipError_t grid_solve_freeze(const Params& P, const ScenCtl& C, int n, int j, hipStream_t s,
+                             unsigned long long* stamps = nullptr);
+// Workgroups of the count and freezing sweeps.  With `stamps` (device,
+// 2 x workgroups words) each workgroup's first thread writes the wall clock
+// (100 MHz) at its start and end: the sweep's duration inside the kernel.
+int count_blocks(int e0, int e1);
+int freeze_blocks(int n);
 // Streaming write of `bytes` (a multiple of 16) over buf.
 hipError_t launch_flush(void* buf, size_t bytes, uint32_t tag, hipStream_t s);
 

@@ -475,21 +475,35 @@ netsim_status prepare(netsim_t* h) {
   // link-major incidence (exact mode's wide solves): flows of each device
   // link in ascending device order, and each entry's link
   const bool exact = h->opt.exact != 0;
-  std::vector<int32_t> lfoff, lfid, lflink;
+  std::vector<int32_t> lfoff, lfid, lfchunk;
+  std::vector<uint64_t> lfhead;
   if (exact) {
     lfoff.assign((size_t)ld + 1, 0);
     for (int64_t k = 0; k < h->nnz; ++k) lfoff[(size_t)plink[(size_t)k] + 1] += 1;
     for (int64_t l = 0; l < ld; ++l) lfoff[(size_t)l + 1] += lfoff[(size_t)l];
     lfid.assign((size_t)std::max<int64_t>(h->nnz, 1), 0);
-    lflink.assign((size_t)std::max<int64_t>(h->nnz, 1), 0);
     std::vector<int32_t> fill(lfoff.begin(), lfoff.end() - 1);
     for (int64_t d = 0; d < F; ++d)
       for (int32_t k = poff[(size_t)d]; k < poff[(size_t)d + 1]; ++k) {
         const int32_t l = plink[(size_t)k];
-        const int32_t at = fill[(size_t)l]++;
-        lfid[(size_t)at] = (int32_t)d;
-        lflink[(size_t)at] = l;
+        lfid[(size_t)fill[(size_t)l]++] = (int32_t)d;
       }
+    // the link of every 256th entry: the last link whose entries start at or
+    // before it (links without entries skipped)
+    lfchunk.assign((size_t)(h->nnz / 256 + 1), 0);
+    int32_t l = 0;
+    for (size_t c = 0; c < lfchunk.size(); ++c) {
+      const int64_t e = (int64_t)c * 256;
+      while (l + 1 < ld && lfoff[(size_t)l + 1] <= e) ++l;
+      lfchunk[c] = l;
+    }
+    // one bit per entry: set where a link's entries start, and past the end
+    lfhead.assign((size_t)((h->nnz + 256) / 64 + 1), ~0ull);
+    for (int64_t e = 0; e < h->nnz; ++e) lfhead[(size_t)(e >> 6)] &= ~(1ull << (e & 63));
+    for (int64_t k = 0; k < ld; ++k) {
+      const int64_t e = lfoff[(size_t)k];
+      if (e < h->nnz) lfhead[(size_t)(e >> 6)] |= 1ull << (e & 63);
+    }
   }
   h->h_lfoff = lfoff;
   // initial dynamic state
@@ -568,8 +582,10 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.xlive1, sizeof(int32_t) * XL},
       {(void**)&P.lfoff, sizeof(int32_t) * (XL + 1)},
       {(void**)&P.lfid, sizeof(int32_t) * (exact ? lfid.size() : 1)},
-      {(void**)&P.lflink, sizeof(int32_t) * (exact ? lflink.size() : 1)},
-      {(void**)&P.xact, exact ? Fz : 1},
+      {(void**)&P.lfchunk, sizeof(int32_t) * (exact ? lfchunk.size() : 1)},
+      {(void**)&P.lfhead, sizeof(uint64_t) * (exact ? lfhead.size() : 1)},
+      {(void**)&P.xmask, sizeof(uint32_t) * (exact ? Fz / 32 + 8 : 1)},  // +8: 16-byte reads past the end
+      {(void**)&P.xfz, XL},
       {(void**)&P.xgrid, sizeof(netsim_dev::XGrid)},
   };
   size_t total = 0;
@@ -603,7 +619,8 @@ netsim_status prepare(netsim_t* h) {
       {capf.data(), P.capf, h->opt.exact ? sizeof(double) * capf.size() : 0},
       {lfoff.data(), P.lfoff, sizeof(int32_t) * lfoff.size()},
       {lfid.data(), P.lfid, sizeof(int32_t) * lfid.size()},
-      {lflink.data(), P.lflink, sizeof(int32_t) * lflink.size()},
+      {lfchunk.data(), P.lfchunk, sizeof(int32_t) * lfchunk.size()},
+      {lfhead.data(), P.lfhead, sizeof(uint64_t) * lfhead.size()},
   };
   for (const Up& u : ups) {
     if (u.bytes == 0) continue;
@@ -879,31 +896,72 @@ netsim_status simulate(netsim_t* h, hipStream_t st, bool resume, int64_t max_eve
 // A wide exact solve of the n flows of part p listed in its act0 slice, on
 // the whole GPU (sweep.hip).  Levels are enqueued in batches; the host reads
 // the unfrozen count after each batch.  Adds the solve's statistics to *out.
-netsim_status grid_solve(netsim_t* h, hipStream_t st, int32_t p, int32_t n, netsim_dev::XGrid* out) {
+struct GridStats {
+  unsigned long long levels = 0, fsw = 0, isw = 0, lsw = 0;
+};
+
+netsim_status grid_solve(netsim_t* h, hipStream_t st, int32_t p, int32_t n, GridStats* out) {
   const Params& P = h->prm;
   const ScenCtl& C = h->h_ctl0[(size_t)p];
   hipError_t he = netsim_dev::grid_solve_begin(P, C, n, st);
   if (he == hipSuccess)
-    he = netsim_dev::grid_solve_count(P, h->h_lfoff[(size_t)C.l0], h->h_lfoff[(size_t)C.l1], st);
+    he = netsim_dev::grid_solve_count(P, C, h->h_lfoff[(size_t)C.l0], h->h_lfoff[(size_t)C.l1], st);
   const int64_t limit = h->opt.max_rounds > 0 ? h->opt.max_rounds : (int64_t)n + 1;
-  netsim_dev::XGrid g{};
-  for (int j = 0; he == hipSuccess;) {
-    for (int b = 0; b < kGridLevelBatch && he == hipSuccess; ++b, ++j) {
-      he = netsim_dev::grid_solve_links(P, C, j, st);
-      if (he == hipSuccess) he = netsim_dev::grid_solve_freeze(P, C, n, j, st);
+  netsim_dev::XGridHead g{};  // the counters the host reads
+  // levels 0 and 1 directly; then batches of kGridLevelBatch levels replayed
+  // from one captured graph (the kernels use only the parity of the level
+  // and whether it is the first, so the batch captured as levels 2, 3, ...
+  // serves for every later batch)
+  hipGraphExec_t batch = nullptr;
+  for (int j = 0; j < 2 && he == hipSuccess; ++j) {
+    he = netsim_dev::grid_solve_links(P, C, j, st);
+    if (he == hipSuccess) he = netsim_dev::grid_solve_freeze(P, C, n, j, st);
+  }
+  if (he == hipSuccess) {
+    hipStream_t cs = nullptr;
+    hipGraph_t graph = nullptr;
+    he = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+    if (he == hipSuccess) he = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+    if (he == hipSuccess) {
+      for (int b = 0; b < kGridLevelBatch && he == hipSuccess; ++b) {
+        he = netsim_dev::grid_solve_links(P, C, 2 + b, cs);
+        if (he == hipSuccess) he = netsim_dev::grid_solve_freeze(P, C, n, 2 + b, cs);
+      }
+      const hipError_t he2 = hipStreamEndCapture(cs, &graph);
+      if (he == hipSuccess) he = he2;
     }
+    if (he == hipSuccess) he = hipGraphInstantiate(&batch, graph, nullptr, nullptr, 0);
+    if (graph) (void)hipGraphDestroy(graph);
+    if (cs) (void)hipStreamDestroy(cs);
+  }
+  for (int rep = 0; he == hipSuccess; ++rep) {
+    if (rep > 0) he = hipGraphLaunch(batch, st);
     if (he == hipSuccess) he = hipMemcpyAsync(&g, P.xgrid, sizeof g, hipMemcpyDeviceToHost, st);
     if (he == hipSuccess) he = hipStreamSynchronize(st);
     if (he != hipSuccess) break;
-    if (g.fault) return fail(h, NETSIM_E_DEVICE, "device solver fault: non-positive fair share");
-    if (g.done || g.cu[j & 1] == 0) break;
-    if ((int64_t)g.levels > limit) return fail(h, NETSIM_E_LIMIT, "device solver fault: round watchdog fired");
+    if (g.fault) {
+      (void)hipGraphExecDestroy(batch);
+      return fail(h, NETSIM_E_DEVICE, "device solver fault: non-positive fair share");
+    }
+    if (g.done) break;
+    if ((int64_t)g.levels > limit) {
+      (void)hipGraphExecDestroy(batch);
+      return fail(h, NETSIM_E_LIMIT, "device solver fault: round watchdog fired");
+    }
   }
+  if (batch) (void)hipGraphExecDestroy(batch);
   if (he != hipSuccess) return hip_fail(h, he, "wide exact solve");
+  // per-workgroup statistics
+  std::vector<unsigned long long> isw((size_t)g.ublocks), lsw((size_t)g.lblocks);
+  const netsim_dev::XGrid* dg = P.xgrid;
+  he = hipMemcpy(isw.data(), dg->isw, sizeof(unsigned long long) * isw.size(), hipMemcpyDeviceToHost);
+  if (he == hipSuccess)
+    he = hipMemcpy(lsw.data(), dg->lsw, sizeof(unsigned long long) * lsw.size(), hipMemcpyDeviceToHost);
+  if (he != hipSuccess) return hip_fail(h, he, "wide exact solve statistics");
   out->levels += g.levels;
   out->fsw += g.fsw;
-  out->isw += g.isw;
-  out->lsw += g.lsw;
+  for (unsigned long long v : isw) out->isw += v;
+  for (unsigned long long v : lsw) out->lsw += v;
   return NETSIM_OK;
 }
 
@@ -1829,7 +1887,7 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, con
   std::vector<ScenCtl> out;
   rc = collect(h, &out);
   if (rc) return rc;
-  netsim_dev::XGrid gs{};
+  GridStats gs;
   if (!wide.empty()) {
     hipEvent_t e0, e1;
     he = hipEventCreate(&e0);
@@ -1883,7 +1941,7 @@ netsim_status netsim_solve_once(netsim_t* h, int32_t scen, int64_t n_active, con
 
 netsim_status netsim_bench_sweeps(netsim_t* h, int32_t scen, int64_t n_active, const int64_t* active_ids,
                                   int32_t reps, int64_t flush_bytes, void* hip_stream, double* count_ms,
-                                  double* freeze_ms) {
+                                  double* freeze_ms, double* count_kernel_ms, double* freeze_kernel_ms) {
   if (!h) return fail(nullptr, NETSIM_E_INVALID, "bench_sweeps: handle is NULL");
   if (!h->opt.exact) return fail(h, NETSIM_E_STATE, "bench_sweeps: needs a handle in exact mode");
   if (scen < 0 || scen >= (int32_t)h->scen.size()) return fail(h, NETSIM_E_INVALID, "bench_sweeps: bad scenario");
@@ -1925,23 +1983,43 @@ netsim_status netsim_bench_sweeps(netsim_t* h, int32_t scen, int64_t n_active, c
     (void)hipGetLastError();
     return fail(h, NETSIM_E_NOMEM, "bench_sweeps: no memory for the flush buffer");
   }
+  // per-workgroup wall-clock stamps of the two sweeps
+  const int e0 = h->h_lfoff[(size_t)C.l0], e1 = h->h_lfoff[(size_t)C.l1];
+  const int cb = netsim_dev::count_blocks(e0, e1), fbk = netsim_dev::freeze_blocks((int)n_active);
+  unsigned long long* stamps = nullptr;
+  if (hipMalloc(&stamps, sizeof(unsigned long long) * 2 * (size_t)(cb + fbk)) != hipSuccess) {
+    (void)hipGetLastError();
+    if (buf) (void)hipFree(buf);
+    return fail(h, NETSIM_E_NOMEM, "bench_sweeps: no memory for the time stamps");
+  }
+  std::vector<unsigned long long> hs((size_t)2 * (cb + fbk));
+  int khz = 0;
+  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->opt.device) != hipSuccess || khz <= 0)
+    khz = 100000;
+  auto span_ms = [&](const unsigned long long* a, int blocks) {
+    unsigned long long lo = ~0ull, hi = 0;
+    for (int b = 0; b < blocks; ++b) {
+      lo = std::min(lo, a[2 * b]);
+      hi = std::max(hi, a[2 * b + 1]);
+    }
+    return hi > lo ? (double)(hi - lo) / (double)khz : 0.0;
+  };
   hipEvent_t ev[4] = {};
   for (auto& e : ev)
     if (he == hipSuccess) he = hipEventCreate(&e);
   const int n = (int)n_active;
-  const int e0 = h->h_lfoff[(size_t)C.l0], e1 = h->h_lfoff[(size_t)C.l1];
   for (int32_t r = 0; r < reps && he == hipSuccess; ++r) {
     // cold caches before each sweep: a streaming write larger than the L2s
     // and the Infinity Cache together
     if (fb > 0) he = netsim_dev::launch_flush(buf, fb, (uint32_t)(2 * r), st);
     if (he == hipSuccess) he = netsim_dev::grid_solve_begin(P, C, n, st);
     if (he == hipSuccess) he = hipEventRecord(ev[0], st);
-    if (he == hipSuccess) he = netsim_dev::grid_solve_count(P, e0, e1, st);
+    if (he == hipSuccess) he = netsim_dev::grid_solve_count(P, C, e0, e1, st, stamps);
     if (he == hipSuccess) he = hipEventRecord(ev[1], st);
     if (he == hipSuccess && fb > 0) he = netsim_dev::launch_flush(buf, fb, (uint32_t)(2 * r + 1), st);
     if (he == hipSuccess) he = netsim_dev::grid_solve_links(P, C, 0, st);
     if (he == hipSuccess) he = hipEventRecord(ev[2], st);
-    if (he == hipSuccess) he = netsim_dev::grid_solve_freeze(P, C, n, 0, st);
+    if (he == hipSuccess) he = netsim_dev::grid_solve_freeze(P, C, n, 0, st, stamps + 2 * cb);
     if (he == hipSuccess) he = hipEventRecord(ev[3], st);
     if (he == hipSuccess) he = hipEventSynchronize(ev[3]);
     float a = 0.0f, b = 0.0f;
@@ -1949,10 +2027,17 @@ netsim_status netsim_bench_sweeps(netsim_t* h, int32_t scen, int64_t n_active, c
     if (he == hipSuccess) he = hipEventElapsedTime(&b, ev[2], ev[3]);
     count_ms[r] = a;
     freeze_ms[r] = b;
+    if (he == hipSuccess)
+      he = hipMemcpy(hs.data(), stamps, sizeof(unsigned long long) * hs.size(), hipMemcpyDeviceToHost);
+    if (he == hipSuccess) {
+      if (count_kernel_ms) count_kernel_ms[r] = span_ms(hs.data(), cb);
+      if (freeze_kernel_ms) freeze_kernel_ms[r] = span_ms(hs.data() + 2 * cb, fbk);
+    }
   }
   for (auto& e : ev)
     if (e) (void)hipEventDestroy(e);
   if (buf) (void)hipFree(buf);
+  (void)hipFree(stamps);
   if (he != hipSuccess) return hip_fail(h, he, "bench_sweeps");
   h->has_state = false;  // the device holds no simulation position now
   return NETSIM_OK;

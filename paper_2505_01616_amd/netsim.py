@@ -120,7 +120,7 @@ _SIGS = {
     "netsim_gc": (_I32, [_H, _D]),
     "netsim_num_checkpoints": (_I32, [_H, ctypes.POINTER(_I64)]),
     "netsim_solve_rates_noalloc": (_I32, [_I32, _I32, _P, _I32, _P, _P, _P, _P, _P]),
-    "netsim_bench_sweeps": (_I32, [_H, _I32, _I64, _P, _I32, _I64, _P, _P, _P]),
+    "netsim_bench_sweeps": (_I32, [_H, _I32, _I64, _P, _I32, _I64, _P, _P, _P, _P, _P]),
     "netsim_last_error": (ctypes.c_char_p, [_H]),
     "netsim_destroy": (None, [_H]),
 }
@@ -434,13 +434,14 @@ def netsim_num_checkpoints(h) -> int:
 
 
 def netsim_bench_sweeps(h, scen, active_ids, reps, flush_bytes, stream=None):
-    """Per-repetition device times (ms) of the count and freezing sweeps."""
+    """Per-repetition times (ms) of the count and freezing sweeps: with HIP
+    events (dispatch included) and inside the kernels."""
     ids = _arr(active_ids, np.int64)
-    a = np.zeros(int(reps))
-    b = np.zeros(int(reps))
+    a, b, c, d = (np.zeros(int(reps)) for _ in range(4))
     _check(h, load_library().netsim_bench_sweeps(h, scen, len(ids), _ptr(ids), int(reps),
-                                                 int(flush_bytes), _stream(stream), _ptr(a), _ptr(b)))
-    return a, b
+                                                 int(flush_bytes), _stream(stream), _ptr(a), _ptr(b),
+                                                 _ptr(c), _ptr(d)))
+    return {"count_ms": a, "freeze_ms": b, "count_kernel_ms": c, "freeze_kernel_ms": d}
 
 
 def netsim_solve_rates_noalloc(device, num_links, d_cap, num_flows, d_path_off, d_path_link,

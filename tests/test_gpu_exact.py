@@ -348,8 +348,10 @@ def test_bench_sweeps_runs_and_leaves_no_position():
     act = np.nonzero(fs.nbytes > 0)[0]
     ld = pr.load_program(program, ns.make_options(exact=1))
     try:
-        a, b = ns.netsim_bench_sweeps(ld.handle, 0, act, 3, 64 << 20)
-        assert np.all(a > 0) and np.all(b > 0)
+        t = ns.netsim_bench_sweeps(ld.handle, 0, act, 3, 64 << 20)
+        for k in ("count_ms", "freeze_ms", "count_kernel_ms", "freeze_kernel_ms"):
+            assert np.all(t[k] > 0), k
+        assert np.all(t["freeze_kernel_ms"] <= t["freeze_ms"] * 1.5)
         rates = ns.netsim_solve_once(ld.handle, 0, act)
     finally:
         ld.close()
