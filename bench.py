@@ -185,6 +185,22 @@ def traffic_from_profile(kernel: str, steps: int):
     return prof["traffic_bytes_per_launch"]
 
 
+def sweep_traffic_from_profile():
+    """HBM bytes of the count and freezing sweeps (cold repetitions) from the
+    committed rocprofv3 counter summary, if taken on the current sweep.hip."""
+    import hashlib
+    try:
+        with open(os.path.join(ROOT, "profiles", "exact_sweeps_c4_traffic.json")) as fh:
+            prof = json.load(fh)
+        with open(os.path.join(ROOT, "paper_2505_01616_amd", "csrc", "sweep.hip"), "rb") as fh:
+            sha = hashlib.sha256(fh.read()).hexdigest()[:16]
+    except OSError:
+        return None
+    if prof.get("sweep_hip_sha256_16") != sha:
+        return None
+    return prof["freeze_traffic_bytes"] + prof["count_traffic_bytes"]
+
+
 def rollback_bench(ns, prog, program, stream, pieces=10):
     """Time rollback on C4: the complete simulation as one launch; the same
     simulation advanced in `pieces` checkpointed launches (on a second
@@ -361,7 +377,7 @@ def main():
         line["roofline_sweep"] = {"bound": "hbm", "achieved": ab / ks / 1e9, "peak": HBM_PEAK_GBPS,
                                   "unit": "GB/s", "frac": ab / ks / 1e9 / HBM_PEAK_GBPS,
                                   "kernel": "exact_count_kernel + exact_freeze_kernel",
-                                  "traffic": None, "detail": sw}
+                                  "traffic": sweep_traffic_from_profile(), "detail": sw}
         print(f"sweeps: freeze {fz['kernel_s'] * 1e6:.1f} us ({fz['achieved']:.0f} GB/s), count "
               f"{ct['kernel_s'] * 1e6:.1f} us ({ct['achieved']:.0f} GB/s), full solve "
               f"{sw['full_solve']['device_s']:.3f} s", file=sys.stderr, flush=True)
