@@ -23,9 +23,14 @@ _I64 = ctypes.c_int64
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
-            build()
-        lib = ctypes.CDLL(LIB)
+        # NETSIM_ORACLE_LIB: another build of netsim_oracle.c (the sanitizer
+        # build of tests/test_native_checks.py)
+        path = os.environ.get("NETSIM_ORACLE_LIB")
+        if not path:
+            path = LIB
+            if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+                build()
+        lib = ctypes.CDLL(path)
         lib.oracle_run.restype = ctypes.c_int
         lib.oracle_run.argtypes = [_I64, _P, _I64, _P, _P, _P, _P, _P, _P, _P, _I64,
                                    ctypes.c_double, _I64, _P, _P, _P, _P]

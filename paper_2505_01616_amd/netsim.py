@@ -18,7 +18,9 @@ from typing import Optional
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libnetsim.so")
+# NETSIM_LIB: another build of the library (the sanitizer build of the host
+# code made by tests/test_native_checks.py)
+LIB_PATH = os.environ.get("NETSIM_LIB") or os.path.join(HERE, "libnetsim.so")
 
 OK, E_INVALID, E_NOMEM, E_DEVICE, E_STATE, E_LIMIT = 0, -1, -2, -3, -4, -5
 TOPO_LEAF_SPINE, TOPO_RAIL, TOPO_FAT_TREE = 1, 2, 3
