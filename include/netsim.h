@@ -104,7 +104,11 @@ typedef struct {
                                 barrier give up at once (the run then fails with
                                 NETSIM_E_DEVICE, "grid barrier timed out"); bit
                                 4 keeps exact-mode link state in global memory
-                                even where it fits shared memory                 */
+                                even where it fits shared memory; bit 5 runs
+                                every exact-mode solve_once on the whole GPU;
+                                bit 6 makes every release of NETSIM_EXEC_CLUSTER
+                                an agent-scope release fence (slower; results
+                                are the same bit for bit)                       */
   int32_t single_clock;      /* 1: one part (one clock) per scenario             */
   int32_t assist_min_flows;  /* NETSIM_EXEC_CLUSTER: smallest re-solve handed to the
                                 helper workgroups; 0 = 4096                      */

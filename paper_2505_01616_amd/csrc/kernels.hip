@@ -309,6 +309,16 @@ __device__ __forceinline__ bool wait_ne(uint32_t* bar, uint32_t* p, uint32_t v, 
 // covers them.
 __device__ __forceinline__ void drain() { __builtin_amdgcn_s_waitcnt(0); }
 
+// The release before a signal to other workgroups of the same XCD: by
+// default each wave drains its memory operations (enough there, see
+// ClusterG); with options.debug bit 6 an agent-scope release fence, the
+// memory model's own form (it also writes the L2 back, for other XCDs).
+constexpr int DEBUG_FORMAL_RELEASE = 64;
+__device__ __forceinline__ void xcd_release(bool formal) {
+  if (formal) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  else drain();
+}
+
 // The helper workgroups of one XCD (all but its leader), solving one job at a
 // time with a barrier of their own.
 //
@@ -338,6 +348,7 @@ struct ClusterG {
   int rank, nh;   // rank among the helpers, number of helpers
   bool ab;
   uint64_t patience;  // barrier time-out (ticks)
+  bool formal;        // agent-scope release fences instead of drains (debug)
   __device__ Lists* lists(ScenCtl* C) const { return &C->k; }
   __device__ int tid() const { return rank * blockDim.x + threadIdx.x; }
   __device__ int block_base() const { return rank * blockDim.x; }
@@ -346,7 +357,7 @@ struct ClusterG {
   __device__ int nthr() const { return nh * blockDim.x; }
   __device__ bool aborted() const { return ab; }
   __device__ __forceinline__ void sync() {
-    drain();
+    xcd_release(formal);
     __syncthreads();
     if (threadIdx.x == 0) {
       // the arrival and a look at the abort word travel together; an abort
@@ -1414,7 +1425,7 @@ struct Assist {
                            __HIP_MEMORY_SCOPE_AGENT);
       }
     }
-    drain();
+    xcd_release(P.debug & DEBUG_FORMAL_RELEASE);
     __syncthreads();
     if (threadIdx.x == 0) {
       int res = NOT_TAKEN, posted = 0;
@@ -1568,7 +1579,7 @@ __device__ __forceinline__ void helper_loop(const Params& P, ClusterG& cg, Solve
       __hip_atomic_store(reinterpret_cast<uint64_t*>(cw + CL_FSW), (uint64_t)ff, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     }
-    drain();
+    xcd_release(P.debug & DEBUG_FORMAL_RELEASE);
     __syncthreads();
     if (threadIdx.x == 0)  // drained above: rates and statistics are in the XCD's L2
       __hip_atomic_fetch_add(&cw[CL_DONE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -2283,7 +2294,8 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
   if (rank != 0) {  // workgroups beyond the helpers have nothing to do
     if (nh > 0 && rank <= nh) {
       const uint64_t patience = (P.debug & DEBUG_HELPER_BARRIER_GIVES_UP) ? 0 : BARRIER_TIMEOUT_TICKS;
-      ClusterG cg{lds, ldsi, &flag, P.bar, cw, 0u, rank - 1, nh, false, patience};
+      ClusterG cg{lds, ldsi, &flag, P.bar, cw, 0u, rank - 1, nh, false, patience,
+                  (P.debug & DEBUG_FORMAL_RELEASE) != 0};
       helper_loop(P, cg, *reinterpret_cast<SolveLds*>(pool), &tally, box, tjob);
     }
     return;

@@ -281,3 +281,29 @@ def test_complete_alltoall_cluster_equals_block_and_is_causal():
     lower = base + fs.start + np.where(wp, fs.nbytes / mincap, 0.0)
     assert np.all(fin >= lower * (1 - 1e-12))
     _say("  block s", sa["device_seconds"], "cluster s", sb["device_seconds"])
+
+
+@pytest.mark.parametrize("case", ["c2-every-resolve", "global-link-state", "c4-complete"])
+def test_formal_release_is_bit_identical(case):
+    """Debug bit 6 makes every release of the cluster layout (the helpers'
+    barrier, the leader's hand-over, a helper's end of job) an agent-scope
+    release fence, the memory model's own form, instead of a drain of the
+    wave's memory operations: the results and statistics are the same bit
+    for bit."""
+    ns, pr = _gpu()
+    _say(f"test_formal_release_is_bit_identical {case}")
+    if case == "c2-every-resolve":
+        program, kw = configs.c2(2, tp_reps=6), dict(assist_min_flows=1)
+    elif case == "global-link-state":
+        program, kw = configs.c4(4, blocks=2, locals_=2, phases=2), dict(assist_min_flows=1024,
+                                                                          single_clock=1)
+    else:
+        program, kw = configs.c4(4), {}
+    a, sa = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, **kw))
+    b, sb = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, debug=64, **kw))
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y, equal_nan=True)
+    for k in SAME + ("assisted_solves",):
+        assert sa[k] == sb[k], k
+    assert sb["assisted_solves"] > 0
+    _say("  drain s", sa["device_seconds"], "formal release s", sb["device_seconds"])
