@@ -228,11 +228,14 @@ typedef struct {
                                 which have no such pass, add nothing)            */
 } netsim_stats;
 
-/* Fills *opt with the defaults (device 0, auto layout, no limits). */
+/* Fills *opt with the defaults (device 0, auto layout, no limits, default solver). */
 void netsim_default_options(netsim_options* opt);
 
 /*
- * Explicit topology: num_scenarios independent scenarios; scenario s owns
+ * Explicit topology (Section 4.1: netsim is configured with the cluster
+ * topology -- its links and their bandwidths; here directed links with their
+ * capacities in bytes per second).  Several independent scenarios per handle
+ * are the batched what-if mode: num_scenarios independent scenarios; scenario s owns
  * links link_off[s] .. link_off[s+1]-1 of capacity_Bps (link_off has S+1
  * entries, link_off[0] = 0, non-decreasing).  Capacities must be finite and
  * > 0.  opt may be NULL (defaults).  Flows must then carry explicit paths.
@@ -241,16 +244,21 @@ void netsim_default_options(netsim_options* opt);
 netsim_status netsim_create(netsim_t** out, int32_t num_scenarios, const int64_t* link_off,
                             const double* capacity_Bps, const netsim_options* opt);
 
-/* Built-in fabrics, one per scenario (topos[num_scenarios]). */
+/* Built-in fabrics, one per scenario (topos[num_scenarios]): the topology
+ * configuration of Section 4.1, with its multipath routing (ECMP) rule. */
 netsim_status netsim_create_topology(netsim_t** out, int32_t num_scenarios,
                                      const netsim_topology* topos, const netsim_options* opt);
 
-/* Number of links of scenario scen, and their capacities (cap_out[L_s], may be NULL). */
+/* Number of links of scenario scen, and their capacities (cap_out[L_s], may be
+ * NULL): the links a built-in fabric created (Section 4.1 topology). */
 netsim_status netsim_get_links(const netsim_t* h, int32_t scen, int64_t* num_links,
                                double* cap_out);
 
 /*
- * Appends n flows to scenario scen.  Flow i: endpoints src[i] -> dst[i]
+ * Appends n flows to scenario scen (Section 4.1: the communication the
+ * simulator intercepts becomes flows between GPUs over the topology;
+ * Section 4.1's event queue releases an operation only after the ones it
+ * depends on, here dependencies between flows).  Flow i: endpoints src[i] -> dst[i]
  * (GPU ranks; may be NULL when paths are given), nbytes[i] >= 0, start[i] >= 0.
  * Path: if path_off is NULL the built-in router chooses it from (src, dst);
  * otherwise flow i crosses links path_link[path_off[i] .. path_off[i+1]-1]
@@ -330,6 +338,20 @@ netsim_status netsim_add_hier_allreduce(netsim_t* h, int32_t scen, int32_t m, in
                                         int64_t* count);
 
 /*
+ * The exit flows of the operation appended by the last successful call of
+ * netsim_add_ring, netsim_add_all_to_all, netsim_add_tree_allreduce,
+ * netsim_add_hier_allreduce or netsim_add_flows on h: the flows a later
+ * operation that depends on it waits for (Section 4.1: a collective is
+ * complete on a rank when its pattern's last transfers are; taken as a
+ * chained ring's last step, every flow of a flat or aggregated ring, of an
+ * all-to-all and of a batch of flows, a double binary tree's broadcast
+ * flows, a hierarchical all-reduce's last phase's last step), ascending.
+ * *n receives their number; ids (may be NULL) receives the *n ids.
+ * NETSIM_E_STATE before any such call.
+ */
+netsim_status netsim_last_exits(const netsim_t* h, int64_t* n, int64_t* ids);
+
+/*
  * Per-link latency of scenario `scen` (num_links = its link count, values
  * finite >= 0, copied), replacing what its built-in fabric set.  A flow
  * sends at its max-min rate as before and frees its links when its last byte
@@ -394,12 +416,14 @@ netsim_status netsim_stream_hier_allreduce(netsim_t* h, int32_t scen, int32_t m,
 netsim_status netsim_stream_send(netsim_t* h, int32_t scen, int32_t src, int64_t src_stream,
                                  int32_t dst, int64_t dst_stream, double nbytes, int64_t* done);
 
-/* Totals over all scenarios: flows, path incidences, dependency entries. */
+/* Totals over all scenarios: flows, path incidences (flow-link pairs of the
+ * Section 4.2 rate solve), dependency entries. */
 netsim_status netsim_counts(const netsim_t* h, int64_t* num_flows, int64_t* num_incidences,
                             int64_t* num_deps);
 
 /*
- * Copies the flows as stored (id order): scenario, endpoints, bytes, start,
+ * Copies the flows as stored (id order; the flows of Section 4.1 with the
+ * routes the fabric chose): scenario, endpoints, bytes, start,
  * path CSR (local link ids) and dependency CSR.  Any pointer may be NULL.
  * Sizes: num_flows (+1 for the offsets), num_incidences, num_deps.
  */
@@ -407,10 +431,15 @@ netsim_status netsim_export_flows(const netsim_t* h, int32_t* scen, int32_t* src
                                   double* nbytes, double* start, int64_t* path_off,
                                   int32_t* path_link, int64_t* dep_off, int64_t* dep_ids);
 
-/* Replaces the stopping points of later runs (see netsim_options). */
+/* Replaces the stopping points of later runs (see netsim_options): Section
+ * 4.2's advance by a number of steps or up to a time. */
 netsim_status netsim_set_limits(netsim_t* h, int64_t max_events, double until);
 
 /*
+ * The simulation (Section 4.2, the network simulator with time rollback:
+ * between neighbouring events flows keep stable throughputs, the max-min
+ * fair allocation found by water-filling; events are processed in time
+ * order, completions releasing what depends on them).
  * Simulates every scenario from t = 0 on the device, in one kernel launch
  * (the event loop and the rate solves stay on the GPU), up to the limits of
  * netsim_options / netsim_set_limits.  hip_stream may be NULL (the default
@@ -467,15 +496,20 @@ netsim_status netsim_gc(netsim_t* h, double t_min);
 netsim_status netsim_num_checkpoints(const netsim_t* h, int64_t* n);
 
 /*
+ * The output of Section 4.1's netsim: the completion time of every flow.
  * finish[num_flows] (host) receives each flow's completion time (NaN for a
  * flow not finished when the run stopped early); makespan[num_scenarios]
  * (may be NULL) each scenario's largest finish time.  Needs a prior run.
  */
 netsim_status netsim_get_finish(const netsim_t* h, double* finish, double* makespan);
 
-/* Same as netsim_get_finish, into device memory d_finish[num_flows]. */
+/* Same as netsim_get_finish (Section 4.1's completion times), into device
+ * memory d_finish[num_flows]. */
 netsim_status netsim_get_finish_device(const netsim_t* h, double* d_finish);
 
+/* Counts and times of the last run (netsim_stats above): the events of the
+ * Section 4.2 event loop, its max-min rate solves and their rounds, the work
+ * swept, device and upload time. */
 netsim_status netsim_get_stats(const netsim_t* h, netsim_stats* stats);
 
 /*
@@ -548,7 +582,8 @@ netsim_status netsim_solve_rates_noalloc(int32_t device, int32_t num_links,
 /* Message of the last failure on h (or of the calling thread when h is NULL). */
 const char* netsim_last_error(const netsim_t* h);
 
-/* Frees the handle and its device memory; NULL is ignored. */
+/* Frees the handle, its device memory and its rollback checkpoints (Section
+ * 4.2's history); NULL is ignored. */
 void netsim_destroy(netsim_t* h);
 
 #ifdef __cplusplus

@@ -54,6 +54,8 @@ struct netsim {
   std::vector<int32_t> p_link;
   std::vector<int64_t> d_off{0};
   std::vector<int64_t> d_ids;
+  std::vector<int64_t> last_exits;    // exit flows of the last operation appended
+  bool has_exits = false;
   std::string err;
   // device layout (built at the first run)
   bool prepared = false;
@@ -99,6 +101,21 @@ bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0.0; }
 
 netsim_status hip_fail(const netsim_t* h, hipError_t e, const char* what) {
   return fail(h, NETSIM_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// The exit flows of the operation just appended (see netsim_last_exits).
+void set_exits(netsim_t* h, int64_t f0, int64_t f1) {
+  h->last_exits.resize((size_t)(f1 - f0));
+  for (int64_t f = f0; f < f1; ++f) h->last_exits[(size_t)(f - f0)] = f;
+  h->has_exits = true;
+}
+void set_exits(netsim_t* h, const std::vector<std::vector<int64_t>>& per_rank) {
+  std::vector<int64_t> all;
+  for (const auto& v : per_rank) all.insert(all.end(), v.begin(), v.end());
+  std::sort(all.begin(), all.end());
+  all.erase(std::unique(all.begin(), all.end()), all.end());
+  h->last_exits = all;
+  h->has_exits = true;
 }
 
 // Validates and appends n flows (all or nothing).  paths: explicit CSR or
@@ -1117,7 +1134,11 @@ netsim_status netsim_add_flows(netsim_t* h, int32_t scen, int64_t n, const int32
                                const int64_t* path_off, const int32_t* path_link,
                                const int64_t* dep_off, const int64_t* dep_ids, int64_t* first_id) {
   if (!h) return fail(nullptr, NETSIM_E_INVALID, "add_flows: handle is NULL");
-  return add_flows_impl(h, scen, n, src, dst, nbytes, start, path_off, path_link, dep_off, dep_ids, first_id);
+  const int64_t first = (int64_t)h->f_bytes.size();
+  const netsim_status st =
+      add_flows_impl(h, scen, n, src, dst, nbytes, start, path_off, path_link, dep_off, dep_ids, first_id);
+  if (st == NETSIM_OK) set_exits(h, first, first + n);  // every flow of the batch
+  return st;
 }
 
 netsim_status netsim_add_ring(netsim_t* h, int32_t scen, int32_t kind, int32_t mode, int32_t p,
@@ -1158,6 +1179,9 @@ netsim_status netsim_add_ring(netsim_t* h, int32_t scen, int32_t kind, int32_t m
   st = add_flows_impl(h, scen, n, src.data(), dst.data(), b.data(), t0.data(), nullptr, nullptr,
                       doff.data(), dids.data(), nullptr);
   if (st) return st;
+  // exits: a chained ring's last step, every flow otherwise
+  const int64_t e0 = mode == NETSIM_MODE_CHAINED ? first + (steps - 1) * p : first;
+  set_exits(h, e0, first + n);
   if (first_id) *first_id = first;
   if (count) *count = n;
   return NETSIM_OK;
@@ -1194,6 +1218,7 @@ netsim_status netsim_add_all_to_all(netsim_t* h, int32_t scen, int32_t p, const 
   st = add_flows_impl(h, scen, n, src.data(), dst.data(), b.data(), t0.data(), nullptr, nullptr,
                       doff.data(), dids.data(), nullptr);
   if (st) return st;
+  set_exits(h, first, first + n);  // every flow
   if (first_id) *first_id = first;
   if (count) *count = n;
   return NETSIM_OK;
@@ -1416,8 +1441,11 @@ netsim_status netsim_add_tree_allreduce(netsim_t* h, int32_t scen, int32_t p, co
   if (st) return st;
   const int64_t first = (int64_t)h->f_bytes.size();
   FlowRows r;
-  tree_rows(p, ranks, nbytes, lag, n_after, after, first, &r, nullptr);
-  return commit_rows(h, scen, r, first, first_id, count);
+  std::vector<std::vector<int64_t>> done((size_t)p);
+  tree_rows(p, ranks, nbytes, lag, n_after, after, first, &r, &done);
+  st = commit_rows(h, scen, r, first, first_id, count);
+  if (st == NETSIM_OK) set_exits(h, done);  // the broadcast flows of both trees
+  return st;
 }
 
 netsim_status netsim_add_hier_allreduce(netsim_t* h, int32_t scen, int32_t m, int32_t g,
@@ -1431,8 +1459,11 @@ netsim_status netsim_add_hier_allreduce(netsim_t* h, int32_t scen, int32_t m, in
   if (st) return st;
   const int64_t first = (int64_t)h->f_bytes.size();
   FlowRows r;
-  hier_rows(m, g, ranks, nbytes, lag, n_after, after, first, &r, nullptr);
-  return commit_rows(h, scen, r, first, first_id, count);
+  std::vector<std::vector<int64_t>> done;
+  hier_rows(m, g, ranks, nbytes, lag, n_after, after, first, &r, &done);
+  st = commit_rows(h, scen, r, first, first_id, count);
+  if (st == NETSIM_OK) set_exits(h, done);  // the last step of the last phase
+  return st;
 }
 
 }  // extern "C"
@@ -1664,6 +1695,14 @@ netsim_status netsim_stream_hier_allreduce(netsim_t* h, int32_t scen, int32_t m,
         return (netsim_status)NETSIM_OK;
       },
       [&](int64_t, int32_t i) { return per_rank[(size_t)i]; });
+}
+
+netsim_status netsim_last_exits(const netsim_t* h, int64_t* n, int64_t* ids) {
+  if (!h || !n) return fail(h, NETSIM_E_INVALID, "last_exits: NULL argument");
+  if (!h->has_exits) return fail(h, NETSIM_E_STATE, "last_exits: no operation appended yet");
+  *n = (int64_t)h->last_exits.size();
+  if (ids) std::copy(h->last_exits.begin(), h->last_exits.end(), ids);
+  return NETSIM_OK;
 }
 
 netsim_status netsim_counts(const netsim_t* h, int64_t* num_flows, int64_t* num_incidences,

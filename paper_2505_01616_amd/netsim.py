@@ -104,6 +104,7 @@ _SIGS = {
     "netsim_stream_tree_allreduce": (_I32, [_H, _I32, _I32, _P, _P, _D, _P]),
     "netsim_stream_hier_allreduce": (_I32, [_H, _I32, _I32, _I32, _P, _P, _D, _P]),
     "netsim_counts": (_I32, [_H, ctypes.POINTER(_I64), ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
+    "netsim_last_exits": (_I32, [_H, ctypes.POINTER(_I64), _P]),
     "netsim_export_flows": (_I32, [_H, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "netsim_set_limits": (_I32, [_H, _I64, _D]),
     "netsim_run": (_I32, [_H, _P]),
@@ -284,6 +285,15 @@ def netsim_counts(h):
     f, z, d = _I64(), _I64(), _I64()
     _check(h, lib.netsim_counts(h, ctypes.byref(f), ctypes.byref(z), ctypes.byref(d)))
     return f.value, z.value, d.value
+
+
+def netsim_last_exits(h) -> np.ndarray:
+    lib = load_library()
+    n = _I64()
+    _check(h, lib.netsim_last_exits(h, ctypes.byref(n), None))
+    ids = np.zeros(max(n.value, 1), np.int64)
+    _check(h, lib.netsim_last_exits(h, ctypes.byref(n), _ptr(ids)))
+    return ids[: n.value]
 
 
 def netsim_export_flows(h) -> dict:

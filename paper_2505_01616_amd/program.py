@@ -24,8 +24,6 @@ _KINDS = {"leaf_spine": ns.TOPO_LEAF_SPINE, "rail": ns.TOPO_RAIL, "fat_tree": ns
 _RING = {"allreduce": ns.RING_ALLREDUCE, "reduce_scatter": ns.RING_REDUCE_SCATTER,
          "all_gather": ns.RING_ALL_GATHER}
 _MODE = {"chained": ns.MODE_CHAINED, "flat": ns.MODE_FLAT, "aggregated": ns.MODE_AGGREGATED}
-_STEPS = {"allreduce": lambda p: 2 * (p - 1), "reduce_scatter": lambda p: p - 1,
-          "all_gather": lambda p: p - 1}
 
 
 def topology_struct(t, keep: list) -> ns.netsim_topology:
@@ -142,39 +140,19 @@ def load_program(program, opt: ns.netsim_options = None) -> Loaded:
                 batch.flush()
                 next_id = ns.netsim_counts(h)[0]
                 if name == "Ring":
-                    p = len(op.ranks)
                     first, n = ns.netsim_add_ring(h, s, _RING[op.kind], _MODE[op.mode], op.ranks,
                                                   op.nbytes, op.lag, after)
-                    firsts.append(first)
-                    if op.mode == "chained":
-                        steps = _STEPS[op.kind](p)
-                        exits.append(list(range(first + (steps - 1) * p, first + steps * p)))
-                    else:
-                        exits.append(list(range(first, first + n)))
                 elif name == "AllToAll":
                     first, n = ns.netsim_add_all_to_all(h, s, op.ranks, op.nbytes, op.lag, after)
-                    firsts.append(first)
-                    exits.append(list(range(first, first + n)))
                 elif name == "Tree":
-                    p = len(op.ranks)
                     first, n = ns.netsim_add_tree_allreduce(h, s, op.ranks, op.nbytes, op.lag, after)
-                    firsts.append(first)
-                    exits.append(list(range(first + (p - 1), first + 2 * (p - 1)))
-                                 + list(range(first + 3 * (p - 1), first + n)))
                 elif name == "Hier":
-                    m, g = np.asarray(op.ranks).shape
                     first, n = ns.netsim_add_hier_allreduce(h, s, op.ranks, op.nbytes, op.lag, after)
-                    firsts.append(first)
-                    # the last step of the last phase: per server (the all-gather),
-                    # or, with one rank per server, the cross-server ring's
-                    if g > 1:
-                        p3 = first + n - m * (g - 1) * g
-                        exits.append([p3 + a * (g - 1) * g + (g - 2) * g + i
-                                      for a in range(m) for i in range(g)])
-                    else:
-                        exits.append(list(range(first + n - m, first + n)))
                 else:
                     raise TypeError(f"unknown operation {name}")
+                # what a later operation waits for: the library's exit flows
+                firsts.append(first)
+                exits.append(ns.netsim_last_exits(h).tolist())
                 next_id = first + n
             batch.flush()
             nflows.append(ns.netsim_counts(h)[0] - first_flow[-1])

@@ -210,3 +210,50 @@ def test_update_start_host_side():
         ns.netsim_gc(h, 1.0)
     finally:
         ns.netsim_destroy(h)
+
+
+@pytest.mark.parametrize("kind", ["ring-chained", "ring-flat", "ring-aggregated", "rs-chained",
+                                  "all-to-all", "tree", "hier"])
+def test_last_exits_are_the_oracles(kind):
+    """netsim_last_exits after each kind of operation equals the oracle's exit
+    flows of that operation, read off the dependency list of a barrier the
+    oracle places after it (ids relative to the operation's first flow)."""
+    from workloads.program import AllToAll, Barrier, Hier, Tree
+    topo = configs.c1_topology(1)
+    ranks = np.array([0, 9, 17, 3, 40, 63], dtype=np.int32)
+    if kind.startswith("ring") or kind.startswith("rs"):
+        k = "reduce_scatter" if kind.startswith("rs") else "allreduce"
+        op = Ring(k, ranks, 12 * MiB, mode=kind.split("-")[1])
+    elif kind == "all-to-all":
+        op = AllToAll(ranks, np.full((6, 6), 1.0 * MiB))
+    elif kind == "tree":
+        op = Tree(ranks, 8 * MiB)
+    else:
+        op = Hier(np.array([[0, 1, 2], [8, 9, 10], [16, 17, 18]], dtype=np.int32), 9 * MiB)
+    sc = Scenario(topo)
+    sc.add(Send(5, 6, 1.0))          # a flow before, so ids do not start at 0
+    sc.add(op)
+    sc.add(Barrier(after=(1,)))
+    fs = oflows.expand(sc)
+    want = fs.dep_ids[fs.dep_off[fs.F - 1]:fs.dep_off[fs.F]] - 1
+    ld = prog.load_program(Program("x", [Scenario(topo, ops=sc.ops[:2])]))
+    try:
+        got = ns.netsim_last_exits(ld.handle) - 1
+    finally:
+        ld.close()
+    assert np.array_equal(np.sort(got), np.sort(want))
+    assert len(got) > 0
+
+
+def test_last_exits_of_a_batch_and_before_any():
+    h = ns.netsim_create(np.array([0, 2], np.int64), np.array([1.0, 2.0]))
+    try:
+        with pytest.raises(ns.NetsimError) as ei:
+            ns.netsim_last_exits(h)
+        assert ei.value.status == ns.E_STATE
+        ns.netsim_add_flows(h, 0, np.array([1.0, 2.0, 0.0]), np.zeros(3),
+                            path_off=np.array([0, 1, 2, 2], np.int64),
+                            path_link=np.array([0, 1], np.int32))
+        assert list(ns.netsim_last_exits(h)) == [0, 1, 2]
+    finally:
+        ns.netsim_destroy(h)
