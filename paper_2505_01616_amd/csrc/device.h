@@ -173,8 +173,10 @@ struct Params {
   uint64_t* slots;         // grid min-reduction slots [4]
 };
 
-// Words of Params::bar, cleared before every launch.
-constexpr int BAR_WORDS = 9216;
+// Words of Params::bar, cleared before every launch: 9,216 words of
+// barrier, registration and cluster words, then the cluster helpers'
+// arrival lines (64 clusters x 32 lines of 32 words).
+constexpr int BAR_WORDS = 9216 + 64 * 32 * 32;
 
 hipError_t launch_block(const Params& p, int blocks, int threads, hipStream_t s);
 hipError_t launch_grid(const Params& p, int blocks, int threads, hipStream_t s);

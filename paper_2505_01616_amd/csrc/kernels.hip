@@ -278,6 +278,10 @@ constexpr int CL_ISW = 48;                // incidences swept (int64, summed ove
 constexpr int CL_CNT = 64;               // barrier among the helpers (arrivals, growing)
 constexpr int CL_CLK = 96;                // job phase times of the first helper (int64 [8])
 constexpr uint32_t CL_CLOSED = 0xFFFFFFFFu;
+// Helper arrival lines: cluster k owns CL_LINES lines of 128 bytes from
+// CL_ARRIVE + CL_ARRIVE_STRIDE*k; helper h writes only line h.
+constexpr int CL_ARRIVE = 9216, CL_LINES = 32, CL_LINE_WORDS = 32;
+constexpr int CL_ARRIVE_STRIDE = CL_LINES * CL_LINE_WORDS;
 constexpr int NOT_TAKEN = 2;              // the helpers have left: solve locally
 // A helper with no job for this long leaves (its leader then solves alone).
 constexpr uint64_t IDLE_TICKS = 6000000000ull;  // 60 s at 100 MHz
@@ -287,7 +291,8 @@ constexpr uint64_t IDLE_TICKS = 6000000000ull;  // 60 s at 100 MHz
 // only shorten the kernel's own bounded waits.
 constexpr int DEBUG_HELPERS_LEAVE = 4, DEBUG_HELPER_BARRIER_GIVES_UP = 8;
 static_assert(XREG_BASE + 16 * 16 <= CL_BASE, "registration words");
-static_assert(CL_BASE + 16 * CL_MAXC * CL_STRIDE <= BAR_WORDS, "cluster words");
+static_assert(CL_BASE + 16 * CL_MAXC * CL_STRIDE <= CL_ARRIVE, "cluster words");
+static_assert(CL_ARRIVE + 16 * CL_MAXC * CL_ARRIVE_STRIDE <= BAR_WORDS, "arrival lines");
 
 // Waits (one thread) until *p != v, giving up when the abort word is set or
 // after `ticks` (then raising it).  Returns false if it gave up.
@@ -334,14 +339,21 @@ __device__ __forceinline__ void xcd_release(bool formal) {
 // when the state lives in global memory, after a full agent-scope release),
 // so the helpers' atomics never follow plain stores to the same words.
 //
-// Barrier: workgroups add one to a counter that only grows and wait until it
-// reaches (barriers passed) x (helpers), so no arrival has to reset it.  A
-// wait longer than `patience` (BARRIER_TIMEOUT_TICKS) raises the launch's
-// abort word.
+// Barrier: each helper has an arrival line of its own (no two arrivals touch
+// one word, so none waits for another's read-modify-write) and, at its k-th
+// barrier, stores (k, payload) into word k mod 2 of it; lane h of the first
+// wave of every helper polls helper h's line until all of them show k.  The
+// payload (the helper's count of unfrozen flows and a fault bit) reaches
+// every helper with the arrival itself, so a round needs no counter in
+// memory.  Two words per line: a helper can be at most one barrier ahead of
+// the slowest poller (it cannot pass barrier k + 1 before that poller
+// arrives there), so word k mod 2 still holds barrier k's payload while
+// anybody polls it.  A wait longer than `patience` (BARRIER_TIMEOUT_TICKS)
+// raises the launch's abort word.
 struct ClusterG {
   double* lds;
   int* ldsi;
-  int* flag;      // shared: abort state as seen by this block's thread 0
+  int* flag;      // shared [2]: abort state as seen by this block's first wave, payload sum
   uint32_t* bar;  // launch words (abort flag)
   uint32_t* cw;   // this XCD's cluster words
   uint32_t gen;
@@ -349,6 +361,10 @@ struct ClusterG {
   bool ab;
   uint64_t patience;  // barrier time-out (ticks)
   bool formal;        // agent-scope release fences instead of drains (debug)
+  uint64_t* lines;    // this cluster's arrival lines (CL_LINE_WORDS / 2 words apart)
+  int64_t* dR;        // shared memory: per-link deltas of this helper (residual,
+  int32_t* dn;        //   unfrozen count), folded into link state once per phase
+  int dcap;           // links the delta arrays hold
   __device__ Lists* lists(ScenCtl* C) const { return &C->k; }
   __device__ int tid() const { return rank * blockDim.x + threadIdx.x; }
   __device__ int block_base() const { return rank * blockDim.x; }
@@ -356,41 +372,67 @@ struct ClusterG {
   __device__ int block_id() const { return rank; }
   __device__ int nthr() const { return nh * blockDim.x; }
   __device__ bool aborted() const { return ab; }
-  __device__ __forceinline__ void sync() {
+  __device__ __forceinline__ void sync() { (void)sync_sum(0u); }
+  // The barrier; returns the sum over the helpers of their payloads (low 31
+  // bits) with bit 31 set if any helper's payload had it.
+  __device__ __forceinline__ uint32_t sync_sum(uint32_t payload) {
     xcd_release(formal);
     __syncthreads();
-    if (threadIdx.x == 0) {
-      // the arrival and a look at the abort word travel together; an abort
-      // raised meanwhile is seen at a later barrier or in a wait (the word
-      // stays set, so a helper that leaves early cannot strand the others)
-      const uint32_t target = (gen + 1) * (uint32_t)nh;
-      uint32_t a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const uint32_t prev =
-          __hip_atomic_fetch_add(&cw[CL_CNT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (a == 0 && prev + 1 != target && !wait_reach(&cw[CL_CNT], target)) a = 1;
+    if (threadIdx.x < 64) {
+      const int lane = (int)threadIdx.x;
+      const uint32_t target = gen + 1;
+      const int w = (int)(target & 1u);
+      uint32_t a = 0;
+      if (lane == 0) {
+        // the arrival and a look at the abort word travel together; an abort
+        // raised meanwhile is seen at a later barrier or in a wait (the word
+        // stays set, so a helper that leaves early cannot strand the others)
+        a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(lines + (size_t)rank * (CL_LINE_WORDS / 2) + w,
+                           ((uint64_t)target << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      a = (uint32_t)__shfl((int)a, 0, 64);
+      uint64_t* mine = lines + (size_t)(lane < nh ? lane : 0) * (CL_LINE_WORDS / 2) + w;
+      uint64_t v = 0;
+      if (a == 0) {
+        const uint64_t t0 = wall_clock64();
+        for (uint32_t i = 1;; ++i) {
+          bool here = true;
+          if (lane < nh) {
+            v = __hip_atomic_load(mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            here = (int32_t)((uint32_t)(v >> 32) - target) >= 0;
+          }
+          if (__all(here)) break;
+          __builtin_amdgcn_s_sleep(1);
+          if ((i & 15) != 1) continue;
+          if (lane == 0) {
+            a = __hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (a == 0 && wall_clock64() - t0 > patience) {
+              __hip_atomic_store(&bar[BAR_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              a = 1;
+            }
+          }
+          a = (uint32_t)__shfl((int)a, 0, 64);
+          if (a != 0) break;
+        }
+      }
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      *flag = (int)a;
+      uint32_t sum = lane < nh ? (uint32_t)v & 0x7FFFFFFFu : 0u;
+      uint32_t any = lane < nh ? (uint32_t)v & 0x80000000u : 0u;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        sum += (uint32_t)__shfl_xor((int)sum, o, 64);
+        any |= (uint32_t)__shfl_xor((int)any, o, 64);
+      }
+      if (lane == 0) {
+        flag[0] = (int)a;
+        flag[1] = (int)(sum | any);
+      }
     }
     gen += 1;
     __syncthreads();
-    ab = *flag != 0;
-  }
-  // Waits until the counter reaches target (counted modulo 2^32); the first
-  // poll and every 16th after it give up on the abort word or after
-  // `patience` ticks (then raising it).  Returns false if it gave up.
-  __device__ __forceinline__ bool wait_reach(uint32_t* p, uint32_t target) {
-    const uint64_t t0 = wall_clock64();
-    for (uint32_t i = 1;
-         (int32_t)(__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0; ++i) {
-      __builtin_amdgcn_s_sleep(1);
-      if ((i & 15) != 1) continue;
-      if (__hip_atomic_load(&bar[BAR_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return false;
-      if (wall_clock64() - t0 > patience) {
-        __hip_atomic_store(&bar[BAR_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return false;
-      }
-    }
-    return true;
+    ab = flag[0] != 0;
+    return (uint32_t)flag[1];
   }
   template <class T>
   __device__ T add(T* p, T v) {
@@ -408,6 +450,8 @@ struct ClusterG {
 
 template <class G> struct IsGrid { static constexpr bool value = false; };
 template <> struct IsGrid<GridG> { static constexpr bool value = true; };
+template <class G> struct IsCluster { static constexpr bool value = false; };
+template <> struct IsCluster<ClusterG> { static constexpr bool value = true; };
 
 // Appends the lanes with `pred` to a list: one atomic per wave.  Must be
 // reached by every lane of the wave.  Returns the slot (or -1 without pred).
@@ -1223,7 +1267,43 @@ struct SolveLds {
   double mf[LDS_FLOWS];
   uint16_t u[2][LDS_FLOWS];
   int cnt;
+  int anybad;  // some thread of the workgroup met a fault (cluster helpers)
 };
+
+// A helper's update of link l (residual r, unfrozen count c): into its
+// shared-memory deltas when it has them (dR non-null, uniform over the
+// workgroup), else straight into the link state.
+template <class G, class LK>
+__device__ __forceinline__ void link_add(G& g, LK& lk, int64_t* dR, int32_t* dn, int l0, int l, int64_t r,
+                                         int32_t c, bool with_r) {
+  if (dR) {
+    if (with_r) __hip_atomic_fetch_add(&dR[l - l0], r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __hip_atomic_fetch_add(&dn[l - l0], c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  } else {
+    if (with_r) lk.addR(g, l, r);
+    lk.addN(g, l, (int64_t)c);
+  }
+}
+
+// Folds a helper's deltas into the link state (one atomic per link and
+// field it changed, instead of one per flow and link) and clears them.
+// Integer sums: the link state ends bit-identical to per-flow updates.
+// Follows a workgroup barrier after the last delta update.
+template <class G, class LK>
+__device__ __forceinline__ void fold_deltas(G& g, LK& lk, int64_t* dR, int32_t* dn, int l0, int nl) {
+  for (int i = threadIdx.x; i < nl; i += blockDim.x) {
+    const int64_t r = dR[i];
+    const int32_t c = dn[i];
+    if (r != 0) {
+      lk.addR(g, l0 + i, r);
+      dR[i] = 0;
+    }
+    if (c != 0) {
+      lk.addN(g, l0 + i, (int64_t)c);
+      dn[i] = 0;
+    }
+  }
+}
 
 template <class G, class LK>
 __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl* C, const int32_t* list0,
@@ -1243,6 +1323,23 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
   if (!warm) cold_links(g, P, lk, C);
   if (tid == 0)
     for (int k = 0; k < 3; ++k) g.store(&K->rem3[k], 0);
+  // a helper whose part's links fit its delta arrays updates link state
+  // through them (folded before each barrier)
+  const int nlk = C->l1 - C->l0;
+  int64_t* dR = nullptr;
+  int32_t* dn = nullptr;
+  if constexpr (IsCluster<G>::value) {
+    if (threadIdx.x == 0) S.anybad = 0;
+    if (nlk <= g.dcap) {
+      dR = g.dR;
+      dn = g.dn;
+      for (int i = threadIdx.x; i < nlk; i += blockDim.x) {
+        dR[i] = 0;
+        dn[i] = 0;
+      }
+    }
+    __syncthreads();
+  }
   int bad = 0;
   // ids and path records into shared memory; re-solving (rs), each flow's
   // take-back too: remaining bytes brought up to rs->t, its rate and one
@@ -1270,14 +1367,18 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
       const int deg = unpack_path(rec, l0, lv);
 #pragma unroll
       for (int k = 0; k < 6; ++k)
-        if (k < deg) {
-          if (!fresh) lk.addR(g, lv[k], qv);
-          lk.addN(g, lv[k], (int64_t)1);
-        }
+        if (k < deg) link_add(g, lk, dR, dn, l0, lv[k], qv, 1, !fresh);
     }
   }
   int nu = nl;
   if (bad) g.store(&K->fault, bad);
+  if constexpr (IsCluster<G>::value) {
+    if (bad) S.anybad = 1;
+    if (dR) {
+      __syncthreads();
+      fold_deltas(g, lk, dR, dn, l0, nlk);
+    }
+  }
   g.sync();
   const uint32_t st0 = first_round(g, P, lk, C);
   clk.lap(2);
@@ -1289,7 +1390,8 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
     const uint16_t* uin = S.u[r & 1];
     uint16_t* uout = S.u[(r & 1) ^ 1];
     if (threadIdx.x == 0) S.cnt = 0;
-    if (tid == 0) g.store(&K->rem3[(r + 1) % 3], 0);
+    if constexpr (!IsCluster<G>::value)
+      if (tid == 0) g.store(&K->rem3[(r + 1) % 3], 0);
     round_table(g, lk, C);
     clk.lap(2);
     // phase B: smallest share on each path; block links above it
@@ -1322,10 +1424,7 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
           const int64_t qv = (int64_t)__builtin_rint(m * P.scale);
 #pragma unroll
           for (int k = 0; k < 6; ++k)
-            if (k < deg) {
-              lk.addR(g, lv[k], -qv);
-              lk.addN(g, lv[k], (int64_t)-1);
-            }
+            if (k < deg) link_add(g, lk, dR, dn, l0, lv[k], -qv, -1, true);
         } else {
           keep = true;
         }
@@ -1341,24 +1440,50 @@ __device__ __forceinline__ int solve_lds(G& g, const Params& P, LK& lk, ScenCtl*
       }
     }
     if (bad) g.store(&K->fault, bad);
-    __syncthreads();
-    const int nu_new = S.cnt;
-    if (threadIdx.x == 0 && nu_new > 0) g.add(&K->rem3[r % 3], (int32_t)nu_new);
-    clk.lap(5);
-    g.sync();
-    clk.lap(6);
-    if (threadIdx.x == 0) {
-      rounds += 1;
-      fsw += total;
+    int ft, left;
+    int nu_new;
+    if constexpr (IsCluster<G>::value) {
+      // the unfrozen count and a fault bit travel with the barrier's arrival
+      if (bad) S.anybad = 1;
+      __syncthreads();
+      nu_new = S.cnt;
+      if (dR) fold_deltas(g, lk, dR, dn, l0, nlk);
+      clk.lap(5);
+      const uint32_t res = g.sync_sum((uint32_t)nu_new | (S.anybad ? 0x80000000u : 0u));
+      clk.lap(6);
+      if (threadIdx.x == 0) {
+        rounds += 1;
+        fsw += total;
+      }
+      if (g.aborted()) return ST_BARRIER;
+      ft = 0;
+      if (res & 0x80000000u) {  // some helper met a fault: which one
+        if (threadIdx.x == 0) bc[0] = g.load(&K->fault);
+        __syncthreads();
+        ft = bc[0];
+      }
+      left = (int)(res & 0x7FFFFFFFu);
+    } else {
+      __syncthreads();
+      nu_new = S.cnt;
+      if (threadIdx.x == 0 && nu_new > 0) g.add(&K->rem3[r % 3], (int32_t)nu_new);
+      clk.lap(5);
+      g.sync();
+      clk.lap(6);
+      if (threadIdx.x == 0) {
+        rounds += 1;
+        fsw += total;
+      }
+      if (g.aborted()) return ST_BARRIER;
+      // one read of the two counters per workgroup, shared through shared memory
+      if (threadIdx.x == 0) {
+        bc[0] = g.load(&K->fault);
+        bc[1] = g.load(&K->rem3[r % 3]);
+      }
+      __syncthreads();
+      ft = bc[0];
+      left = bc[1];
     }
-    if (g.aborted()) return ST_BARRIER;
-    // one read of the two counters per workgroup, shared through shared memory
-    if (threadIdx.x == 0) {
-      bc[0] = g.load(&K->fault);
-      bc[1] = g.load(&K->rem3[r % 3]);
-    }
-    __syncthreads();
-    const int ft = bc[0], left = bc[1];
     if (ft != 0) { rc = ft == 2 ? ST_OVERFLOW : ST_BAD_SHARE; break; }
     if (left == 0) break;
     if (left >= total) { rc = ST_BAD_SHARE; break; }  // a round must freeze something
@@ -2255,7 +2380,7 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
   __shared__ int ldsi[128];
   __shared__ Tally tally;
   __shared__ Lists lists;
-  __shared__ int flag;
+  __shared__ int flag[2];
   __shared__ int box[8];
   __shared__ double tjob[1];
   __shared__ int claim;
@@ -2283,9 +2408,8 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
     box[0] = (int)x * CL_MAXC + cid;
     box[1] = (int)rank - cid * size;  // rank in the cluster
     // helpers: the cluster's other workgroups, at most P.assist_helpers of
-    // them (every helper arrives on one counter at each barrier, and arrivals
-    // on one word serialise: fewer helpers, each with more flows, are faster)
-    box[2] = ok ? min(members - 1, max(P.assist_helpers, 0)) : 0;
+    // them and one per arrival line
+    box[2] = ok ? min(min(members - 1, max(P.assist_helpers, 0)), CL_LINES) : 0;
   }
   __syncthreads();
   const int cl = box[0], rank = box[1], nh = box[2];
@@ -2294,8 +2418,14 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
   if (rank != 0) {  // workgroups beyond the helpers have nothing to do
     if (nh > 0 && rank <= nh) {
       const uint64_t patience = (P.debug & DEBUG_HELPER_BARRIER_GIVES_UP) ? 0 : BARRIER_TIMEOUT_TICKS;
-      ClusterG cg{lds, ldsi, &flag, P.bar, cw, 0u, rank - 1, nh, false, patience,
-                  (P.debug & DEBUG_FORMAL_RELEASE) != 0};
+      // per-link deltas in the pool after the solve's own arrays
+      constexpr int off = (int)((sizeof(SolveLds) + 15) & ~size_t(15));
+      constexpr int dcap = (POOL_BYTES - off) / 12;
+      ClusterG cg{lds, ldsi, flag, P.bar, cw, 0u, rank - 1, nh, false, patience,
+                  (P.debug & DEBUG_FORMAL_RELEASE) != 0,
+                  reinterpret_cast<uint64_t*>(P.bar + CL_ARRIVE + CL_ARRIVE_STRIDE * cl),
+                  reinterpret_cast<int64_t*>(pool + off), reinterpret_cast<int32_t*>(pool + off + 8 * dcap),
+                  dcap};
       helper_loop(P, cg, *reinterpret_cast<SolveLds*>(pool), &tally, box, tjob);
     }
     return;
