@@ -201,12 +201,17 @@ def sweep_traffic_from_profile():
     return prof["freeze_traffic_bytes"] + prof["count_traffic_bytes"]
 
 
-def rollback_bench(ns, prog, program, stream, pieces=10):
+def rollback_bench(ns, prog, program, stream, pieces=10, history_mb=72000):
     """Time rollback on C4: the complete simulation as one launch; the same
-    simulation advanced in `pieces` checkpointed launches (on a second
-    handle); then a start moved for a flow that finished at about 55% of the
-    horizon: its part goes back to the checkpoint before the flow's release
-    and is re-simulated to the end while the other parts stay finished."""
+    simulation advanced in `pieces` checkpointed launches, with checkpoints
+    only (AUTO's cluster layout, and the block layout) and also keeping the
+    rollback history (`history_mb` MiB: every undo record of the complete
+    run fits; the block layout, as the cluster kernel keeps none); then a
+    start moved for a flow that finished at about 55% of the horizon.  With
+    checkpoints only its part goes back to the last checkpoint before the
+    flow's release, with the history to its last event before it; either
+    way the part is re-simulated to the end while the other parts stay
+    finished, and both give the same finish times bit for bit."""
     import numpy as np
     out = {"metric": "time rollback on the 4096-GPU all-to-all workload", "pieces": pieces}
     ld = prog.load_program(program)
@@ -217,30 +222,45 @@ def rollback_bench(ns, prog, program, stream, pieces=10):
     finally:
         ld.close()
     T = float(np.nanmax(ref))
-    ld = prog.load_program(program)
-    h = ld.handle
-    try:
-        dev, wall = 0.0, time.perf_counter()
-        for k in range(1, pieces + 1):
-            ns.netsim_advance(h, until=T * k / pieces if k < pieces else math.inf, stream=stream)
-            dev += ns.netsim_get_stats(h)["device_seconds"]
-            print(f"advance {k}/{pieces}", file=sys.stderr, flush=True)
-        out["pieces_device_s"] = dev
-        out["pieces_wall_s_incl_checkpoints"] = time.perf_counter() - wall
-        out["pieces_equal_one_run_bitwise"] = bool(np.array_equal(ns.netsim_get_finish(h), ref))
-        out["checkpoints"] = ns.netsim_num_checkpoints(h)
-        ex = ns.netsim_export_flows(h)
-        cand = np.nonzero((ex["nbytes"] > 0) & (ref > 0.55 * T) & (ref < 0.6 * T))[0]
-        x = int(cand[len(cand) // 2])
-        t0 = time.perf_counter()
-        ns.netsim_update_start(h, x, float(ex["start"][x]) + 20e-6)
-        out["rollback_update_wall_s"] = time.perf_counter() - t0
-        ns.netsim_advance(h, stream=stream)
-        out["resimulate_device_s"] = ns.netsim_get_stats(h)["device_seconds"]
-        got = ns.netsim_get_finish(h)
-        out["moved_flows"] = int(np.sum(got != ref))
-    finally:
-        ld.close()
+    results = {}
+    legs = (("checkpoints", 0, ns.EXEC_AUTO), ("checkpoints_block", 0, ns.EXEC_BLOCK),
+            ("history", history_mb, ns.EXEC_AUTO))
+    for name, mb, ex in legs:
+        ld = prog.load_program(program, ns.make_options(history_mb=mb, exec=ex))
+        h = ld.handle
+        r = {"history_mb": mb}
+        try:
+            dev, wall = 0.0, time.perf_counter()
+            for k in range(1, pieces + 1):
+                ns.netsim_advance(h, until=T * k / pieces if k < pieces else math.inf, stream=stream)
+                dev += ns.netsim_get_stats(h)["device_seconds"]
+            print(f"{name}: {pieces} advances done", file=sys.stderr, flush=True)
+            r["pieces_device_s"] = dev
+            r["pieces_wall_s_incl_checkpoints"] = time.perf_counter() - wall
+            r["pieces_equal_one_run_bitwise"] = bool(np.array_equal(ns.netsim_get_finish(h), ref))
+            r["checkpoints"] = ns.netsim_num_checkpoints(h)
+            ex = ns.netsim_export_flows(h)
+            cand = np.nonzero((ex["nbytes"] > 0) & (ref > 0.55 * T) & (ref < 0.6 * T))[0]
+            x = int(cand[len(cand) // 2])
+            t0 = time.perf_counter()
+            ns.netsim_update_start(h, x, float(ex["start"][x]) + 20e-6)
+            r["rollback_update_wall_s"] = time.perf_counter() - t0
+            ns.netsim_advance(h, stream=stream)
+            st = ns.netsim_get_stats(h)
+            r["layout"] = {ns.EXEC_GRID: "grid", ns.EXEC_BLOCK: "block",
+                           ns.EXEC_CLUSTER: "cluster"}.get(st["layout"], st["layout"])
+            r["resimulate_device_s"] = st["device_seconds"]
+            r["resimulated_events"] = st["launch_events"]
+            got = ns.netsim_get_finish(h)
+            r["moved_flows"] = int(np.sum(got != ref))
+            results[name] = (r, got)
+            print(f"{name}: rollback and re-simulation done", file=sys.stderr, flush=True)
+        finally:
+            ld.close()
+        out[name] = r
+    out["history_equals_checkpoints_bitwise"] = bool(
+        np.array_equal(results["history"][1], results["checkpoints"][1]) and
+        np.array_equal(results["history"][1], results["checkpoints_block"][1]))
     return out
 
 

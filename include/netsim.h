@@ -135,7 +135,17 @@ typedef struct {
                                 changes, independent parts on their own clocks):
                                 the same allocation in exact arithmetic, with
                                 different rounding                              */
-  int32_t reserved;
+  int32_t history_mb;        /* MiB of device memory for the rollback history
+                                (Section 4.2: the throughput history of every
+                                flow): per part a ring of undo records (32 bytes
+                                per flow re-solved in an event) and of event
+                                records (80 bytes each), shared among the parts
+                                in proportion to their flows.  With it,
+                                netsim_update_start returns a part to the end of
+                                its last event before the changed release, as
+                                long as the ring still holds every record since;
+                                otherwise (and with 0, the default, or in exact
+                                mode) to the latest checkpoint before it        */
 } netsim_options;
 
 /*
@@ -226,6 +236,9 @@ typedef struct {
                                 of exact mode; the share-table passes of the
                                 default solver (rounds run by helper workgroups,
                                 which have no such pass, add nothing)            */
+  int64_t launch_events;     /* events processed by the last launch, summed over
+                                parts (a continuation after a rollback re-simulates
+                                only from where the part went back to)           */
 } netsim_stats;
 
 /* Fills *opt with the defaults (device 0, auto layout, no limits, default solver). */

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnetsim.so")
-SOURCES = ["netsim.cpp", "fabric.cpp", "kernels.hip", "exact.hip", "sweep.hip"]
+SOURCES = ["netsim.cpp", "fabric.cpp", "kernels.hip", "exact.hip", "sweep.hip", "history.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

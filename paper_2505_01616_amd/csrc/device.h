@@ -31,6 +31,28 @@ struct Lists {
   int64_t lsw;             // links with unfrozen flows summed over the share-table passes
 };
 
+// Rollback history (paper Section 4.2: the simulator keeps every flow's
+// throughput history so that it can return to the state at any earlier
+// event).  Per part two rings in device memory: an undo record for every
+// flow taken back for a re-solve, holding its remaining bytes, their time
+// and its rate from before that event changed them, and a record of every
+// event.  Going back to event e takes the state after the last event,
+// applies each flow's first undo record written after e, and rebuilds
+// which flows were waiting, pending, active or finished from the events at
+// which each flow reached those states.
+struct HistUndo {
+  int32_t f, ev;           // device flow id; event (index in its part) that re-solved it
+  double rem, tref, rate;  // the flow's values before that event
+};
+struct HistEv {
+  double t;                // event time
+  int64_t hpos;            // undo records written up to the end of this event
+  int64_t solves, rounds, flows_swept, active_swept;  // statistics at its end
+  int64_t pending_swept, reselected, wide_solves, assisted;
+};
+// "Not yet" in the per-flow event indices (Params::evr, eva, evd).
+constexpr int32_t EV_NEVER = 0x7F7F7F7F;
+
 // Control block of one part in device memory.  A part is a set of flows of
 // one scenario that shares no link and no dependency with the rest of the
 // scenario, simulated with its own clock.  The host fills the ranges and the
@@ -56,6 +78,10 @@ struct ScenCtl {
   int64_t reselected, wide_solves;
   int64_t assisted;        // re-solves run by helper workgroups (cluster kernel)
   int64_t links_swept;     // links with unfrozen flows summed over link passes
+  // rollback history of the part (hcap = 0: none): undo records
+  // hist[hbase + (i mod hcap)] for i < hpos, event records hev[ebase + (e mod ecap)]
+  int64_t hpos, hbase, hcap, ebase, ecap;
+  int64_t launch_events;   // events processed by the last launch
   int32_t status;          // 0 ran to the end, 1 stopped at a limit, < 0 fault
   int32_t reserved;
   int64_t ticks[8];        // wall-clock ticks per phase (first thread of the group)
@@ -131,6 +157,12 @@ struct Params {
   double* rel;             // [F] release time (set when a flow is released or pending)
   double* base;            // [F] release base: finish time of the last predecessor
   int32_t* cnt;            // [F] predecessors not yet finished
+  int32_t* evr;            // [F] event (index in the part) at which the flow's last
+                           //     predecessor finished (EV_NEVER: not yet or none)
+  int32_t* eva;            // [F] event at which it became active (or, zero bytes, finished)
+  int32_t* evd;            // [F] event at which it finished
+  HistUndo* hist;          // rollback history (NULL: none), ring per part
+  HistEv* hev;
   const int32_t* comp;     // [F] component of the flow (flows of different
                            //     components share no link)
   uint64_t* theta;         // [C] per component: lowest level that may change
@@ -190,6 +222,14 @@ hipError_t cluster_capacity(int device, int* blocks);
 // Exact mode: one workgroup per part (one part per scenario), the oracle's
 // arithmetic (exact.hip); p.exact_lds_bytes of dynamic shared memory.
 hipError_t launch_exact(const Params& p, int blocks, int threads, hipStream_t s);
+// Part p (flows [f0, f1)) back to the end of its event es from the rollback
+// history (history.hip): rec is the record of event es, hpos_now the undo
+// records written so far; cnt0 and rel0 (device, [f1 - f0]) the part's
+// initial predecessor counts and release times; first ([f1 - f0]) and
+// counters ([2]) device scratch.  Asynchronous on st.
+hipError_t history_restore(const Params& P, int p, int f0, int f1, int64_t hbase, int64_t hcap, int32_t es,
+                           const HistEv& rec, int64_t hpos_now, const int32_t* cnt0, const double* rel0,
+                           int32_t* first, uint32_t* counters, hipStream_t st);
 // Bytes of exact-mode link state per link.
 int exact_link_bytes();
 // A wide exact solve of part C's n flows listed in act0 + C.f0, on the whole

@@ -496,6 +496,7 @@ __device__ void exact_loop(const Params& P, int sc, XShared& sh, unsigned char* 
     C->npend = np;
     C->holes = 0;
     C->events = events;
+    C->launch_events = events - events0;
     C->solves = solves;
     C->rounds = rounds;
     C->flows_swept = sh.fsw;

@@ -275,7 +275,6 @@ constexpr int CL_DONE = 32;               // jobs finished, summed over the help
 constexpr int CL_RC = 33;                 // job status (first helper)
 constexpr int CL_ROUNDS = 34, CL_FSW = 36;  // job rounds and flows swept (int64, first helper)
 constexpr int CL_ISW = 48;                // incidences swept (int64, summed over the helpers)
-constexpr int CL_CNT = 64;               // barrier among the helpers (arrivals, growing)
 constexpr int CL_CLK = 96;                // job phase times of the first helper (int64 [8])
 constexpr uint32_t CL_CLOSED = 0xFFFFFFFFu;
 // Helper arrival lines: cluster k owns CL_LINES lines of 128 bytes from
@@ -1562,11 +1561,16 @@ struct Assist {
       __hip_atomic_store(&cw[CL_SNEW], (uint32_t)s_new, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(reinterpret_cast<uint64_t*>(cw + CL_T), (uint64_t)__double_as_longlong(t),
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      // link state in global memory was last updated by this workgroup's
+      // the job's words must be performed before the post that publishes
+      // them (a helper that sees the new count reads them next).  Link state
+      // in global memory was last updated by this workgroup's
       // workgroup-scope atomics: a full agent-scope release (an L2
-      // write-back) puts it where the helpers' agent-scope atomics act on it;
-      // a copied-out state was stored at agent scope and is drained already
+      // write-back) puts it where the helpers' agent-scope atomics act on it
+      // and covers the job's words too; a copied-out state was stored at
+      // agent scope and is drained already, so the job's words need only
+      // their own drain
       if constexpr (!LK::kTable) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      else xcd_release(P.debug & DEBUG_FORMAL_RELEASE);
       uint32_t expect = seq;
       if (__hip_atomic_compare_exchange_strong(&cw[CL_MB], &expect, seq + 1, __ATOMIC_RELAXED,
                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
@@ -1739,12 +1743,13 @@ constexpr double KEEP = 1.0 - 1e-9;  // safety margin below theta
 
 // Flow f becomes active at time t: remaining bytes, active counts on its
 // links, a new slot (tau set after its first solve) and the arrivals list.
-template <class G, class LK>
+template <bool HIST, class G, class LK>
 __device__ __forceinline__ void activate(G& g, const Params& P, LK& lk, Lists* K, int f, double t,
                                          const Slots& sl, int32_t* arrOut, int ib, int cap,
-                                         int& err) {
+                                         int ev, int& err) {
   P.rem[f] = P.nbytes[f];
   P.tref[f] = t;
+  if constexpr (HIST) P.eva[f] = ev;
   for (int j = P.poff[f]; j < P.poff[f + 1]; ++j) lk.addNact(g, P.plink[j], 1);
   const int s = g.add(&K->slots, 1);
   if (s < cap) {
@@ -1761,21 +1766,26 @@ __device__ __forceinline__ void activate(G& g, const Params& P, LK& lk, Lists* K
 
 // Releases flow h at event time t, once its predecessors have all finished,
 // the latest of them at `base` (>= t) (called once per h).
-template <class G, class LK>
+template <bool HIST, class G, class LK>
 __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, Lists* K, int h, double t,
                                             double base, int ob, int ib, const Slots& sl,
                                             int32_t* pendOut, int32_t* arrOut, int32_t* cout,
-                                            int32_t* coutCnt, int cap, int& err) {
+                                            int32_t* coutCnt, int cap, int ev, int& err) {
   const double rl = P.start[h] + base;
   P.base[h] = base;
   P.rel[h] = rl;
+  if constexpr (HIST) P.evr[h] = ev;
   if (rl <= t) {
     if (P.nbytes[h] == 0.0) {
       P.finish[h] = rl;
+      if constexpr (HIST) {
+        P.eva[h] = ev;
+        P.evd[h] = ev;
+      }
       const int s = g.add(coutCnt, 1);
       if (s < cap) cout[s] = h; else err = 1;
     } else {
-      activate(g, P, lk, K, h, t, sl, arrOut, ib, cap, err);
+      activate<HIST>(g, P, lk, K, h, t, sl, arrOut, ib, cap, ev, err);
     }
   } else {
     const int s = g.add(&K->pend[ob], 1);
@@ -1783,7 +1793,9 @@ __device__ __forceinline__ void release_one(G& g, const Params& P, LK& lk, Lists
   }
 }
 
-template <class G, class LK, class AS = NoAssist>
+// HIST: keep the rollback history (per-flow event indices, undo and event
+// records); the cluster kernel is built without it.
+template <bool HIST, class G, class LK, class AS = NoAssist>
 __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const int sc, SolveLds* S,
                                            Tally* tl, const FlowCache& fc, AS* as = nullptr) {
   ScenCtl* C = &P.ctl[sc];
@@ -1835,6 +1847,8 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
   int nPend = resume ? C->npend : C->n_pend0;
   int e = resume ? C->e : 0;  // event index: pend[e&1] is this event's pending list
   int q = resume ? C->q : 0;  // completion-list phase index (three rotating lists)
+  int64_t hp = resume ? C->hpos : 0;  // undo records written (rollback history)
+  const bool hist = HIST && P.hist != nullptr && C->hcap > 0;
   int status = ST_DONE;
   if (resume) {
     // link state of the active flows, rebuilt exactly (integer sums): every
@@ -1927,6 +1941,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       const double r = sl.rate[s];
       // the last byte leaves now; it arrives the path latency later
       P.finish[f] = P.lat ? tn + P.lat[f] : tn;
+      if constexpr (HIST) P.evd[f] = e;
       g.amin(&P.theta[P.comp[f]], (uint64_t)__double_as_longlong(r));
       const int64_t qv = (int64_t)__builtin_rint(r * P.scale);
       for (int k = P.poff[f]; k < P.poff[f + 1]; ++k) {
@@ -1977,9 +1992,13 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
               if (P.nbytes[f] == 0.0) {
                 pr[0] = true;
                 P.finish[f] = rl;
+                if constexpr (HIST) {
+                  P.eva[f] = e;
+                  P.evd[f] = e;
+                }
                 if (P.soff[f + 1] > P.soff[f]) g.store(&K->succ_flag[ib], 1);
               } else {
-                activate(g, P, lk, K, f, tn, sl, arrs, ib, cap, err);
+                activate<HIST>(g, P, lk, K, f, tn, sl, arrs, ib, cap, e, err);
               }
             } else {
               pr[1] = true;
@@ -2042,14 +2061,14 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
           if (g.add(&P.cnt[h], -1) == 1) {
             const double b = __longlong_as_double((long long)__hip_atomic_load(
                 reinterpret_cast<uint64_t*>(&P.base[h]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-            release_one(g, P, lk, K, h, t, b, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, err);
+            release_one<HIST>(g, P, lk, K, h, t, b, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, e, err);
           }
         });
       } else {
         // arrival = last byte: the last predecessor to finish is the latest
         for_succ([&](int, int h) {
           if (g.add(&P.cnt[h], -1) == 1)
-            release_one(g, P, lk, K, h, t, t, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, err);
+            release_one<HIST>(g, P, lk, K, h, t, t, ob, ib, sl, pendOut, arrs, cout, coutCnt, cap, e, err);
         });
       }
       if (err) g.store(&K->fault, 2);
@@ -2109,6 +2128,16 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
               if (slot < cap) {
                 arrs[slot] = x.f;
                 arrSlot[slot] = x.k;
+                if (HIST && hist) {
+                  // undo record: the flow's values before this event re-solves it
+                  HistUndo u;
+                  u.f = x.f;
+                  u.ev = e;
+                  u.rem = P.rem[x.f];
+                  u.tref = P.tref[x.f];
+                  u.rate = x.a;
+                  P.hist[C->hbase + (hp + slot) % C->hcap] = u;
+                }
               } else {
                 err = 1;
               }
@@ -2120,6 +2149,7 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       for (int c = C->c0 + tid; c < C->c0 + C->nc; c += T) P.theta[c] = INF_BITS;
       const int nSel = g.load(&K->sel);
       if (threadIdx.x == 0) tl->sel += nSel;
+      if constexpr (HIST) hp += nSel;
       int rc = 0;
       if (nSel > 0) {
         const Resel rs{sl, arrSlot, slots0, t};
@@ -2243,6 +2273,20 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
       }
     }
     nPend = pNew;
+    if (HIST && hist && tid == 0) {
+      HistEv r;
+      r.t = t;
+      r.hpos = hp;
+      r.solves = tl->solves;
+      r.rounds = tl->rounds;
+      r.flows_swept = tl->fsw;
+      r.active_swept = tl->asw;
+      r.pending_swept = tl->psw;
+      r.reselected = tl->sel;
+      r.wide_solves = tl->wide;
+      r.assisted = tl->asst;
+      P.hev[C->ebase + (int64_t)e % C->ecap] = r;
+    }
     e += 1;
   }
   if (tid == 0 && !resume) C->incidences_swept = 0;
@@ -2268,6 +2312,8 @@ __device__ __forceinline__ void event_loop(G& g, const Params& P, LK& lk, const 
     C->wide_solves = tl->wide;
     C->assisted = tl->asst;
     C->links_swept = (resume ? C->links_swept : 0) + g.load(&K->lsw);
+    if constexpr (HIST) C->hpos = hp;
+    C->launch_events = events - events0;
     C->status = status;
     for (int k = 0; k < 8; ++k) C->ticks[k] = (int64_t)tl->clk[k];
   }
@@ -2339,10 +2385,10 @@ __global__ __launch_bounds__(NT) void netsim_block_kernel(Params P) {
       solve_only(g, P, sc, nullptr, &tally, fc);
     } else if (in_lds) {
       LinksShared lk(pool, C->l0, nl, P.inv_scale);
-      event_loop(g, P, lk, sc, nullptr, &tally, fc);
+      event_loop<true>(g, P, lk, sc, nullptr, &tally, fc);
     } else {
       LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
-      event_loop(g, P, lk, sc, nullptr, &tally, fc);
+      event_loop<true>(g, P, lk, sc, nullptr, &tally, fc);
     }
     __syncthreads();
   }
@@ -2359,7 +2405,7 @@ __global__ __launch_bounds__(1024) void netsim_grid_kernel(Params P) {
   LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
   const FlowCache none{nullptr, nullptr, 0};
   for (int sc = 0; sc < P.num_scen; ++sc) {
-    if (P.mode == 0) event_loop(g, P, lk, sc, &S, &tally, none);
+    if (P.mode == 0) event_loop<true>(g, P, lk, sc, &S, &tally, none);
     else solve_only(g, P, sc, &S, &tally, none);
     g.sync();
   }
@@ -2455,10 +2501,10 @@ __global__ __launch_bounds__(1024) void netsim_cluster_kernel(Params P) {
                        reinterpret_cast<int32_t*>(pool + used + 16 * ncache), ncache};
     if (in_lds) {
       LinksShared lk(pool, C->l0, nl, P.inv_scale);
-      event_loop(g, P, lk, sc, nullptr, &tally, fc, &as);
+      event_loop<false>(g, P, lk, sc, nullptr, &tally, fc, &as);
     } else {
       LinksGlobal lk{P.lst, P.nact, P.fl, P.inv_scale};
-      event_loop(g, P, lk, sc, nullptr, &tally, fc, &as);
+      event_loop<false>(g, P, lk, sc, nullptr, &tally, fc, &as);
     }
     __syncthreads();
   }

@@ -72,6 +72,8 @@ struct netsim {
   std::vector<int32_t> h_lfoff;       // exact mode: link-major incidence offsets
   double scale = 1.0;
   void* d_block = nullptr;            // one allocation holding every device array
+  void* d_hist = nullptr;             // rollback history (options.history_mb; exact mode: none)
+  bool hist_ok = false;               // every launch since t = 0 kept the history
   char* persist = nullptr;            // the persistent dynamic state inside it
   size_t persist_bytes = 0;
   bool has_state = false;             // the device holds a simulation position
@@ -538,6 +540,29 @@ netsim_status prepare(netsim_t* h) {
       }
     c.n_pend0 = np;
   }
+  // rollback history: 1/16 of it for event records, the rest for undo
+  // records, shared among the parts in proportion to their flows
+  size_t hist_bytes = 0;
+  if (h->opt.history_mb > 0 && !exact && F > 0) {
+    const size_t total = (size_t)h->opt.history_mb << 20;
+    const int64_t ev_total = (int64_t)(total / 16 / sizeof(netsim_dev::HistEv));
+    const int64_t un_total = (int64_t)((total - (size_t)ev_total * sizeof(netsim_dev::HistEv)) /
+                                       sizeof(netsim_dev::HistUndo));
+    int64_t hb = 0, eb = 0;
+    for (int32_t k = 0; k < NP; ++k) {
+      ScenCtl& c = ctl[(size_t)k];
+      const double share = (double)(c.f1 - c.f0) / (double)F;
+      c.hbase = hb;
+      // undo offsets within a part are 32-bit (history.hip)
+      c.hcap = std::min<int64_t>(std::max<int64_t>(1, (int64_t)((double)un_total * share)),
+                                 std::numeric_limits<int32_t>::max());
+      c.ebase = eb;
+      c.ecap = std::max<int64_t>(1, (int64_t)((double)ev_total * share));
+      hb += c.hcap;
+      eb += c.ecap;
+    }
+    hist_bytes = (size_t)hb * sizeof(netsim_dev::HistUndo) + (size_t)eb * sizeof(netsim_dev::HistEv);
+  }
   h->h_ctl0 = ctl;
   // one device allocation, carved into aligned arrays
   const size_t Fz = (size_t)std::max<int64_t>(F, 1), Lz = (size_t)std::max<int64_t>(ld, 1);
@@ -561,6 +586,9 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.rel, sizeof(double) * Fz},
       {(void**)&P.base, sizeof(double) * Fz},
       {(void**)&P.cnt, sizeof(int32_t) * Fz},
+      {(void**)&P.evr, sizeof(int32_t) * Fz},
+      {(void**)&P.eva, sizeof(int32_t) * Fz},
+      {(void**)&P.evd, sizeof(int32_t) * Fz},
       {(void**)&P.act0, sizeof(int32_t) * Fz},
       {(void**)&P.act1, sizeof(int32_t) * Fz},
       {(void**)&P.tau0, sizeof(double) * Fz},
@@ -621,6 +649,19 @@ netsim_status prepare(netsim_t* h) {
   }
   h->persist = (char*)P.rem;
   h->persist_bytes = (size_t)((char*)P.ctl - (char*)P.rem) + sizeof(ScenCtl) * (size_t)std::max<int32_t>(NP, 1);
+  if (hist_bytes > 0) {
+    he = hipMalloc(&h->d_hist, hist_bytes);
+    if (he != hipSuccess) {
+      (void)hipGetLastError();
+      h->d_hist = nullptr;
+      return fail(h, NETSIM_E_NOMEM, "hipMalloc of " + std::to_string(hist_bytes) +
+                                         " bytes for the rollback history failed");
+    }
+    int64_t hb = 0;
+    for (const ScenCtl& c : h->h_ctl0) hb += c.hcap;
+    P.hist = (netsim_dev::HistUndo*)h->d_hist;
+    P.hev = (netsim_dev::HistEv*)((char*)h->d_hist + (size_t)hb * sizeof(netsim_dev::HistUndo));
+  }
   struct Up { const void* src; const void* dst; size_t bytes; };
   const Up ups[] = {
       {poff.data(), P.poff, sizeof(int32_t) * (size_t)(F + 1)},
@@ -675,7 +716,11 @@ netsim_status reset_state(netsim_t* h, hipStream_t st) {
     he = hipMemcpyAsync(u.dst, u.src, u.bytes, hipMemcpyHostToDevice, st);
     if (he != hipSuccess) return hip_fail(h, he, "hipMemcpyAsync (reset)");
   }
+  h->hist_ok = P.hist != nullptr;
   he = hipMemsetAsync(P.nact, 0, sizeof(int32_t) * Lz, st);
+  // per-flow event indices: EV_NEVER, every byte 0x7F
+  for (int32_t* a : {P.evr, P.eva, P.evd})
+    if (he == hipSuccess) he = hipMemsetAsync(a, 0x7F, sizeof(int32_t) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.base, 0, sizeof(double) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.rate, 0, sizeof(double) * Fz, st);
   if (he == hipSuccess) he = hipMemsetAsync(P.bar, 0, sizeof(uint32_t) * netsim_dev::BAR_WORDS, st);
@@ -723,12 +768,15 @@ netsim_status launch(netsim_t* h, hipStream_t st, bool solve_only, float* ms, bo
       cus = 0;
     const int xcds = cus / kCusPerXcd;
     if (S == 1 && widest > 65536) exec = NETSIM_EXEC_GRID;
-    else if (!solve_only && S <= kMaxClustersPerXcd * xcds && widest > 16384) exec = NETSIM_EXEC_CLUSTER;
+    // (not with the rollback history, which the cluster kernel does not keep)
+    else if (!solve_only && S <= kMaxClustersPerXcd * xcds && widest > 16384 && h->opt.history_mb <= 0)
+      exec = NETSIM_EXEC_CLUSTER;
     else exec = NETSIM_EXEC_BLOCK;
   }
   if (exec == NETSIM_EXEC_CLUSTER && solve_only) exec = NETSIM_EXEC_BLOCK;
   if (h->opt.exact) exec = NETSIM_EXEC_EXACT;
   h->layout = exec;
+  if (!solve_only && (exec == NETSIM_EXEC_CLUSTER || exec == NETSIM_EXEC_EXACT)) h->hist_ok = false;
   // grid-barrier words and min-reduction slots start fresh in every launch
   // (a launch that continues a run must not see the last launch's counts)
   uint64_t inf_slots[8];
@@ -893,6 +941,7 @@ netsim_status simulate(netsim_t* h, hipStream_t st, bool resume, int64_t max_eve
     s.wide_solves += c.wide_solves;
     s.assisted_solves += c.assisted;
     s.links_swept += c.links_swept;
+    s.launch_events += c.launch_events;
     s.layout = h->layout;
     s.sim_time = std::max(s.sim_time, c.t);
     if (c.status != 0) s.complete = 0;
@@ -1023,7 +1072,8 @@ netsim_status restore_part(netsim_t* h, int32_t p, int k) {
     const char* src = (const char*)h->checkpoints[(size_t)k].dev;
     struct A { void* a; size_t z; };
     const A arrays[] = {{P.rem, 8}, {P.tref, 8}, {P.rate, 8}, {P.finish, 8}, {P.rel, 8}, {P.base, 8},
-                        {P.cnt, 4}, {P.act0, 4}, {P.act1, 4}, {P.tau0, 8}, {P.tau1, 8},
+                        {P.cnt, 4}, {P.evr, 4}, {P.eva, 4}, {P.evd, 4},
+                        {P.act0, 4}, {P.act1, 4}, {P.tau0, 8}, {P.tau1, 8},
                         {P.srate0, 8}, {P.srate1, 8}, {P.pend0, 4}, {P.pend1, 4}};
     for (const A& a : arrays) {
       const size_t off = (size_t)((char*)a.a - h->persist) + f0 * a.z;
@@ -1040,6 +1090,8 @@ netsim_status restore_part(netsim_t* h, int32_t p, int k) {
       if (he == hipSuccess) he = hipMemcpy(P.finish + f0, nan.data(), 8 * n, hipMemcpyHostToDevice);
       if (he == hipSuccess) he = hipMemcpy(P.base + f0, zero.data(), 8 * n, hipMemcpyHostToDevice);
       if (he == hipSuccess) he = hipMemcpy(P.rate + f0, zero.data(), 8 * n, hipMemcpyHostToDevice);
+      for (int32_t* a : {P.evr, P.eva, P.evd})
+        if (he == hipSuccess) he = hipMemset(a + f0, 0x7F, 4 * n);
     }
     if (he == hipSuccess) he = hipMemcpy(P.ctl + p, &c0, sizeof(ScenCtl), hipMemcpyHostToDevice);
   }
@@ -1048,6 +1100,61 @@ netsim_status restore_part(netsim_t* h, int32_t p, int k) {
     h->checkpoints[j].valid[(size_t)p] = 0;
   h->part_t[(size_t)p] = k >= 0 ? h->checkpoints[(size_t)k].t[(size_t)p]
                                 : -std::numeric_limits<double>::infinity();
+  return NETSIM_OK;
+}
+
+// Part p back to the end of its last event before `before` from the
+// rollback history (Section 4.2).  *done = false when the history cannot do
+// it (none, or its rings no longer hold every record since): nothing has
+// changed then.
+netsim_status history_rollback(netsim_t* h, int32_t p, double before, bool* done) {
+  *done = false;
+  const Params& P = h->prm;
+  if (!P.hist || !h->hist_ok) return NETSIM_OK;
+  ScenCtl c;
+  hipError_t he = hipMemcpy(&c, P.ctl + p, sizeof c, hipMemcpyDeviceToHost);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (control block)");
+  if (c.hcap <= 0 || c.ecap <= 0) return NETSIM_OK;
+  const int64_t E = c.started ? (int64_t)c.e : 0;  // events processed so far
+  const int64_t lo = std::max<int64_t>(0, E - c.ecap);  // oldest event still recorded
+  netsim_dev::HistEv rec{};
+  auto read = [&](int64_t e) {
+    return hipMemcpy(&rec, P.hev + c.ebase + e % c.ecap, sizeof rec, hipMemcpyDeviceToHost);
+  };
+  // first recorded event at or after `before` (event times increase)
+  int64_t a = lo, b = E;
+  while (a < b && he == hipSuccess) {
+    const int64_t m = a + (b - a) / 2;
+    he = read(m);
+    if (rec.t < before) a = m + 1; else b = m;
+  }
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (event record)");
+  const int64_t es = a - 1;  // the last event before `before`
+  if (es < lo) {
+    if (lo > 0) return NETSIM_OK;  // older than the ring holds
+    netsim_status rc = restore_part(h, p, -1);  // no event before it: t = 0
+    if (rc == NETSIM_OK) *done = true;
+    return rc;
+  }
+  he = read(es);
+  if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (event record)");
+  if (c.hpos - rec.hpos > c.hcap) return NETSIM_OK;  // undo records overwritten
+  const ScenCtl& c0 = h->h_ctl0[(size_t)p];
+  const int32_t f0 = c0.f0, f1 = c0.f1;
+  const size_t n = (size_t)(f1 - f0);
+  if (n > 0) {
+    he = hipMemcpy(P.unf0 + f0, h->h_cnt0.data() + f0, 4 * n, hipMemcpyHostToDevice);
+    if (he == hipSuccess) he = hipMemcpy(P.mf + f0, h->h_rel0.data() + f0, 8 * n, hipMemcpyHostToDevice);
+  }
+  if (he == hipSuccess)
+    he = netsim_dev::history_restore(P, p, f0, f1, c.hbase, c.hcap, (int32_t)es, rec, c.hpos, P.unf0 + f0,
+                                     P.mf + f0, P.arr + f0, P.bar, nullptr);
+  if (he == hipSuccess) he = hipStreamSynchronize(nullptr);
+  if (he != hipSuccess) return hip_fail(h, he, "rollback from the history");
+  for (auto& ck : h->checkpoints)
+    if (ck.t[(size_t)p] > rec.t) ck.valid[(size_t)p] = 0;
+  h->part_t[(size_t)p] = rec.t;
+  *done = true;
   return NETSIM_OK;
 }
 
@@ -1088,6 +1195,10 @@ netsim_status netsim_create(netsim_t** out, int32_t num_scenarios, const int64_t
   if (!h) return fail(nullptr, NETSIM_E_NOMEM, "create: out of memory");
   if (opt) h->opt = *opt;
   else netsim_default_options(&h->opt);
+  if (h->opt.history_mb < 0) {
+    delete h;
+    return fail(nullptr, NETSIM_E_INVALID, "create: history_mb must be >= 0");
+  }
   h->scen.resize((size_t)num_scenarios);
   for (int32_t s = 0; s < num_scenarios; ++s)
     h->scen[(size_t)s].cap.assign(capacity_Bps + link_off[s], capacity_Bps + link_off[s + 1]);
@@ -1104,6 +1215,10 @@ netsim_status netsim_create_topology(netsim_t** out, int32_t num_scenarios,
   if (!h) return fail(nullptr, NETSIM_E_NOMEM, "create_topology: out of memory");
   if (opt) h->opt = *opt;
   else netsim_default_options(&h->opt);
+  if (h->opt.history_mb < 0) {
+    delete h;
+    return fail(nullptr, NETSIM_E_INVALID, "create: history_mb must be >= 0");
+  }
   h->scen.resize((size_t)num_scenarios);
   for (int32_t s = 0; s < num_scenarios; ++s) {
     Scen& sc = h->scen[(size_t)s];
@@ -1785,8 +1900,13 @@ netsim_status netsim_update_start(netsim_t* h, int64_t id, double start) {
   // time rollback (Section 4.2): the part goes back to the latest state in
   // which the flow was not yet released and that precedes its new release
   const double before = released ? std::min(rel_old, rel_new) : rel_new;
-  netsim_status rc = restore_part(h, p, latest_checkpoint(h, p, before));
+  bool done = false;
+  netsim_status rc = history_rollback(h, p, before, &done);
   if (rc) return rc;
+  if (!done) {
+    rc = restore_part(h, p, latest_checkpoint(h, p, before));
+    if (rc) return rc;
+  }
   he = hipMemcpy(&cnt, P.cnt + d, sizeof(int32_t), hipMemcpyDeviceToHost);
   if (he != hipSuccess) return hip_fail(h, he, "hipMemcpy (flow state)");
   if (cnt == 0) {
@@ -2092,6 +2212,7 @@ void netsim_destroy(netsim_t* h) {
     (void)hipSetDevice(h->opt.device);
     drop_checkpoints(h);
     (void)hipFree(h->d_block);
+    if (h->d_hist) (void)hipFree(h->d_hist);
   }
   delete h;
 }

@@ -38,7 +38,7 @@ class netsim_options(ctypes.Structure):
                 ("max_rounds", ctypes.c_int32), ("block_threads", ctypes.c_int32),
                 ("debug", ctypes.c_int32), ("single_clock", ctypes.c_int32),
                 ("assist_min_flows", ctypes.c_int32), ("assist_helpers", ctypes.c_int32),
-                ("exact", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("exact", ctypes.c_int32), ("history_mb", ctypes.c_int32)]
 
 
 class netsim_topology(ctypes.Structure):
@@ -65,7 +65,8 @@ class netsim_stats(ctypes.Structure):
                 ("sim_time", ctypes.c_double), ("device_seconds", ctypes.c_double),
                 ("upload_seconds", ctypes.c_double), ("phase_seconds", ctypes.c_double * 8),
                 ("assisted_solves", ctypes.c_int64), ("layout", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("links_swept", ctypes.c_int64)]
+                ("reserved", ctypes.c_int32), ("links_swept", ctypes.c_int64),
+                ("launch_events", ctypes.c_int64)]
 
     def as_dict(self):
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
@@ -170,12 +171,12 @@ def netsim_default_options() -> netsim_options:
 
 def make_options(device=0, exec=EXEC_AUTO, max_events=0, until=math.inf, max_rounds=0,
                  block_threads=0, debug=0, single_clock=0, assist_min_flows=0,
-                 assist_helpers=0, exact=0) -> netsim_options:
+                 assist_helpers=0, exact=0, history_mb=0) -> netsim_options:
     o = netsim_default_options()
     o.device, o.exec, o.max_events, o.until = device, exec, max_events, until
     o.max_rounds, o.block_threads, o.debug = max_rounds, block_threads, debug
     o.single_clock, o.assist_min_flows, o.assist_helpers = single_clock, assist_min_flows, assist_helpers
-    o.exact = exact
+    o.exact, o.history_mb = exact, history_mb
     return o
 
 

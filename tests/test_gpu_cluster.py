@@ -167,6 +167,10 @@ def test_auto_picks_the_layout():
     assert st["layout"] == ns.EXEC_GRID and st["parts"] == 1
     _, st = pr.run_program(configs.c4(4), ns.make_options(exec=ns.EXEC_CLUSTER, until=1e-4))
     assert st["layout"] == ns.EXEC_CLUSTER
+    # the cluster kernel keeps no rollback history: with one, AUTO runs C4
+    # one workgroup per part
+    _, st = pr.run_program(configs.c4(4), ns.make_options(until=1e-4, history_mb=64))
+    assert st["layout"] == ns.EXEC_BLOCK and st["parts"] == 8
 
 
 def test_cluster_leader_solves_alone_when_helpers_leave():

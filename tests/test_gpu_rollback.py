@@ -226,3 +226,155 @@ def test_rollback_random_micro_batch():
         ref = _oracle(sc, {loc: v for (t, loc), v in upd.items() if t == s})
         assert _rel(got[a:a + ld.num_flows[s]], ref) < TOL, s
     assert not np.array_equal(got, base)
+
+
+def _advance_update_finish(program, x, new, history_mb, **opt):
+    """Advance to 30% and 60% of the horizon, move flow x's start, continue to
+    the end: the finish times and the events the continuation processed."""
+    ns, pr = _gpu()
+    ref_T = opt.pop("T")
+    ld = pr.load_program(program, ns.make_options(history_mb=history_mb, **opt))
+    try:
+        h = ld.handle
+        ns.netsim_advance(h, until=0.3 * ref_T)
+        ns.netsim_advance(h, until=0.6 * ref_T)
+        ns.netsim_update_start(h, x, new)
+        ns.netsim_advance(h)
+        st = ns.netsim_get_stats(h)
+        assert st["complete"] == 1
+        return ns.netsim_get_finish(h), st["launch_events"]
+    finally:
+        ld.close()
+
+
+@pytest.mark.parametrize("exec_", ["block", "grid", "cluster"])
+@pytest.mark.parametrize("with_deps,delta", [(True, 30e-6), (True, -1.0), (False, 25e-6)])
+def test_history_rollback_to_the_event_before(exec_, with_deps, delta):
+    """With the rollback history the part goes back to the end of its last
+    event before the changed release (not to the last checkpoint before it):
+    the result equals, bit for bit, a fresh run with the new start and the
+    rollback without history, and the continuation re-simulates no more
+    events than the one from the checkpoint (fewer when the release is not
+    at t = 0).  The cluster kernel keeps no history: there the rollback goes
+    to the checkpoint either way."""
+    ns, pr = _gpu()
+    _say(f"test_history_rollback exec={exec_} deps={with_deps} delta={delta}")
+    program = configs.c2(2, tp_reps=6)
+    sc = program.scenarios[0]
+    fs = oflows.expand(sc)
+    lay = _layout(ns, exec_)
+    ref = _fresh(program, {}, **lay)
+    T = float(np.nanmax(ref))
+    x = _pick(fs, ref, 0.2 * T, 0.4 * T, with_deps)
+    new = max(0.0, float(fs.start[x]) + delta)
+    if new == fs.start[x]:
+        new = float(fs.start[x]) + 5e-6
+    upd = {x: new}
+    got, ev_hist = _advance_update_finish(program, x, new, 64, T=T, **lay)
+    alt, ev_ckpt = _advance_update_finish(program, x, new, 0, T=T, **lay)
+    want = _fresh(program, upd, **lay)
+    assert np.array_equal(got, want)
+    assert np.array_equal(alt, want)
+    assert not np.array_equal(want, ref)
+    if exec_ == "cluster":
+        assert ev_hist == ev_ckpt
+    else:
+        assert ev_hist <= ev_ckpt
+        if delta > 0:
+            assert ev_hist < ev_ckpt
+    _say("  continuation events: history", ev_hist, "checkpoint", ev_ckpt)
+    assert _rel(got, _oracle(sc, upd)) < TOL
+
+
+def test_history_several_updates_and_gc():
+    """Several updates in a row (a pending flow, then finished flows after
+    further advances) with the rollback history, garbage collection between
+    them: the run with all of them, bit for bit."""
+    ns, pr = _gpu()
+    _say("test_history_several_updates_and_gc")
+    program = configs.c2(2, tp_reps=6)
+    sc = program.scenarios[0]
+    fs = oflows.expand(sc)
+    ref = _fresh(program, {})
+    T = float(np.nanmax(ref))
+    late = _pick(fs, ref, 0.85 * T, 0.95 * T, True)
+    early = _pick(fs, ref, 0.5 * T, 0.7 * T, False)
+    other = _pick(fs, ref, 0.75 * T, 0.8 * T, True)
+    upd = {}
+    ld = pr.load_program(program, ns.make_options(history_mb=64))
+    try:
+        h = ld.handle
+        for frac in (0.1, 0.2, 0.3, 0.4):
+            ns.netsim_advance(h, until=frac * T)
+        upd[late] = float(fs.start[late]) + 40e-6
+        ns.netsim_update_start(h, late, upd[late])
+        ns.netsim_gc(h, 0.35 * T)
+        ns.netsim_advance(h, until=0.9 * T)
+        upd[early] = float(fs.start[early]) + 10e-6
+        ns.netsim_update_start(h, early, upd[early])
+        ns.netsim_advance(h, until=0.95 * T)
+        upd[other] = float(fs.start[other]) + 15e-6
+        ns.netsim_update_start(h, other, upd[other])
+        ns.netsim_advance(h)
+        got = ns.netsim_get_finish(h)
+    finally:
+        ld.close()
+    want = _fresh(program, upd)
+    assert np.array_equal(got, want)
+    assert _rel(got, _oracle(sc, upd)) < TOL
+
+
+def test_history_ring_too_small_falls_back_to_checkpoints():
+    """A history of 1 MiB holds only the last few hundred events of C2: a
+    rollback further back goes to the latest checkpoint instead, with the
+    same result."""
+    ns, pr = _gpu()
+    _say("test_history_ring_too_small")
+    program = configs.c2(2, tp_reps=6)
+    sc = program.scenarios[0]
+    fs = oflows.expand(sc)
+    ref = _fresh(program, {})
+    T = float(np.nanmax(ref))
+    x = _pick(fs, ref, 0.2 * T, 0.4 * T, True)
+    new = float(fs.start[x]) + 30e-6
+    got, ev_small = _advance_update_finish(program, x, new, 1, T=T)
+    _, ev_ckpt = _advance_update_finish(program, x, new, 0, T=T)
+    assert np.array_equal(got, _fresh(program, {x: new}))
+    assert ev_small == ev_ckpt
+
+
+def test_history_rollback_random_micro_batch():
+    """100 random dynamic micro cases in one batched handle with the rollback
+    history: one flow's start moved in every case after half the horizon."""
+    ns, pr = _gpu()
+    _say("test_history_rollback_random_micro_batch")
+    scs = []
+    for seed in range(100):
+        scs += micro.random_dynamic(500 + seed, integer_caps=(seed % 2 == 0)).scenarios
+    program = Program("micro-rollback", scs)
+    base = _fresh(program, {}, exec=ns.EXEC_BLOCK)
+    ld = pr.load_program(program, ns.make_options(exec=ns.EXEC_BLOCK, history_mb=16))
+    try:
+        h = ld.handle
+        ms = np.array([np.nanmax(base[a:a + n]) for a, n in zip(ld.first_flow, ld.num_flows)])
+        half = 0.5 * float(np.median(ms))
+        rng = np.random.default_rng(11)
+        upd = {}
+        ns.netsim_advance(h, until=half)
+        for s, sc in enumerate(scs):
+            fs = oflows.expand(sc)
+            loc = int(rng.integers(fs.F))
+            upd[(s, loc)] = float(fs.start[loc]) + float(rng.uniform(0, 2.0)) * ms[s] / 10
+            ns.netsim_update_start(h, ld.first_flow[s] + loc, upd[(s, loc)])
+        ns.netsim_advance(h)
+        got = ns.netsim_get_finish(h)
+    finally:
+        ld.close()
+    want = _fresh(program, {ld.first_flow[s] + loc: v for (s, loc), v in upd.items()},
+                  exec=ns.EXEC_BLOCK)
+    assert np.array_equal(got, want)
+    for s, sc in enumerate(scs):
+        a = ld.first_flow[s]
+        ref = _oracle(sc, {loc: v for (t, loc), v in upd.items() if t == s})
+        assert _rel(got[a:a + ld.num_flows[s]], ref) < TOL, s
+    assert not np.array_equal(got, base)

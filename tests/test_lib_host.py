@@ -257,3 +257,11 @@ def test_last_exits_of_a_batch_and_before_any():
         assert list(ns.netsim_last_exits(h)) == [0, 1, 2]
     finally:
         ns.netsim_destroy(h)
+
+
+def test_negative_history_is_refused():
+    opt = ns.make_options(history_mb=-1)
+    with pytest.raises(ns.NetsimError) as ei:
+        ns.netsim_create(np.array([0, 1], np.int64), np.array([1.0]), opt)
+    assert ei.value.status == ns.E_INVALID
+    assert "history_mb" in str(ei.value)
