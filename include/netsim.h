@@ -143,9 +143,13 @@ typedef struct {
                                 in proportion to their flows.  With it,
                                 netsim_update_start returns a part to the end of
                                 its last event before the changed release, as
-                                long as the ring still holds every record since;
-                                otherwise (and with 0, the default, or in exact
-                                mode) to the latest checkpoint before it        */
+                                long as the ring still holds every record since
+                                and every launch since t = 0 kept it; otherwise
+                                (and with 0, the default) to the latest
+                                checkpoint before it.  The cluster layout and
+                                exact mode keep no history; with history_mb > 0
+                                NETSIM_EXEC_AUTO uses the block layout where it
+                                would pick the cluster one                      */
 } netsim_options;
 
 /*
@@ -487,10 +491,12 @@ netsim_status netsim_advance(netsim_t* h, double until, int64_t max_events, void
  * Sets flow id's start (its absolute start when it has no dependencies, else
  * its lag after the last of them) to `start` (finite, >= 0).  If the
  * simulation of the flow's part has already processed its old or its new
- * release time, the part is rolled back to the latest checkpoint in which
- * the flow was not yet released and whose last event precedes the new
- * release (t = 0 if there is none), and the checkpoints after it no longer
- * apply to that part; other parts keep their position.  The next
+ * release time, the part is rolled back (Section 4.2, time rollback): with
+ * the rollback history (options.history_mb) to the end of its last event
+ * before the earlier of the two releases, else to the latest checkpoint in
+ * which the flow was not yet released and whose last event precedes the new
+ * release (t = 0 if there is none); checkpoints after that point no longer
+ * apply to the part; other parts keep their position.  The next
  * netsim_advance (or netsim_run, from t = 0) re-simulates with the new
  * start, so completion times that depended on the flow change accordingly
  * (through the dependency graph).  Valid before the first run as well.
