@@ -172,3 +172,62 @@ def test_latency_pieces_and_rollback(exec_):
     finally:
         ld.close()
     assert np.array_equal(got, fresh({x: new}))
+
+
+@pytest.mark.parametrize("exec_", ["block", "grid"])
+def test_latency_rollback_from_history(exec_):
+    """With latencies and the rollback history: starts of flows with and
+    without predecessors moved after the simulation passed them (each part
+    goes back to its last event before the change, rebuilding the waiting
+    flows' counts and, with latency, their bases from the arrivals of the
+    predecessors finished by then); then advancing equals, bit for bit, a
+    fresh run with those starts, and the rollback re-simulates fewer events
+    than the one from the latest checkpoint."""
+    ns, pr, _ = _gpu()
+    _say(f"test_latency_rollback_from_history exec={exec_}")
+    program = Program("next4", _scenarios()[:2])
+    ex = _layout(ns, exec_)
+
+    def fresh(updates):
+        ld = pr.load_program(program, ns.make_options(**ex))
+        try:
+            for fid, s in updates.items():
+                ns.netsim_update_start(ld.handle, fid, s)
+            ns.netsim_run(ld.handle)
+            return ns.netsim_get_finish(ld.handle)
+        finally:
+            ld.close()
+
+    ref = fresh({})
+    T = float(np.nanmax(ref))
+
+    def rolled(history_mb):
+        ld = pr.load_program(program, ns.make_options(history_mb=history_mb, **ex))
+        try:
+            h = ld.handle
+            ns.netsim_advance(h, until=0.3 * T)
+            ns.netsim_advance(h)
+            ex_ = ns.netsim_export_flows(h)
+            deps = ex_["dep_off"][1:] > ex_["dep_off"][:-1]
+            upd = {}
+            for want_deps, frac, d in ((True, 0.6, 2e-5), (False, 0.45, 3e-5)):
+                # the flow of that kind finishing nearest to frac of the horizon
+                c = np.nonzero((ex_["nbytes"] > 0) & (deps == want_deps))[0]
+                assert len(c), want_deps
+                x = int(c[np.argmin(np.abs(ref[c] - frac * T))])
+                upd[x] = float(ex_["start"][x]) + d
+                ns.netsim_update_start(h, x, upd[x])
+            ns.netsim_advance(h)
+            return ns.netsim_get_finish(h), ns.netsim_get_stats(h)["launch_events"], upd
+        finally:
+            ld.close()
+
+    got, ev_hist, upd = rolled(64)
+    alt, ev_ckpt, upd2 = rolled(0)
+    assert upd == upd2
+    want = fresh(upd)
+    assert np.array_equal(got, want)
+    assert np.array_equal(alt, want)
+    assert not np.array_equal(want, ref)
+    assert ev_hist < ev_ckpt
+    _say("  continuation events: history", ev_hist, "checkpoint", ev_ckpt)

@@ -148,3 +148,43 @@ def test_compute_duration_change_rolls_back(exec_):
     assert np.sum(got != before) > 0
     ref = otl.simulate(tr2)
     assert _rel(got, ref.finish) < TOL
+
+
+@pytest.mark.parametrize("exec_", ["block", "grid"])
+def test_compute_duration_change_rolls_back_from_history(exec_):
+    """The same with tree all-reduce, link latencies and the rollback
+    history: the part returns to its last event before the computation's
+    new end instead of a checkpoint; the result equals, bit for bit, a run
+    of the trace with the right duration from the start, and the oracle's
+    timeline of that trace."""
+    import copy
+    ns, ptr = _gpu()
+    _say(f"test_compute_duration_change_rolls_back_from_history exec={exec_}")
+    tr = training_step(seed=9, tp=4, pp=2, dp=2, microbatches=3, layers=2, allreduce="tree",
+                       fabric_latency_s=1e-6, nvlink_latency_s=3e-7)
+    ex = _layout(ns, exec_)
+    computes = [k for k, op in enumerate(tr.ops) if type(op).__name__ == "Compute"]
+    k = computes[len(computes) // 2]
+    new_d = tr.ops[k].duration + 3e-4
+    ld = ptr.load_trace(tr, ns.make_options(history_mb=32, **ex))
+    try:
+        h = ld.handle
+        ns.netsim_advance(h)
+        before = ns.netsim_get_finish(h)
+        x = int(ld.done[k][0])
+        assert np.isfinite(before[x])
+        ns.netsim_update_start(h, x, new_d)
+        ns.netsim_advance(h)
+        got = ns.netsim_get_finish(h)
+        resim = ns.netsim_get_stats(h)["launch_events"]
+        total = ns.netsim_get_stats(h)["events"]
+    finally:
+        ld.close()
+    tr2 = copy.deepcopy(tr)
+    tr2.ops[k].duration = new_d
+    fin2, _, _, _ = ptr.run_trace(tr2, ns.make_options(**ex))
+    assert np.array_equal(got, fin2)
+    assert np.sum(got != before) > 0
+    assert 0 < resim < total  # from the event before the change, not from t = 0
+    ref = otl.simulate(tr2)
+    assert _rel(got, ref.finish) < TOL
