@@ -311,3 +311,26 @@ def test_formal_release_is_bit_identical(case):
         assert sa[k] == sb[k], k
     assert sb["assisted_solves"] > 0
     _say("  drain s", sa["device_seconds"], "formal release s", sb["device_seconds"])
+
+
+@pytest.mark.parametrize("assist_min", [1, 256])
+@pytest.mark.parametrize("single_clock", [0, 1])
+def test_cluster_random_micro_batch(assist_min, single_clock):
+    """100 random dynamic micro cases (random fabrics, releases,
+    dependencies, zero-byte flows) in one batched handle: the cluster layout,
+    with every re-solve handed to the helpers or with the leaders solving
+    what is smaller than 256 flows, gives the block layout's bits."""
+    ns, pr = _gpu()
+    _say(f"test_cluster_random_micro_batch assist_min={assist_min} single_clock={single_clock}")
+    scs = []
+    for seed in range(100):
+        scs += micro.random_dynamic(900 + seed, integer_caps=(seed % 3 == 0)).scenarios
+    program = Program("micro-cluster", scs)
+    a, sa = pr.run_program(program, ns.make_options(exec=ns.EXEC_BLOCK, single_clock=single_clock))
+    b, sb = pr.run_program(program, ns.make_options(exec=ns.EXEC_CLUSTER, assist_min_flows=assist_min,
+                                                    single_clock=single_clock))
+    assert sb["layout"] == ns.EXEC_CLUSTER
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    assert sa["events"] == sb["events"] and sa["solves"] == sb["solves"]
+    if assist_min == 1:
+        assert sb["assisted_solves"] > 0
