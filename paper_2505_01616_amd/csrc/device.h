@@ -113,6 +113,7 @@ struct XGridHead {
   int32_t ublocks, useg;   // freezing sweep: workgroups, entries per segment
   int32_t lblocks, lseg;   // link pass: workgroups, entries per segment
   unsigned long long levels, fsw;  // iterations; flows swept
+  double sstar[2];         // level minimum, by parity (bottleneck pass -> freezing sweep)
 };
 struct XGrid : XGridHead {
   int32_t ucnt[2][XG_MAX_BLOCKS];  // unfrozen flows per segment, by level parity
@@ -195,8 +196,7 @@ struct Params {
   const int32_t* lfchunk;  // [nnz/256 + 1]
   const uint64_t* lfhead;  // [(nnz + 256)/64 + 1] bit e: entry e starts a link (or e >= nnz)
   uint32_t* xmask;         // [F/32 + 1] bit f: flow f is active in the wide exact solve
-  void* spare;             // unused: keeps the layout of the kernel arguments (and so
-                           // the compiled kernels) as verified and profiled
+  uint8_t* xfz;            // [L] 1: the link is a bottleneck of the current level
   XGrid* xgrid;            // counters of a wide exact solve
   int32_t exact_lds_bytes; // dynamic shared memory of the exact kernel (link state
                            // of a part with at most exact_lds_bytes / 24 links)

@@ -630,6 +630,7 @@ netsim_status prepare(netsim_t* h) {
       {(void**)&P.lfchunk, sizeof(int32_t) * (exact ? lfchunk.size() : 1)},
       {(void**)&P.lfhead, sizeof(uint64_t) * (exact ? lfhead.size() : 1)},
       {(void**)&P.xmask, sizeof(uint32_t) * (exact ? Fz / 32 + 8 : 1)},  // +8: 16-byte reads past the end
+      {(void**)&P.xfz, XL},
       {(void**)&P.xgrid, sizeof(netsim_dev::XGrid)},
   };
   size_t total = 0;

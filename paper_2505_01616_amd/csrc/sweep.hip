@@ -13,11 +13,12 @@
 //          that still carry unfrozen flows, and the level minimum s*
 //          (wave shuffles, then one value per wave in shared memory, then one
 //          value per workgroup, which the freezing sweep's workgroups reduce);
-//   freeze (per level)   -- the level minimum s* over those values, then a
-//          coalesced sweep of the unfrozen flows' path records: a flow
-//          crossing a bottleneck link (s_l <= s* * THR, THR = 1 + 1e-12)
-//          gets rate s* and adds 1 to k_l of each of its links; the others
-//          are kept for the next level.
+//   bottlenecks (per level) -- the level minimum s* and one byte per live
+//          link: s_l <= s* * THR (THR = 1 + 1e-12), the freeze mask;
+//   freeze (per level)   -- coalesced sweep of the unfrozen flows' path
+//          records: a flow crossing a bottleneck link gets rate s* and adds 1
+//          to k_l of each of its links; the others are kept for the next
+//          level.
 // Both lists are kept in per-workgroup segments (workgroup b of a sweep owns
 // its slice of the list and a count), so compaction uses shared-memory
 // counters only: no workgroup waits on an atomic in global memory.
@@ -313,20 +314,62 @@ __global__ __launch_bounds__(256) void exact_links_kernel(Params P, int l0, int 
   }
 }
 
-// Level j, freezing sweep: workgroup b takes the level minimum s* over the
-// link pass's per-workgroup minima, then its segment of the unfrozen flows
-// (path records: six part-local 16-bit link ids, 0xFFFF = none; or the path
-// CSR), freezes every flow crossing a bottleneck link (s_l <= s* * THR, its
-// share from the link pass) at rate s* and keeps the others in its segment
-// of the other list.  A level minimum that is not a positive finite number
-// stops the solve (fault).
+// Level j, bottlenecks: the level minimum s* (over the link pass's
+// per-workgroup minima; workgroup 0 records it for the freezing sweep) and,
+// for each live link of the workgroup's segment, one byte: s_l <= s* * THR.
+// The freezing sweep reads these bytes (a table small enough to stay in each
+// compute unit's L1) instead of gathering 8-byte shares.
+__global__ __launch_bounds__(256) void exact_bottleneck_kernel(Params P, int l0, int j, XGrid* g) {
+  __shared__ double smin[4];
+  if (g->done || g->fault) return;
+  const int b = blockIdx.x, seg = g->lseg, tid = threadIdx.x;
+  const int n_in = g->lcnt[(j + 1) & 1][b];  // the live links the link pass kept
+  const int32_t* lv = ((j & 1) ? P.xlive0 : P.xlive1) + l0 + b * seg;
+  int l = -1;
+  double sv = 0.0;
+  if (tid < n_in) {
+    l = lv[tid];
+    sv = P.xs[l];
+  }
+  double m = GINF;
+  for (int q = tid; q < (int)gridDim.x; q += blockDim.x) {
+    const double v = g->bmin[j & 1][q];
+    m = v < m ? v : m;
+  }
+  m = gwave_min(m);
+  if ((tid & 63) == 0) smin[tid >> 6] = m;
+  __syncthreads();
+  double s = smin[0];
+  for (int w = 1; w < 4; ++w) s = smin[w] < s ? smin[w] : s;
+  if (!(s > 0.0) || !(s < GINF)) {
+    if (first_thread()) g->fault = 1;
+    return;
+  }
+  if (first_thread()) g->sstar[j & 1] = s;
+  const double thr = s * GTHR;
+  for (int i0 = 0; i0 < n_in; i0 += blockDim.x) {
+    const int i = i0 + tid;
+    if (i < n_in) {
+      if (i0 > 0) {
+        l = lv[i];
+        sv = P.xs[l];
+      }
+      P.xfz[l] = sv <= thr ? 1 : 0;
+    }
+  }
+}
+
+// Level j, freezing sweep: workgroup b takes its segment of the unfrozen
+// flows (path records: six part-local 16-bit link ids, 0xFFFF = none; or
+// the path CSR), freezes every flow crossing a bottleneck link (its byte from
+// the bottleneck pass) at rate s* and keeps the others in its segment of the
+// other list.
 template <bool REC>
 __global__ __launch_bounds__(256) void exact_freeze_kernel(Params P, int l0, int f0, int n0, int j,
                                                            XGrid* g, unsigned long long* stamps) {
   if (stamps && threadIdx.x == 0) stamps[2 * blockIdx.x] = wall_clock64();
   __shared__ unsigned long long inc_sum;
   __shared__ int kept;
-  __shared__ double smin[4];
   if (g->done || g->fault) return;
   const int b = blockIdx.x;
   int seg, n_in;
@@ -349,26 +392,13 @@ __global__ __launch_bounds__(256) void exact_freeze_kernel(Params P, int l0, int
     f = uin[threadIdx.x];
     if constexpr (REC) rec = P.path16[f];
   }
-  // the level minimum: over the link pass's per-workgroup minima
-  double m = GINF;
-  for (int q = threadIdx.x; q < g->lblocks; q += blockDim.x) {
-    const double v = g->bmin[j & 1][q];
-    m = v < m ? v : m;
-  }
-  m = gwave_min(m);
-  if ((threadIdx.x & 63) == 0) smin[threadIdx.x >> 6] = m;
+  // the level minimum the bottleneck pass recorded
+  const double s = g->sstar[j & 1];
   if (threadIdx.x == 0) {
     inc_sum = 0;
     kept = 0;
   }
   __syncthreads();
-  double s = smin[0];
-  for (int w = 1; w < 4; ++w) s = smin[w] < s ? smin[w] : s;
-  if (!(s > 0.0) || !(s < GINF)) {
-    if (first_thread()) g->fault = 1;
-    return;
-  }
-  const double thr = s * GTHR;
   if (first_thread()) g->levels += 1;
   unsigned long long inc = 0;
   for (int i0 = 0; i0 < n_in; i0 += blockDim.x) {
@@ -388,13 +418,13 @@ __global__ __launch_bounds__(256) void exact_freeze_kernel(Params P, int l0, int
           const uint32_t id = (w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu;
           if (id != 0xFFFFu) lv[deg++] = l0 + (int)id;
         }
-        for (int q = 0; q < deg; ++q) fz |= P.xs[lv[q]] <= thr;
+        for (int q = 0; q < deg; ++q) fz |= P.xfz[lv[q]] != 0;
         inc += (unsigned long long)deg;
         if (fz)
           for (int q = 0; q < deg; ++q) atomicAdd(&P.xk[lv[q]], 1);
       } else {
         const int e0 = P.poff[f], e1 = P.poff[f + 1];
-        for (int e = e0; e < e1; ++e) fz |= P.xs[P.plink[e]] <= thr;
+        for (int e = e0; e < e1; ++e) fz |= P.xfz[P.plink[e]] != 0;
         inc += (unsigned long long)(e1 - e0);
         if (fz)
           for (int e = e0; e < e1; ++e) atomicAdd(&P.xk[P.plink[e]], 1);
@@ -461,6 +491,7 @@ hipError_t grid_solve_links(const Params& P, const ScenCtl& C, int j, hipStream_
   int blocks, seg;
   segments(C.l1 - C.l0, &blocks, &seg);
   hipLaunchKernelGGL(exact_links_kernel, dim3(blocks), dim3(256), 0, s, P, C.l0, C.l1, j, P.xgrid);
+  hipLaunchKernelGGL(exact_bottleneck_kernel, dim3(blocks), dim3(256), 0, s, P, C.l0, j, P.xgrid);
   return hipGetLastError();
 }
 
