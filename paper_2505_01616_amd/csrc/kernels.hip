@@ -599,7 +599,7 @@ __device__ __forceinline__ bool in_range(int f, int f0, int cap) {
 // Per link: residual capacity R (fixed point), unfrozen flows n, active flows
 // nact and a "blocked" stamp: a link is blocked in a freezing round iff its
 // stamp equals that round's number, so flags never need clearing (round
-// numbers keep growing through a part's solves; see next_rounds).  Two homes
+// numbers keep growing through a part's solves; see first_round).  Two homes
 // for the state, with one interface taking device link ids:
 //   LinksGlobal - global memory; any group (the whole grid, or a workgroup
 //                 on a part too large for shared memory);
